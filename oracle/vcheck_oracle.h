@@ -1,0 +1,97 @@
+/*
+ * vcheck_oracle.h -- CPU oracle for candidate-vs-reference validation.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library. The product path never
+ * calls it, and this oracle shares no code, header, table or helper with the
+ * HIP implementation.
+ *
+ * What it computes (one plain loop per case, flat row-major index order, all
+ * floating point in IEEE binary64 with round-to-nearest-even, no fused
+ * multiply-add):
+ *
+ *   Validate(K, R, T, tau) of the problem formulation (Sec. 3.2, Eq. 1 and the
+ *   conditions after it): every element of a candidate output is compared with
+ *   the reference output under the tolerance gate |c - r| <= atol + rtol*|r|,
+ *   together with the numerical-deviation metrics that the same section lists
+ *   as diagnostic evidence (counts, NaN/Inf, max abs/rel error, error sums),
+ *   the localization data of Sec. 4.2 (per-tile mismatch map, first failing
+ *   indices), output-level degenerate-output detectors for the integrity
+ *   hazards of Sec. 1 and Sec. 4.3, and the per-case pass/fail and suite match
+ *   rate of the full-coverage evaluation (Sec. 4.3, Sec. S3.4).
+ *
+ * Parity status: every output of this oracle is pinned by the CPU test suite
+ * (library routines, closed forms of the synthetic workloads, invariants and
+ * hand-built boundary cases); see the pin list in the test module header.
+ */
+#ifndef VCHECK_ORACLE_H
+#define VCHECK_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORC_F32 = 0, ORC_F16 = 1, ORC_BF16 = 2 };
+
+enum {
+  ORC_FLAG_ALL_ZERO = 1u << 0,
+  ORC_FLAG_CONSTANT = 1u << 1,
+  ORC_FLAG_INPUT_COPY = 1u << 2,
+  ORC_FLAG_LOWPREC_BF16 = 1u << 3,
+  ORC_FLAG_LOWPREC_FP16 = 1u << 4
+};
+
+typedef struct orc_stats {
+  uint64_t numel;
+  uint64_t mismatches; /* at the primary tolerance pair */
+  uint64_t nan_cand, inf_cand, nan_ref, inf_ref;
+  uint64_t n_finite, n_rel, n_rel_undef;
+  double max_abs;
+  int64_t argmax_abs;
+  double max_rel;
+  int64_t argmax_rel;
+  double sum_abs, sum_rel;
+} orc_stats;
+
+typedef struct orc_integrity {
+  uint64_t zero_cand, zero_ref, eqfirst_cand, eqfirst_ref;
+  uint64_t bf16rep_cand, bf16rep_ref, fp16rep_cand, fp16rep_ref;
+  uint32_t flags;
+  int32_t copy_input;
+  uint32_t cand_eq_input_mask, ref_eq_input_mask;
+  uint32_t cand_eq_ref;
+  uint32_t reserved;
+} orc_integrity;
+
+/* Decode n elements of the given storage type to binary64 (exact). */
+void orc_decode(int32_t dtype, const void *src, int64_t n, double *dst);
+
+/* Validate one case. cand/ref hold rows*cols elements of `dtype`, row-major.
+ * mismatches[n_tols] receives the mismatch count of every tolerance pair.
+ * tile_map (nullable) receives ceil(rows/tile_h)*ceil(cols/tile_w) counters
+ * and is zeroed first; first_k (nullable) receives k indices, -1 padded.
+ * integ (nullable) enables the degenerate-output detectors; inputs[j] is the
+ * j-th operator input (input_dtype[j], input_numel[j]). Returns 0, or -1 on
+ * an argument the oracle cannot evaluate. */
+int32_t orc_validate(int32_t dtype, const void *cand, const void *ref, int64_t rows,
+                     int64_t cols, int32_t n_tols, const double *atol, const double *rtol,
+                     const int32_t *equal_nan, int32_t primary, uint64_t *mismatches,
+                     orc_stats *st, int32_t tile_h, int32_t tile_w, uint32_t *tile_map,
+                     int32_t k, int64_t *first_k, int32_t n_inputs,
+                     const void *const *inputs, const int32_t *input_dtype,
+                     const int64_t *input_numel, orc_integrity *integ);
+
+/* Suite verdict over n_cases x n_tols mismatch counts (case-major).
+ * status[c] < 0 marks a case that could not be evaluated (it fails).
+ * flags[c] (nullable) are the detector flags; certification requires 0.
+ * pass[c*n_tols+p] = 1 iff the case passes numerically at pair p;
+ * rate[p] = certified cases / n_cases (0 when n_cases == 0). */
+void orc_suite(int32_t n_cases, int32_t n_tols, const uint64_t *mismatches,
+               const int32_t *status, const uint32_t *flags, uint8_t *pass, double *rate);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
