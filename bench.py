@@ -1,0 +1,226 @@
+#!/usr/bin/env python3
+"""Throughput of the validation hot path on one MI355X.
+
+One step = one vcheck_sweep call over a whole synthetic workload (tolerance
+gate, NaN/Inf counts, exact max abs/rel, error sums, tile map, first-k,
+detectors and suite match rate: every stage of the path), inputs resident in
+HBM. The Infinity Cache is flushed (512 MiB write) before every step, outside
+the timed interval; each step is timed with HIP events on the launch stream.
+
+Headline line: the fp16 batch of 64 cases of 2048x2048 (the configuration the
+metric is quoted on). ``workloads`` holds the same figures for all five
+workloads, measured in the same run. ``roofline`` reports the main streaming
+kernel's achieved HBM bandwidth (algorithmic bytes / its event-timed average
+duration) against the 8 TB/s peak; ``cpu_baseline`` times the CPU oracle on a
+bounded sample of the headline workload on this host.
+
+Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--headline-only]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "validated GB/s (ref+cand bytes) and % of HBM peak; test cases/sec"
+HBM_PEAK_GBS = 8000.0
+HEADLINE = 2
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_02712_amd", "csrc", "vcheck_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def kernel_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(w, classes=None):
+    """ref + cand bytes, plus operator-input bytes read while cand is a copy."""
+    b = w.ref_cand_bytes
+    if w.integrity and classes is not None:
+        import workloads as wl
+
+        for case, k in zip(w.cases, classes):
+            if int(k) == wl.CLASS_COPY:
+                b += sum(x.numel() * x.element_size() for x in case.inputs)
+    return b
+
+
+def time_sweep(sw, steps, warmup, flush):
+    import torch
+    from paper_2608_02712_amd import vcheck as vc
+
+    for _ in range(warmup):
+        sw.launch()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    stream = torch.cuda.current_stream()
+    for quad in evs:
+        for e in quad:
+            e.record(stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        flush.fill_(i & 0xFF)
+        c0, c1, m0, m1 = evs[i]
+        c0.record(stream)
+        vc.vcheck_profile_events(m0, m1)
+        sw.launch(stream)
+        c1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    call_ms = sorted(a.elapsed_time(b) for a, b, _, _ in evs)
+    main_ms = [m0.elapsed_time(m1) for _, _, m0, m1 in evs]
+    return call_ms, main_ms, wall
+
+
+def measure(cfg, steps, warmup, flush):
+    import torch
+
+    import workloads as wl
+    from paper_2608_02712_amd import vcheck as vc
+
+    t = time.perf_counter()
+    w = wl.CONFIGS[cfg]("cuda")
+    torch.cuda.synchronize()
+    log("workload %d (%s) generated in %.1f s" % (cfg, w.name, time.perf_counter() - t))
+    sw = vc.Sweep([(c.cand, c.ref, c.inputs) for c in w.cases], w.tols, primary=w.primary,
+                  tile=w.tile, k=w.k or 0, integrity=w.integrity)
+    call_ms, main_ms, wall = time_sweep(sw, steps, warmup, flush)
+    res = sw.results()
+    ms = call_ms[len(call_ms) // 2]
+    main_avg = sum(main_ms) / len(main_ms)
+    rc = w.ref_cand_bytes
+    alg = algorithmic_bytes(w, w.meta.get("classes"))
+    out = {
+        "workload": w.name,
+        "n_cases": len(w.cases),
+        "elements": w.numel,
+        "ref_cand_bytes": rc,
+        "ms_per_call": round(ms, 5),
+        "gbps": round(rc / (ms * 1e-3) / 1e9, 2),
+        "pct_hbm_peak": round(100.0 * rc / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "cases_per_s": round(len(w.cases) / (ms * 1e-3), 1),
+        "main_kernel_ms": round(main_avg, 5),
+        "main_kernel_alg_bytes": alg,
+        "main_kernel_gbps": round(alg / (main_avg * 1e-3) / 1e9, 2),
+        "match_rate": [float(x) for x in res["match_rate"]],
+        "wall_s_timed_loop": round(wall, 3),
+    }
+    log("workload %d: %.3f ms/call, %.1f GB/s (%.1f%% of peak), main kernel %.3f ms" % (
+        cfg, ms, out["gbps"], out["pct_hbm_peak"], main_avg))
+    return w, out
+
+
+def cpu_baseline(w, seconds):
+    """The CPU oracle, single thread, on whole cases of the workload until the
+    time budget is used (at least one case)."""
+    import oracle
+    import workloads as wl
+
+    oracle.default_lib()
+    done_cases, done_bytes, spent = 0, 0, 0.0
+    for case in w.cases:
+        cand, ref = wl.raw_numpy(case.cand).reshape(-1), wl.raw_numpy(case.ref).reshape(-1)
+        t = time.perf_counter()
+        oracle.validate_case(cand, ref, wl.dtype_code(case.ref.dtype), tuple(case.ref.shape),
+                             w.tols, primary=w.primary, tile=w.tile, k=w.k)
+        spent += time.perf_counter() - t
+        done_cases += 1
+        done_bytes += cand.nbytes + ref.nbytes
+        if spent >= seconds:
+            break
+    log("cpu oracle: %d cases in %.1f s" % (done_cases, spent))
+    return {"value": round(done_bytes / spent / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "cases_per_s": round(done_cases / spent, 3),
+            "sample": "%d of %d cases (%d elements), one thread, plain C oracle" % (
+                done_cases, len(w.cases), done_bytes // (2 * w.cases[0].ref.element_size()))}
+
+
+def traffic_for(name, launches_bytes):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, if they
+    were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = data.get(name)
+    if not ent or ent.get("kernel_sha") != kernel_hash():
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--headline-only", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build validates on a single MI355X "
+              "(--gpus 1); multi-GPU runs are not part of it.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    torch.cuda.init()
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    results = {}
+    w, head = measure(HEADLINE, args.steps, args.warmup, flush)
+    results[HEADLINE] = head
+    cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds)
+    del w
+    torch.cuda.empty_cache()
+    if not args.headline_only:
+        for cfg in (1, 3, 4, 5):
+            wk, r = measure(cfg, args.steps, args.warmup, flush)
+            results[cfg] = r
+            del wk
+            torch.cuda.empty_cache()
+
+    achieved = head["main_kernel_gbps"]
+    traffic = traffic_for(head["workload"], head["main_kernel_alg_bytes"])
+    line = {
+        "metric": METRIC,
+        "value": head["gbps"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_call"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": head["workload"], "storage": "fp16", "n_cases": head["n_cases"],
+                   "tols": [[1e-3, 1e-3]], "tile": [64, 64], "k": 64,
+                   "pct_hbm_peak": head["pct_hbm_peak"], "cases_per_s": head["cases_per_s"],
+                   "ref_cand_bytes": head["ref_cand_bytes"], "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "kernel": "main_kernel (fp16, 1 tolerance pair)",
+                     "alg_bytes_per_launch": head["main_kernel_alg_bytes"],
+                     "avg_launch_ms": head["main_kernel_ms"]},
+        "cpu_baseline": cpu,
+        "workloads": {str(k): v for k, v in sorted(results.items())},
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

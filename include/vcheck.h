@@ -1,0 +1,270 @@
+/*
+ * vcheck.h -- C ABI of the MI355X (gfx950) validation and failure-forensics
+ * library. ABI version 1.
+ *
+ * The library is the engine-owned validator of the paper's debug loop: it
+ * compares a candidate operator output with the reference output over every
+ * test case (Sec. 3.2, Eq. 1: Validate(K, R, T_ext, tau) = true), produces the
+ * numerical-deviation metrics that the same section lists as diagnostic
+ * evidence, localizes mismatches (Sec. 4.2, diagnostic instrumentation;
+ * Sec. S2.2, NaN/Inf forensics triggering localization), runs output-level
+ * degenerate-output detectors on every candidate (Sec. 4.1: integrity
+ * checking on every candidate belongs to the engine; Sec. 4.3 anti-cheat),
+ * and reduces per-case verdicts and suite match rates over the full case
+ * matrix (Sec. 4.3 full-coverage evaluation; Sec. S3.4, P/x = x% matched
+ * cases). Only this library's results carry acceptance: the caller cannot
+ * make a case pass (Sec. 1 and Sec. 4.1, evidence ownership).
+ *
+ * ---- Conventions shared by every entry point ----------------------------
+ *
+ * Element semantics (per case; the view is (R, C) with C = last dimension,
+ * R = product of the others; a 0-d tensor is (1, 1)):
+ *   - values are decoded exactly (fp32 widened, fp16 per binary16 incl.
+ *     subnormals, bf16 = upper half of a binary32 pattern) and compared in
+ *     IEEE binary64 with round-to-nearest-even and no fused multiply-add;
+ *   - gate for tolerance pair p:  close_p(i) = (c_i == r_i)
+ *       or (c_i, r_i finite and |c_i - r_i| <= atol_p + rtol_p * |r_i|)
+ *       or (equal_nan_p and c_i, r_i both NaN);  mismatch = not close.
+ *     +Inf == +Inf is close, +0 == -0 is close, NaN is never close unless
+ *     equal_nan is set;
+ *   - metrics run over finite pairs only: d_i = |c_i - r_i|, and
+ *     q_i = d_i / |r_i| where r_i != 0; argmax ties go to the smallest index.
+ *
+ * Memory: every data and output pointer is a DEVICE pointer on the current
+ * HIP device; descriptor structs (vc_tensor, vc_case, vc_tol, vc_sweep_opts,
+ * vc_sweep_out) are HOST memory and are not referenced after the call
+ * returns. The caller owns every buffer, including the workspace (device
+ * memory of at least vcheck_workspace_bytes() bytes, any alignment, contents
+ * ignored on entry and clobbered); it must keep them alive until the stream
+ * has finished the enqueued work. Results are valid after the stream syncs.
+ * Input tensors must be contiguous row-major; a data pointer must be aligned
+ * to its element size (16-byte alignment takes the fast vectorised path).
+ *
+ * Errors: every argument is checked on the host before anything is enqueued.
+ * On error the call returns a negative vc_status, enqueues nothing and writes
+ * no output; vcheck_last_error() gives a thread-local description. VC_OK
+ * means the work was enqueued on `stream` (a hipStream_t; NULL = the null
+ * stream). HIP launch failures return VC_ERR_HIP with the HIP error string.
+ *
+ * Determinism: results are bit-identical across runs for identical inputs
+ * (fixed-order reductions, no floating-point atomics).
+ *
+ * Concurrency: calls on different streams may run concurrently as long as
+ * they use different workspaces and outputs.
+ */
+#ifndef VCHECK_H
+#define VCHECK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VCHECK_ABI_VERSION 1
+#define VC_MAX_NDIM 8
+#define VC_MAX_TOLS 8
+#define VC_MAX_INPUTS 8
+#define VC_MAX_K 1024
+
+typedef int32_t vc_status;
+#define VC_OK 0
+#define VC_ERR_NULL (-1)      /* a required pointer is NULL */
+#define VC_ERR_DTYPE (-2)     /* unknown dtype, or cand/ref dtypes differ */
+#define VC_ERR_SHAPE (-3)     /* bad ndim/shape, or cand/ref shapes differ */
+#define VC_ERR_TOL (-4)       /* atol/rtol negative or not finite, bad primary_tol */
+#define VC_ERR_TILE (-5)      /* tile_h or tile_w < 1 while a tile map is requested */
+#define VC_ERR_K (-6)         /* k < 0, k > VC_MAX_K, or first_k NULL with k > 0 */
+#define VC_ERR_WORKSPACE (-7) /* workspace NULL or smaller than required */
+#define VC_ERR_LIMIT (-8)     /* n_tols, n_inputs or n_cases outside its range */
+#define VC_ERR_HIP (-9)       /* HIP runtime / launch failure */
+#define VC_ERR_ALIGN (-10)    /* data pointer not aligned to its element size */
+
+typedef enum vc_dtype { VC_F32 = 0, VC_F16 = 1, VC_BF16 = 2 } vc_dtype;
+
+/* Detector flag bits (vc_integrity.flags); each is a conjunction, so each
+ * degenerate class raises exactly one of them. n = numel. */
+#define VC_FLAG_ALL_ZERO (1u << 0)     /* every cand element is +-0, ref is not */
+#define VC_FLAG_CONSTANT (1u << 1)     /* n >= 2, every cand element has the bit pattern
+                                          of element 0, cand is not all zero, ref is not
+                                          constant */
+#define VC_FLAG_INPUT_COPY (1u << 2)   /* cand is a bit copy of an operator input that
+                                          ref is not a copy of */
+#define VC_FLAG_LOWPREC_BF16 (1u << 3) /* fp32 only: n >= 2, every cand value is
+                                          bf16-representable, cand neither constant nor
+                                          all zero, ref not all bf16-representable */
+#define VC_FLAG_LOWPREC_FP16 (1u << 4) /* fp32 only: as above for binary16, and cand is
+                                          not all bf16-representable */
+
+/* Tensor descriptor (host struct; data is a device pointer). */
+typedef struct vc_tensor {
+  const void *data;
+  int32_t dtype; /* vc_dtype */
+  int32_t ndim;  /* 0 .. VC_MAX_NDIM */
+  int64_t shape[VC_MAX_NDIM];
+} vc_tensor; /* 80 bytes */
+
+/* One tolerance pair; atol and rtol finite and >= 0; equal_nan 0 or 1. */
+typedef struct vc_tol {
+  double atol;
+  double rtol;
+  int32_t equal_nan;
+  int32_t reserved; /* must be 0 */
+} vc_tol; /* 24 bytes */
+
+/* Per-case statistics (device-resident output). Counts at the primary pair. */
+typedef struct vc_stats {
+  uint64_t numel;
+  uint64_t mismatches;                      /* at the primary tolerance pair */
+  uint64_t nan_cand, inf_cand, nan_ref, inf_ref; /* element counts */
+  uint64_t n_finite;    /* pairs with both values finite */
+  uint64_t n_rel;       /* finite pairs with r != 0 */
+  uint64_t n_rel_undef; /* finite pairs with r == 0 and c != 0 */
+  double max_abs;       /* 0.0 when n_finite == 0 */
+  int64_t argmax_abs;   /* flat index, -1 when n_finite == 0 */
+  double max_rel;       /* exact (correctly rounded quotient) */
+  int64_t argmax_rel;   /* -1 when n_rel == 0 */
+  double sum_abs;       /* sum of d_i, binary64 (order-dependent, ~1e-12 rel) */
+  double sum_rel;       /* sum of q_i, binary64, within 1e-6 relative */
+  int32_t case_status;  /* 0, or a negative vc_status for a case that could not run */
+  int32_t pass;         /* 1 iff case_status == 0 and mismatches == 0 */
+} vc_stats; /* 128 bytes */
+
+/* Degenerate-output detector results (device-resident output). */
+typedef struct vc_integrity {
+  uint64_t zero_cand, zero_ref;       /* elements equal to +-0 */
+  uint64_t eqfirst_cand, eqfirst_ref; /* elements bit-equal to element 0 */
+  uint64_t bf16rep_cand, bf16rep_ref; /* fp32 only: low 16 pattern bits zero */
+  uint64_t fp16rep_cand, fp16rep_ref; /* fp32 only: exactly representable in binary16
+                                         (NaN and +-Inf count as representable) */
+  uint32_t flags;                     /* VC_FLAG_* */
+  int32_t copy_input;                 /* smallest j raising INPUT_COPY, else -1 */
+  uint32_t cand_eq_input_mask;        /* bit j: cand bit-equal to input j (same dtype,
+                                         same numel) */
+  uint32_t ref_eq_input_mask;         /* bit j: ref bit-equal to input j */
+  uint32_t cand_eq_ref;               /* 1 iff cand bit-equal to ref (evidence only) */
+  uint32_t reserved;
+} vc_integrity; /* 88 bytes */
+
+/* One test case of a sweep (host struct). inputs: host array of n_inputs
+ * operator-input descriptors used by the input-copy detector. */
+typedef struct vc_case {
+  vc_tensor cand;
+  vc_tensor ref;
+  const vc_tensor *inputs;
+  int32_t n_inputs; /* 0 .. VC_MAX_INPUTS */
+  int32_t reserved;
+} vc_case; /* 176 bytes */
+
+typedef struct vc_sweep_opts {
+  int32_t primary_tol;  /* pair used for vc_stats.mismatches, tile maps, first-k */
+  int32_t tile_h, tile_w; /* tile geometry, used when out->tile_maps != NULL */
+  int32_t k;            /* first-k length, used when out->first_k != NULL */
+  int32_t do_integrity; /* 1: run the detectors (out->integ required) */
+  int32_t reserved;
+} vc_sweep_opts;
+
+/* Sweep outputs (host struct of device pointers). */
+typedef struct vc_sweep_out {
+  vc_stats *stats;        /* [n_cases], required */
+  uint64_t *mismatches;   /* [n_cases * n_tols] case-major, nullable */
+  uint8_t *pass;          /* [n_cases * n_tols]: numeric pass per pair, nullable */
+  double *match_rate;     /* [n_tols]: certified cases / n_cases, nullable;
+                             certified = pass and (no integrity run or flags == 0) */
+  double *numeric_rate;   /* [n_tols]: passing cases / n_cases, nullable */
+  uint32_t *tile_maps;    /* concatenated per-case tile maps, nullable; case i
+                             starts at sum_{j<i} vcheck_tile_count(case j) */
+  int64_t *first_k;       /* [n_cases * k], -1 padded, nullable */
+  vc_integrity *integ;    /* [n_cases], required iff do_integrity */
+} vc_sweep_out;
+
+/*
+ * vcheck_compare -- validate one candidate against its reference at one
+ * tolerance pair (Sec. 3.2 Validate; metrics of the diagnostic evidence D).
+ *   cand, ref: same dtype and shape.  tol: one pair.
+ *   out: device vc_stats.  ws/ws_bytes: workspace (vcheck_workspace_bytes
+ *   with the case {cand, ref}, n_tols = 1, opts = NULL).
+ */
+vc_status vcheck_compare(const vc_tensor *cand, const vc_tensor *ref, const vc_tol *tol,
+                         vc_stats *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * vcheck_localize -- vcheck_compare plus localization (Sec. 4.2 diagnostic
+ * instrumentation; Sec. S2.2 NaN/Inf forensics triggering localization).
+ *   tile_map: device uint32[vcheck_tile_count(cand, tile_h, tile_w)],
+ *     mismatches per tile_h x tile_w tile of the (R, C) view, row-major
+ *     tiles, partial edge tiles included.
+ *   first_k: device int64[k], the k smallest mismatching flat indices in
+ *     ascending order, -1 padded (may be NULL when k == 0).
+ *   out: device vc_stats, nullable.
+ *   Workspace: vcheck_workspace_bytes with opts.k = k.
+ */
+vc_status vcheck_localize(const vc_tensor *cand, const vc_tensor *ref, const vc_tol *tol,
+                          int32_t tile_h, int32_t tile_w, uint32_t *tile_map, int32_t k,
+                          int64_t *first_k, vc_stats *out, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/*
+ * vcheck_integrity -- degenerate-output detectors in the same pass as the
+ * comparison (integrity hazards: Sec. 1 "degeneration", Sec. 3.3 host-wrapper
+ * bypass, Sec. 4.3 anti-cheat, Sec. 4.4 degenerate-round and fp16-ceiling
+ * detection, Sec. S2.2 golden-output cache).
+ *   inputs: host array of n_inputs (0 .. VC_MAX_INPUTS) operator inputs;
+ *     an input takes part in the copy detector when its dtype and numel
+ *     match cand's. Input data is read only while cand or ref is still
+ *     bit-equal to it.
+ *   out: device vc_integrity.  stats: device vc_stats, nullable.
+ */
+vc_status vcheck_integrity(const vc_tensor *cand, const vc_tensor *ref, const vc_tensor *inputs,
+                           int32_t n_inputs, const vc_tol *tol, vc_integrity *out,
+                           vc_stats *stats, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * vcheck_sweep -- validate a whole case matrix in one call (Sec. 4.3
+ * full-coverage evaluation: per-case pass/fail and match rates over all
+ * shapes and dtypes), evaluating n_tols (1 .. VC_MAX_TOLS) tolerance pairs in
+ * the same pass. n_cases 0 .. 2^24.
+ * A case whose cand/ref dtype or shape differ, or whose pointers are not
+ * element-aligned, is a data outcome, not an API error: it gets a negative
+ * case_status and pass = 0 (the paper's runtime-failure class), the rest of
+ * the batch runs.
+ * opts: NULL means primary_tol 0, no tile maps, k = 0, no integrity.
+ */
+vc_status vcheck_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols, int32_t n_tols,
+                       const vc_sweep_opts *opts, const vc_sweep_out *out, void *ws,
+                       size_t ws_bytes, void *stream);
+
+/* Profiling hook (tracing): the next vcheck_compare / _localize / _integrity /
+ * _sweep call made on this thread records `begin_event` on its stream just
+ * before its first streaming-kernel launch and `end_event` just after its
+ * last one, so hipEventElapsedTime gives the duration of the main kernels
+ * alone (without the tile-map fill, finalize and rate kernels). Both are
+ * hipEvent_t handles created by the caller; the hook is consumed by that one
+ * call. Pass NULL, NULL to clear it. Returns VC_OK, or VC_ERR_NULL when only
+ * one of the two is NULL. */
+vc_status vcheck_profile_events(void *begin_event, void *end_event);
+
+/* Workspace bytes for a sweep over `cases` (also for the single-case entry
+ * points: one case, n_tols = 1, opts carrying k). Returns VC_OK and writes
+ * *bytes, or an error status for arguments the sweep would reject. */
+vc_status vcheck_workspace_bytes(const vc_case *cases, int32_t n_cases, int32_t n_tols,
+                                 const vc_sweep_opts *opts, size_t *bytes);
+
+/* Number of tiles of t's (R, C) view: ceil(R/tile_h) * ceil(C/tile_w);
+ * -1 for an invalid descriptor or tile size. */
+int64_t vcheck_tile_count(const vc_tensor *t, int32_t tile_h, int32_t tile_w);
+
+/* Static description of a status code. */
+const char *vcheck_status_str(vc_status status);
+
+/* Thread-local description of the last error on this thread ("" if none). */
+const char *vcheck_last_error(void);
+
+/* VCHECK_ABI_VERSION of the loaded library. */
+int32_t vcheck_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VCHECK_H */

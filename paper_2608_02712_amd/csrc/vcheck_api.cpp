@@ -1,0 +1,604 @@
+// vcheck_api.cpp -- host side of the C ABI declared in include/vcheck.h:
+// argument validation (before anything is enqueued), work planning, workspace
+// layout, descriptor upload and kernel launches.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "vcheck_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local hipEvent_t g_prof_begin = nullptr, g_prof_end = nullptr;
+
+vc_status fail(vc_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t elem_size(int32_t dtype) { return dtype == VC_F32 ? 4 : 2; }
+bool dtype_ok(int32_t dtype) { return dtype == VC_F32 || dtype == VC_F16 || dtype == VC_BF16; }
+
+// numel of a descriptor; -1 on an invalid shape or overflow past 2^62.
+int64_t numel_of(const vc_tensor &t) {
+  if (t.ndim < 0 || t.ndim > VC_MAX_NDIM) return -1;
+  int64_t n = 1;
+  for (int i = 0; i < t.ndim; ++i) {
+    if (t.shape[i] < 0) return -1;
+    if (t.shape[i] == 0) n = 0;
+    else if (n != 0 && n > (int64_t(1) << 62) / t.shape[i]) return -1;
+    else n *= t.shape[i];
+  }
+  return n;
+}
+
+// C of the (R, C) view: last dimension, 1 for a 0-d tensor.
+uint64_t cols_of(const vc_tensor &t) { return t.ndim == 0 ? 1 : (uint64_t)t.shape[t.ndim - 1]; }
+
+bool same_shape(const vc_tensor &a, const vc_tensor &b) {
+  if (a.ndim != b.ndim) return false;
+  for (int i = 0; i < a.ndim; ++i)
+    if (a.shape[i] != b.shape[i]) return false;
+  return true;
+}
+
+// Checks one descriptor on its own. Returns VC_OK or an error status.
+vc_status check_tensor(const vc_tensor *t, const char *what) {
+  if (t == nullptr) return fail(VC_ERR_NULL, "%s descriptor is NULL", what);
+  if (!dtype_ok(t->dtype)) return fail(VC_ERR_DTYPE, "%s has unknown dtype %d", what, t->dtype);
+  if (t->ndim < 0 || t->ndim > VC_MAX_NDIM)
+    return fail(VC_ERR_SHAPE, "%s has ndim %d outside 0..%d", what, t->ndim, VC_MAX_NDIM);
+  const int64_t n = numel_of(*t);
+  if (n < 0) return fail(VC_ERR_SHAPE, "%s has a negative or too large shape", what);
+  if (n > 0 && t->data == nullptr) return fail(VC_ERR_NULL, "%s data is NULL", what);
+  if ((uintptr_t)t->data % elem_size(t->dtype) != 0)
+    return fail(VC_ERR_ALIGN, "%s data is not aligned to its element size", what);
+  return VC_OK;
+}
+
+vc_status check_tols(const vc_tol *tols, int32_t n_tols) {
+  if (n_tols < 1 || n_tols > VC_MAX_TOLS)
+    return fail(VC_ERR_LIMIT, "n_tols %d outside 1..%d", n_tols, VC_MAX_TOLS);
+  if (tols == nullptr) return fail(VC_ERR_NULL, "tolerance array is NULL");
+  for (int p = 0; p < n_tols; ++p) {
+    const vc_tol &t = tols[p];
+    if (!std::isfinite(t.atol) || !std::isfinite(t.rtol) || t.atol < 0 || t.rtol < 0)
+      return fail(VC_ERR_TOL, "tolerance pair %d: atol and rtol must be finite and >= 0", p);
+    if (t.equal_nan != 0 && t.equal_nan != 1)
+      return fail(VC_ERR_TOL, "tolerance pair %d: equal_nan must be 0 or 1", p);
+  }
+  return VC_OK;
+}
+
+struct Group {
+  int32_t dtype;
+  uint64_t case_lo, case_hi;    // table range
+  uint64_t chunk_lo, n_chunks;  // global chunk range
+  uint32_t unit;
+};
+
+struct Plan {
+  std::vector<vck::DevCase> table;
+  std::vector<Group> groups;
+  uint64_t total_chunks = 0;
+  uint64_t tiles_total = 0;
+  int32_t n_cases = 0, n_tols = 1, nt_class = 1, k = 0, primary = 0, tile_h = 1, tile_w = 1;
+  bool do_tiles = false, do_firstk = false, do_integ = false;
+  size_t off_table = 0, off_recs = 0, off_stage = 0, off_pass = 0, off_flags = 0, bytes = 0;
+};
+
+// Elements per wave range: about 16K waves over the group, 1 Ki .. 64 KiB of
+// each tensor per wave, a power of two (so every range is 16-byte aligned).
+uint32_t unit_for(uint64_t group_elems, int32_t dtype) {
+  const uint64_t lo = 1024, hi = 65536 / elem_size(dtype);
+  uint64_t u = lo;
+  while (u < hi && u * 2 * 16384 <= group_elems) u *= 2;
+  return (uint32_t)u;
+}
+
+// Builds the plan. `single` requests the API-error behaviour of the
+// single-case entry points for dtype/shape mismatches.
+vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, int32_t n_tols,
+                    const vc_sweep_opts &opts, bool want_tiles, bool want_firstk, bool single,
+                    Plan &plan) {
+  if (n_cases < 0 || n_cases > (1 << 24))
+    return fail(VC_ERR_LIMIT, "n_cases %d outside 0..2^24", n_cases);
+  if (n_cases > 0 && cases == nullptr) return fail(VC_ERR_NULL, "case array is NULL");
+  {
+    const vc_status st = check_tols(tols, n_tols);
+    if (st != VC_OK) return st;
+  }
+  if (opts.primary_tol < 0 || opts.primary_tol >= n_tols)
+    return fail(VC_ERR_TOL, "primary_tol %d outside 0..%d", opts.primary_tol, n_tols - 1);
+  if (want_tiles && (opts.tile_h < 1 || opts.tile_w < 1))
+    return fail(VC_ERR_TILE, "tile_h and tile_w must be >= 1 (got %d x %d)", opts.tile_h,
+                opts.tile_w);
+  if (opts.k < 0 || opts.k > VC_MAX_K) return fail(VC_ERR_K, "k %d outside 0..%d", opts.k, VC_MAX_K);
+  if (opts.do_integrity != 0 && opts.do_integrity != 1)
+    return fail(VC_ERR_LIMIT, "do_integrity must be 0 or 1");
+
+  plan.n_cases = n_cases;
+  plan.n_tols = n_tols;
+  plan.nt_class = n_tols <= 1 ? 1 : n_tols <= 2 ? 2 : n_tols <= 4 ? 4 : 8;
+  plan.primary = opts.primary_tol;
+  plan.do_tiles = want_tiles;
+  plan.do_firstk = want_firstk && opts.k > 0;
+  plan.k = plan.do_firstk ? opts.k : 0;
+  plan.tile_h = want_tiles ? opts.tile_h : 1;
+  plan.tile_w = want_tiles ? opts.tile_w : 1;
+  plan.do_integ = opts.do_integrity == 1;
+
+  // per-case descriptors in caller order first
+  std::vector<vck::DevCase> dc(n_cases);
+  std::vector<uint64_t> tile_count(n_cases, 0);
+  for (int32_t i = 0; i < n_cases; ++i) {
+    const vc_case &c = cases[i];
+    char what[64];
+    // A malformed descriptor (NULL data, unknown dtype, bad shape) is an API
+    // error. A misaligned pointer or a cand/ref dtype or shape difference is
+    // a per-case outcome in a sweep and an API error for a single case.
+    snprintf(what, sizeof what, "case %d cand", i);
+    vc_status st = check_tensor(&c.cand, what);
+    if (st != VC_OK && st != VC_ERR_ALIGN) return st;
+    snprintf(what, sizeof what, "case %d ref", i);
+    vc_status st_r = check_tensor(&c.ref, what);
+    if (st_r != VC_OK && st_r != VC_ERR_ALIGN) return st_r;
+    if (st == VC_OK) st = st_r;
+    if (c.n_inputs < 0 || c.n_inputs > VC_MAX_INPUTS)
+      return fail(VC_ERR_LIMIT, "case %d: n_inputs %d outside 0..%d", i, c.n_inputs,
+                  VC_MAX_INPUTS);
+    if (c.n_inputs > 0 && c.inputs == nullptr)
+      return fail(VC_ERR_NULL, "case %d: inputs array is NULL", i);
+    if (plan.do_integ) {
+      for (int32_t j = 0; j < c.n_inputs; ++j) {
+        snprintf(what, sizeof what, "case %d input %d", i, j);
+        const vc_status sx = check_tensor(&c.inputs[j], what);
+        if (sx != VC_OK && sx != VC_ERR_ALIGN) return sx;
+      }
+    }
+    if (st == VC_OK && c.cand.dtype != c.ref.dtype)
+      st = fail(VC_ERR_DTYPE, "case %d: cand and ref dtypes differ", i);
+    if (st == VC_OK && !same_shape(c.cand, c.ref))
+      st = fail(VC_ERR_SHAPE, "case %d: cand and ref shapes differ", i);
+    if (st != VC_OK && single) return st;
+
+    vck::DevCase &d = dc[i];
+    memset(&d, 0, sizeof d);
+    d.orig = (uint32_t)i;
+    d.dtype = (uint32_t)c.ref.dtype;
+    const int64_t n = numel_of(c.ref);
+    d.numel = (uint64_t)n;
+    if (st != VC_OK) {
+      d.status = st;
+      continue;
+    }
+    d.cand = (const uint8_t *)c.cand.data;
+    d.ref = (const uint8_t *)c.ref.data;
+    d.cols = cols_of(c.ref);
+    bool vec = ((uintptr_t)c.cand.data % 16 == 0) && ((uintptr_t)c.ref.data % 16 == 0);
+    if (plan.do_integ) {
+      for (int32_t j = 0; j < c.n_inputs; ++j) {
+        const vc_tensor &x = c.inputs[j];
+        if (x.dtype == c.ref.dtype && numel_of(x) == n &&
+            (uintptr_t)x.data % elem_size(x.dtype) == 0) {
+          d.inp_mask |= 1u << j;
+          d.inp[j] = (const uint8_t *)x.data;
+          vec = vec && ((uintptr_t)x.data % 16 == 0);
+        }
+      }
+    }
+    d.vec_ok = vec ? 1u : 0u;
+    if (want_tiles && n > 0) {
+      const uint64_t rows = (uint64_t)n / d.cols;
+      d.tiles_c = (d.cols + opts.tile_w - 1) / opts.tile_w;
+      tile_count[i] = ((rows + opts.tile_h - 1) / opts.tile_h) * d.tiles_c;
+    }
+  }
+  // tile-map offsets follow the caller's case order
+  if (want_tiles) {
+    uint64_t acc = 0;
+    for (int32_t i = 0; i < n_cases; ++i) {
+      dc[i].tile_off = acc;
+      acc += tile_count[i];
+    }
+    plan.tiles_total = acc;
+  }
+  // group by dtype (stable): F32, F16, BF16; chunks numbered in table order
+  uint64_t chunk = 0;
+  for (int32_t dt : {VC_F32, VC_F16, VC_BF16}) {
+    Group g{};
+    g.dtype = dt;
+    g.case_lo = plan.table.size();
+    uint64_t elems = 0;
+    for (int32_t i = 0; i < n_cases; ++i)
+      if ((int32_t)dc[i].dtype == dt && dc[i].status == 0) elems += dc[i].numel;
+    g.unit = unit_for(elems, dt);
+    g.chunk_lo = chunk;
+    for (int32_t i = 0; i < n_cases; ++i) {
+      if ((int32_t)dc[i].dtype != dt) continue;
+      vck::DevCase d = dc[i];
+      d.unit_elems = g.unit;
+      d.chunk_begin = chunk;
+      const uint64_t ch = 4ull * g.unit;
+      const uint64_t nc = d.status == 0 ? (d.numel + ch - 1) / ch : 0;
+      if (nc > 0xffffffffull) return fail(VC_ERR_LIMIT, "case %d is too large", (int)d.orig);
+      d.n_chunks = (uint32_t)nc;
+      chunk += nc;
+      plan.table.push_back(d);
+    }
+    g.case_hi = plan.table.size();
+    g.n_chunks = chunk - g.chunk_lo;
+    if (g.case_hi > g.case_lo) plan.groups.push_back(g);
+  }
+  plan.total_chunks = chunk;
+
+  // workspace layout
+  size_t off = 0;
+  plan.off_table = off;
+  off += align_up(sizeof(vck::DevCase) * (size_t)n_cases);
+  plan.off_recs = off;
+  off += align_up(sizeof(vck::ChunkRec) * (size_t)plan.total_chunks);
+  plan.off_stage = off;
+  off += align_up(sizeof(uint32_t) * (size_t)plan.total_chunks * vck::kWavesPerBlock *
+                  (size_t)plan.k);
+  plan.off_pass = off;
+  off += align_up((size_t)n_cases * (size_t)n_tols);
+  plan.off_flags = off;
+  off += align_up(sizeof(uint32_t) * (size_t)n_cases);
+  plan.bytes = off + kAlign;  // slack for aligning the caller's base pointer
+  return VC_OK;
+}
+
+// ---- pinned staging for descriptor uploads ---------------------------------
+// A small ring of pinned host buffers per device. A slot is reused only after
+// the event recorded behind its previous copy has completed.
+struct Slot {
+  void *host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+struct DeviceStaging {
+  std::mutex mu;
+  Slot slots[8];
+  int next = 0;
+};
+constexpr int kMaxDevices = 64;
+DeviceStaging g_staging[kMaxDevices];
+
+vc_status upload(void *dst, const void *src, size_t bytes, hipStream_t s) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(VC_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(VC_ERR_HIP, "device id %d out of range", dev);
+  DeviceStaging &ds = g_staging[dev];
+  std::lock_guard<std::mutex> lock(ds.mu);
+  Slot &sl = ds.slots[ds.next];
+  ds.next = (ds.next + 1) % 8;
+  if (sl.pending) {
+    e = hipEventSynchronize(sl.ev);
+    if (e != hipSuccess) return fail(VC_ERR_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
+    sl.pending = false;
+  }
+  if (sl.ev == nullptr) {
+    e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
+    if (e != hipSuccess) return fail(VC_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(e));
+  }
+  if (sl.cap < bytes) {
+    if (sl.host != nullptr) (void)hipHostFree(sl.host);
+    sl.host = nullptr;
+    sl.cap = 0;
+    const size_t cap = std::max<size_t>(bytes, 64 * 1024);
+    e = hipHostMalloc(&sl.host, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return fail(VC_ERR_HIP, "hipHostMalloc: %s", hipGetErrorString(e));
+    sl.cap = cap;
+  }
+  memcpy(sl.host, src, bytes);
+  e = hipMemcpyAsync(dst, sl.host, bytes, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return fail(VC_ERR_HIP, "hipMemcpyAsync: %s", hipGetErrorString(e));
+  e = hipEventRecord(sl.ev, s);
+  if (e != hipSuccess) return fail(VC_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+  sl.pending = true;
+  return VC_OK;
+}
+
+vc_status hip_check(hipError_t e, const char *what) {
+  if (e == hipSuccess) return VC_OK;
+  return fail(VC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct Outputs {
+  vc_stats *stats = nullptr;
+  uint64_t *mismatches = nullptr;
+  uint8_t *pass = nullptr;
+  double *match_rate = nullptr;
+  double *numeric_rate = nullptr;
+  uint32_t *tile_maps = nullptr;
+  int64_t *first_k = nullptr;
+  vc_integrity *integ = nullptr;
+};
+
+// Enqueues the planned work. `single` passes the one descriptor by value
+// (no upload).
+vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws, size_t ws_bytes,
+              hipStream_t stream, bool single) {
+  if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < plan.bytes)
+    return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
+  uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
+
+  vck::Params P;
+  memset(&P, 0, sizeof P);
+  P.n_cases = plan.n_cases;
+  P.n_tols = plan.n_tols;
+  P.primary = plan.primary;
+  P.tile_h = plan.tile_h;
+  P.tile_w = plan.tile_w;
+  P.k = plan.k;
+  P.do_tiles = plan.do_tiles ? 1 : 0;
+  P.do_integ = plan.do_integ ? 1 : 0;
+  for (int p = 0; p < VC_MAX_TOLS; ++p) {
+    const vc_tol &t = tols[p < plan.n_tols ? p : plan.n_tols - 1];
+    P.atol[p] = t.atol;
+    P.rtol[p] = t.rtol;
+    if (t.equal_nan) P.eqnan_mask |= 1u << p;
+  }
+  P.recs = (vck::ChunkRec *)(base + plan.off_recs);
+  P.stage = (uint32_t *)(base + plan.off_stage);
+  P.tile_maps = plan.do_tiles ? out.tile_maps : nullptr;
+  P.stats = out.stats;
+  P.mismatches = out.mismatches;
+  P.pass_out = out.pass;
+  P.first_k = plan.do_firstk ? out.first_k : nullptr;
+  P.integ = out.integ;
+  P.ws_pass = base + plan.off_pass;
+  P.ws_flags = (uint32_t *)(base + plan.off_flags);
+  P.match_rate = out.match_rate;
+  P.numeric_rate = out.numeric_rate;
+  P.tiles_total = plan.tiles_total;
+  if (single) {
+    P.cases = nullptr;
+    P.single = plan.table[0];
+  } else if (plan.n_cases > 0) {
+    P.cases = (const vck::DevCase *)(base + plan.off_table);
+    const vc_status st =
+        upload(base + plan.off_table, plan.table.data(), sizeof(vck::DevCase) * plan.table.size(),
+               stream);
+    if (st != VC_OK) return st;
+  }
+  vc_status st = VC_OK;
+  if (plan.do_tiles && plan.tiles_total > 0) {
+    st = hip_check(vck::launch_fill_u32(out.tile_maps, plan.tiles_total, stream), "tile-map fill");
+    if (st != VC_OK) return st;
+  }
+  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
+  g_prof_begin = g_prof_end = nullptr;
+  if (prof_begin != nullptr) {
+    st = hip_check(hipEventRecord(prof_begin, stream), "profile begin event");
+    if (st != VC_OK) return st;
+  }
+  for (const Group &g : plan.groups) {
+    vck::Params Q = P;
+    Q.chunk_lo = g.chunk_lo;
+    Q.case_lo = g.case_lo;
+    Q.case_hi = g.case_hi;
+    Q.unit_elems = g.unit;
+    st = hip_check(vck::launch_main(g.dtype, plan.nt_class, plan.do_integ ? 1 : 0, Q, g.n_chunks,
+                                    stream),
+                   "main kernel launch");
+    if (st != VC_OK) return st;
+  }
+  if (prof_end != nullptr) {
+    st = hip_check(hipEventRecord(prof_end, stream), "profile end event");
+    if (st != VC_OK) return st;
+  }
+  if (plan.n_cases > 0) {
+    vck::Params Q = P;
+    Q.case_lo = 0;
+    Q.case_hi = plan.table.size();
+    st = hip_check(vck::launch_finalize(Q, plan.table.size(), stream), "finalize launch");
+    if (st != VC_OK) return st;
+  }
+  if (out.match_rate != nullptr || out.numeric_rate != nullptr)
+    st = hip_check(vck::launch_rates(P, stream), "rates launch");
+  return st;
+}
+
+vc_case one_case(const vc_tensor *cand, const vc_tensor *ref, const vc_tensor *inputs,
+                 int32_t n_inputs) {
+  vc_case c;
+  memset(&c, 0, sizeof c);
+  c.cand = *cand;
+  c.ref = *ref;
+  c.inputs = inputs;
+  c.n_inputs = n_inputs;
+  return c;
+}
+
+vc_status check_pair(const vc_tensor *cand, const vc_tensor *ref) {
+  vc_status st = check_tensor(cand, "cand");
+  if (st != VC_OK) return st;
+  st = check_tensor(ref, "ref");
+  if (st != VC_OK) return st;
+  if (cand->dtype != ref->dtype) return fail(VC_ERR_DTYPE, "cand and ref dtypes differ");
+  if (!same_shape(*cand, *ref)) return fail(VC_ERR_SHAPE, "cand and ref shapes differ");
+  return VC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+vc_status vcheck_compare(const vc_tensor *cand, const vc_tensor *ref, const vc_tol *tol,
+                         vc_stats *out, void *ws, size_t ws_bytes, void *stream) {
+  g_last_error.clear();
+  vc_status st = check_pair(cand, ref);
+  if (st != VC_OK) return st;
+  if (tol == nullptr) return fail(VC_ERR_NULL, "tolerance is NULL");
+  if (out == nullptr) return fail(VC_ERR_NULL, "output stats pointer is NULL");
+  const vc_case c = one_case(cand, ref, nullptr, 0);
+  vc_sweep_opts opts{};
+  Plan plan;
+  st = make_plan(&c, 1, tol, 1, opts, false, false, true, plan);
+  if (st != VC_OK) return st;
+  Outputs o;
+  o.stats = out;
+  return run(plan, tol, o, ws, ws_bytes, (hipStream_t)stream, true);
+}
+
+vc_status vcheck_localize(const vc_tensor *cand, const vc_tensor *ref, const vc_tol *tol,
+                          int32_t tile_h, int32_t tile_w, uint32_t *tile_map, int32_t k,
+                          int64_t *first_k, vc_stats *out, void *ws, size_t ws_bytes,
+                          void *stream) {
+  g_last_error.clear();
+  vc_status st = check_pair(cand, ref);
+  if (st != VC_OK) return st;
+  if (tol == nullptr) return fail(VC_ERR_NULL, "tolerance is NULL");
+  if (tile_h < 1 || tile_w < 1)
+    return fail(VC_ERR_TILE, "tile_h and tile_w must be >= 1 (got %d x %d)", tile_h, tile_w);
+  if (k < 0 || k > VC_MAX_K) return fail(VC_ERR_K, "k %d outside 0..%d", k, VC_MAX_K);
+  if (k > 0 && first_k == nullptr) return fail(VC_ERR_K, "first_k is NULL with k = %d", k);
+  const int64_t tiles = vcheck_tile_count(cand, tile_h, tile_w);
+  if (tiles > 0 && tile_map == nullptr) return fail(VC_ERR_NULL, "tile_map is NULL");
+  const vc_case c = one_case(cand, ref, nullptr, 0);
+  vc_sweep_opts opts{};
+  opts.tile_h = tile_h;
+  opts.tile_w = tile_w;
+  opts.k = k;
+  Plan plan;
+  st = make_plan(&c, 1, tol, 1, opts, true, true, true, plan);
+  if (st != VC_OK) return st;
+  Outputs o;
+  o.stats = out;
+  o.tile_maps = tile_map;
+  o.first_k = first_k;
+  return run(plan, tol, o, ws, ws_bytes, (hipStream_t)stream, true);
+}
+
+vc_status vcheck_integrity(const vc_tensor *cand, const vc_tensor *ref, const vc_tensor *inputs,
+                           int32_t n_inputs, const vc_tol *tol, vc_integrity *out,
+                           vc_stats *stats, void *ws, size_t ws_bytes, void *stream) {
+  g_last_error.clear();
+  vc_status st = check_pair(cand, ref);
+  if (st != VC_OK) return st;
+  if (tol == nullptr) return fail(VC_ERR_NULL, "tolerance is NULL");
+  if (out == nullptr) return fail(VC_ERR_NULL, "output integrity pointer is NULL");
+  if (n_inputs < 0 || n_inputs > VC_MAX_INPUTS)
+    return fail(VC_ERR_LIMIT, "n_inputs %d outside 0..%d", n_inputs, VC_MAX_INPUTS);
+  if (n_inputs > 0 && inputs == nullptr) return fail(VC_ERR_NULL, "inputs array is NULL");
+  const vc_case c = one_case(cand, ref, inputs, n_inputs);
+  vc_sweep_opts opts{};
+  opts.do_integrity = 1;
+  Plan plan;
+  st = make_plan(&c, 1, tol, 1, opts, false, false, true, plan);
+  if (st != VC_OK) return st;
+  Outputs o;
+  o.stats = stats;
+  o.integ = out;
+  return run(plan, tol, o, ws, ws_bytes, (hipStream_t)stream, true);
+}
+
+vc_status vcheck_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols, int32_t n_tols,
+                       const vc_sweep_opts *opts, const vc_sweep_out *out, void *ws,
+                       size_t ws_bytes, void *stream) {
+  g_last_error.clear();
+  if (out == nullptr) return fail(VC_ERR_NULL, "output descriptor is NULL");
+  if (out->stats == nullptr && n_cases > 0) return fail(VC_ERR_NULL, "out->stats is NULL");
+  vc_sweep_opts o{};
+  if (opts != nullptr) o = *opts;
+  if (o.do_integrity == 1 && out->integ == nullptr && n_cases > 0)
+    return fail(VC_ERR_NULL, "do_integrity is set but out->integ is NULL");
+  const bool want_tiles = out->tile_maps != nullptr;
+  const bool want_firstk = out->first_k != nullptr;
+  if (o.k > 0 && !want_firstk) o.k = 0;
+  Plan plan;
+  vc_status st = make_plan(cases, n_cases, tols, n_tols, o, want_tiles, want_firstk, false, plan);
+  if (st != VC_OK) return st;
+  Outputs oo;
+  oo.stats = out->stats;
+  oo.mismatches = out->mismatches;
+  oo.pass = out->pass;
+  oo.match_rate = out->match_rate;
+  oo.numeric_rate = out->numeric_rate;
+  oo.tile_maps = out->tile_maps;
+  oo.first_k = out->first_k;
+  oo.integ = out->integ;
+  return run(plan, tols, oo, ws, ws_bytes, (hipStream_t)stream, false);
+}
+
+vc_status vcheck_workspace_bytes(const vc_case *cases, int32_t n_cases, int32_t n_tols,
+                                 const vc_sweep_opts *opts, size_t *bytes) {
+  g_last_error.clear();
+  if (bytes == nullptr) return fail(VC_ERR_NULL, "bytes is NULL");
+  vc_sweep_opts o{};
+  if (opts != nullptr) o = *opts;
+  if (n_tols < 1 || n_tols > VC_MAX_TOLS)
+    return fail(VC_ERR_LIMIT, "n_tols %d outside 1..%d", n_tols, VC_MAX_TOLS);
+  // sizing does not depend on tolerance values or tile geometry
+  vc_tol dummy[VC_MAX_TOLS];
+  for (auto &t : dummy) t = vc_tol{0.0, 0.0, 0, 0};
+  o.tile_h = o.tile_h < 1 ? 1 : o.tile_h;
+  o.tile_w = o.tile_w < 1 ? 1 : o.tile_w;
+  if (o.primary_tol < 0 || o.primary_tol >= n_tols) o.primary_tol = 0;
+  Plan plan;
+  const vc_status st = make_plan(cases, n_cases, dummy, n_tols, o, false, o.k > 0, false, plan);
+  if (st != VC_OK) return st;
+  *bytes = plan.bytes;
+  return VC_OK;
+}
+
+int64_t vcheck_tile_count(const vc_tensor *t, int32_t tile_h, int32_t tile_w) {
+  if (t == nullptr || tile_h < 1 || tile_w < 1) return -1;
+  const int64_t n = numel_of(*t);
+  if (n < 0) return -1;
+  if (n == 0) return 0;
+  const uint64_t cols = cols_of(*t);
+  const uint64_t rows = (uint64_t)n / cols;
+  return (int64_t)(((rows + tile_h - 1) / tile_h) * ((cols + tile_w - 1) / tile_w));
+}
+
+const char *vcheck_status_str(vc_status status) {
+  switch (status) {
+    case VC_OK: return "ok";
+    case VC_ERR_NULL: return "a required pointer is NULL";
+    case VC_ERR_DTYPE: return "unknown dtype or cand/ref dtypes differ";
+    case VC_ERR_SHAPE: return "bad shape or cand/ref shapes differ";
+    case VC_ERR_TOL: return "invalid tolerance";
+    case VC_ERR_TILE: return "invalid tile size";
+    case VC_ERR_K: return "invalid first-k length";
+    case VC_ERR_WORKSPACE: return "workspace missing or too small";
+    case VC_ERR_LIMIT: return "a count is outside its supported range";
+    case VC_ERR_HIP: return "HIP runtime error";
+    case VC_ERR_ALIGN: return "data pointer not aligned to its element size";
+    default: return "unknown status";
+  }
+}
+
+const char *vcheck_last_error(void) { return g_last_error.c_str(); }
+
+int32_t vcheck_abi_version(void) { return VCHECK_ABI_VERSION; }
+
+vc_status vcheck_profile_events(void *begin_event, void *end_event) {
+  g_last_error.clear();
+  if ((begin_event == nullptr) != (end_event == nullptr))
+    return fail(VC_ERR_NULL, "profile events must both be set or both be NULL");
+  g_prof_begin = (hipEvent_t)begin_event;
+  g_prof_end = (hipEvent_t)end_event;
+  return VC_OK;
+}
+
+}  // extern "C"
