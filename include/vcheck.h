@@ -174,7 +174,9 @@ typedef struct vc_sweep_out {
                              certified = pass and (no integrity run or flags == 0) */
   double *numeric_rate;   /* [n_tols]: passing cases / n_cases, nullable */
   uint32_t *tile_maps;    /* concatenated per-case tile maps, nullable; case i
-                             starts at sum_{j<i} vcheck_tile_count(case j) */
+                             starts at sum_{j<i} vcheck_tile_count(ref of case j)
+                             (cases with a negative case_status keep their slots,
+                             which stay 0) */
   int64_t *first_k;       /* [n_cases * k], -1 padded, nullable */
   vc_integrity *integ;    /* [n_cases], required iff do_integrity */
 } vc_sweep_out;

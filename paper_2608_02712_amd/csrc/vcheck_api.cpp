@@ -101,8 +101,10 @@ struct Plan {
   size_t off_table = 0, off_recs = 0, off_stage = 0, off_pass = 0, off_flags = 0, bytes = 0;
 };
 
-// Elements per wave range: about 16K waves over the group, 1 Ki .. 64 KiB of
-// each tensor per wave, a power of two (so every range is 16-byte aligned).
+// Elements per wave (a chunk is four of them): about 8K waves over the
+// group, between 1 Ki elements and 64 KiB of each tensor per wave, a power of
+// two (so every step is 16-byte aligned). Long wave ranges amortize the
+// per-wave setup and the running-maximum records (about ln(steps) of them).
 uint32_t unit_for(uint64_t group_elems, int32_t dtype) {
   const uint64_t lo = 1024, hi = 65536 / elem_size(dtype);
   uint64_t u = lo;
@@ -182,6 +184,12 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
     d.dtype = (uint32_t)c.ref.dtype;
     const int64_t n = numel_of(c.ref);
     d.numel = (uint64_t)n;
+    // every case, evaluated or not, owns vcheck_tile_count(ref) tile slots
+    if (want_tiles && n > 0) {
+      const uint64_t cols = cols_of(c.ref), rows = (uint64_t)n / cols;
+      tile_count[i] = ((rows + opts.tile_h - 1) / opts.tile_h) *
+                      ((cols + opts.tile_w - 1) / opts.tile_w);
+    }
     if (st != VC_OK) {
       d.status = st;
       continue;
@@ -202,11 +210,7 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
       }
     }
     d.vec_ok = vec ? 1u : 0u;
-    if (want_tiles && n > 0) {
-      const uint64_t rows = (uint64_t)n / d.cols;
-      d.tiles_c = (d.cols + opts.tile_w - 1) / opts.tile_w;
-      tile_count[i] = ((rows + opts.tile_h - 1) / opts.tile_h) * d.tiles_c;
-    }
+    if (want_tiles && n > 0) d.tiles_c = (d.cols + opts.tile_w - 1) / opts.tile_w;
   }
   // tile-map offsets follow the caller's case order
   if (want_tiles) {

@@ -12,7 +12,7 @@ namespace vck {
 constexpr int kWaveSize = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWaveSize * kWavesPerBlock;
-constexpr int kTileWindow = 1024;  // LDS tile counters per wave
+constexpr int kTileWindow = 2048;  // LDS tile counters per block
 
 // Device-side case descriptor. The host builds one per case, in launch
 // order (grouped by dtype), and uploads the table into the workspace.
@@ -36,14 +36,13 @@ struct DevCase {
 };
 static_assert(sizeof(DevCase) == 152, "DevCase layout");
 
-// Partial result of one chunk (one block of the main kernel: four
-// consecutive wave ranges of one case). Offsets are element offsets within
-// the chunk.
+// Partial result of one chunk (one block of the main kernel; its four waves
+// interleave over the chunk). Offsets are element offsets within the chunk.
 struct ChunkRec {
   uint32_t mism[VC_MAX_TOLS];
   uint32_t nan_c, inf_c, nan_r, inf_r;
   uint32_t n_fin, n_rel, n_rel_undef, eq_bits;  // eq_bits: see kEq* below
-  uint32_t nfound[kWavesPerBlock];              // first-k entries staged per wave
+  uint32_t nfound[kWavesPerBlock];              // staged first-k entries (all in slot 0)
   uint32_t zero_c, zero_r, eqf_c, eqf_r;
   uint32_t bf_c, bf_r, f16_c, f16_r;
   double max_abs, max_rel;  // -1.0 when the chunk has no finite / no rel pair
@@ -74,6 +73,7 @@ struct Params {
   uint64_t case_hi;
   double atol[VC_MAX_TOLS];
   double rtol[VC_MAX_TOLS];
+
   ChunkRec *recs;        // [total chunks]
   uint32_t *stage;       // [total chunks * 4 * k] first-k staging (offsets)
   uint32_t *tile_maps;   // user tile maps (nullable)

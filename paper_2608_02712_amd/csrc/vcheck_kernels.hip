@@ -9,25 +9,32 @@
 // degenerate-output detector counts.
 //
 // Work decomposition: a case is cut into chunks of 4 * U elements; one block
-// (4 waves) owns one chunk and each wave one contiguous quarter of it, so
-// per-wave results combine in flat-index order. Each lane loads 16 bytes of
-// cand and 16 bytes of ref per step (one fully coalesced 1 KiB access per
-// wave and tensor), with the next step's loads issued before the current
-// step is evaluated.
+// (4 waves) owns one chunk and streams it front to back: a step is 64 lanes x
+// 16 bytes (one fully coalesced 1 KiB non-temporal load per tensor) and the
+// four waves take steps round robin, so the block's loads always target one
+// contiguous stretch of memory (this interleave reads HBM markedly faster
+// than one contiguous range per wave). The loop is unrolled twice so the
+// next step's loads are in flight while the current step is evaluated.
+// Per-wave results carry chunk offsets, so ties and first-k are resolved by
+// index, not by which wave saw an element first.
 //
-// Exactness: the gate is evaluated in binary64 on exactly decoded values with
-// separate rounding of rtol*|r| and atol + (.) (no contraction anywhere in
-// this file). Per-step fast path: when every pair of the step is finite and
-// every |r| is non-zero (detected by the finiteness of the step's approximate
-// relative-error sum), the counters are known without per-element class
-// tests; otherwise the step is redone element by element on the exact path
-// from the registers it already holds. max |c-r| is tracked exactly; max
-// |c-r|/|r| candidates are found with the exact sign test
-// fma(-M, |r|, d) > 0 <=> d/|r| > M and confirmed with a correctly rounded
-// division, so the reported maximum equals the correctly rounded quotient.
-// Only sum_rel uses an approximate reciprocal (it is specified to 1e-6
-// relative). Counts come from wave ballots and popcounts; no floating-point
-// atomics are used, so every result is bit-reproducible.
+// Exactness. The definition is binary64 on exactly decoded values (every
+// storage type widens exactly to binary32, and binary32 to binary64). Each
+// step first runs a fast path that evaluates the gate, |c - r| and |r| in
+// binary64 exactly as the definition (separately rounded rtol*|r| and
+// atol + (.), no contraction anywhere in this file), keeps the lane maximum
+// of |c - r| in binary64 and tests every element against the wave's exact
+// running maximum of |c - r|/|r| with the exact sign test
+// fma(-M, |r|, d) > 0 <=> d/|r| > M. Only an element that strictly beats a
+// running maximum reaches the update path (a correctly rounded division and a
+// wave reduction that keeps the smallest index on ties), so ties cost
+// nothing. The fast path assumes every value finite and every r non-zero
+// (checked through the finiteness of the lane's quotient estimates); a step
+// that breaks this is evaluated element by element with the class tests (the
+// exact path) from the registers it already holds. Only sum_rel uses binary32
+// quotient estimates (relative error below 5e-7, within the 1e-6 contract).
+// Counts come from wave ballots and popcounts; no floating-point atomics are
+// used, so every result is bit-reproducible.
 #pragma clang fp contract(off)
 
 #include "vcheck_internal.h"
@@ -53,31 +60,35 @@ struct Tr<VC_BF16> {
   static constexpr int ES = 2;
 };
 
-// Exact widening of one storage element to binary64.
+// 16 bytes of raw storage held by one lane.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Raw storage pattern of element j (0 <= j < V) of a 16-byte vector.
 template <int DT>
-__device__ __forceinline__ double decode(uint32_t raw) {
-  if constexpr (DT == VC_F32) {
-    return (double)__uint_as_float(raw);
-  } else if constexpr (DT == VC_F16) {
-    const _Float16 h = __builtin_bit_cast(_Float16, (uint16_t)raw);
-    return (double)(float)h;
+__device__ __forceinline__ uint32_t elem(const u32x4 &x, int j) {
+  if constexpr (Tr<DT>::ES == 4) {
+    return j == 0 ? x[0] : j == 1 ? x[1] : j == 2 ? x[2] : x[3];
   } else {
-    return (double)__uint_as_float(raw << 16);
+    const int w = j >> 1;
+    const uint32_t v = w == 0 ? x[0] : w == 1 ? x[1] : w == 2 ? x[2] : x[3];
+    return (j & 1) ? (v >> 16) : (v & 0xffffu);
   }
 }
 
+// Exact widening of one storage pattern to binary32 / binary64.
 template <int DT>
-__device__ __forceinline__ bool is_zero_bits(uint32_t raw) {
-  if constexpr (DT == VC_F32) return (raw & 0x7fffffffu) == 0;
-  else return (raw & 0x7fffu) == 0;
+__device__ __forceinline__ float dec32(uint32_t raw) {
+  if constexpr (DT == VC_F32) {
+    return __uint_as_float(raw);
+  } else if constexpr (DT == VC_F16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)raw);
+  } else {
+    return __uint_as_float(raw << 16);
+  }
 }
-
-// binary16 holds the binary32 value exactly (NaN and +-Inf count): the
-// round trip through binary16 returns the value unchanged.
-__device__ __forceinline__ bool fp16_exact(uint32_t raw) {
-  const float f = __uint_as_float(raw);
-  const float rt = (float)(_Float16)f;
-  return rt == f || f != f;
+template <int DT>
+__device__ __forceinline__ double dec64(uint32_t raw) {
+  return (double)dec32<DT>(raw);
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
@@ -87,40 +98,45 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-template <int DT>
-__device__ __forceinline__ void load_vec(const uint8_t *p, uint32_t (&v)[Tr<DT>::V]) {
-  const uint4 x = *reinterpret_cast<const uint4 *>(p);
-  if constexpr (Tr<DT>::ES == 4) {
-    v[0] = x.x;
-    v[1] = x.y;
-    v[2] = x.z;
-    v[3] = x.w;
-  } else {
-    v[0] = x.x & 0xffffu;
-    v[1] = x.x >> 16;
-    v[2] = x.y & 0xffffu;
-    v[3] = x.y >> 16;
-    v[4] = x.z & 0xffffu;
-    v[5] = x.z >> 16;
-    v[6] = x.w & 0xffffu;
-    v[7] = x.w >> 16;
-  }
+// Loads through global-address-space pointers (the data pointers come from
+// the case table, so the compiler cannot infer it; generic loads would also
+// wait on the LDS counter).
+#define VCK_GLOBAL __attribute__((address_space(1)))
+#define VCK_CONST __attribute__((address_space(4)))
+
+// Streamed data is read once: non-temporal loads keep it from displacing
+// reused lines in the caches.
+__device__ __forceinline__ u32x4 load16(const uint8_t *p) {
+  return __builtin_nontemporal_load((const VCK_GLOBAL u32x4 *)(p));
 }
 
 // Element loads of positions idx0 .. idx0+V-1 below `end` (others read 0).
 template <int DT>
-__device__ __forceinline__ void load_guarded(const uint8_t *base, uint64_t idx0, uint64_t end,
-                                             uint32_t (&v)[Tr<DT>::V]) {
+__device__ __forceinline__ u32x4 load_guarded(const uint8_t *base, uint64_t idx0, uint64_t end) {
+  uint32_t v[Tr<DT>::V];
 #pragma unroll
   for (int j = 0; j < Tr<DT>::V; ++j) {
     const uint64_t i = idx0 + j;
     uint32_t x = 0;
     if (i < end) {
-      if constexpr (Tr<DT>::ES == 4) x = *reinterpret_cast<const uint32_t *>(base + i * 4);
-      else x = *reinterpret_cast<const uint16_t *>(base + i * 2);
+      if constexpr (Tr<DT>::ES == 4) x = *(const VCK_GLOBAL uint32_t *)(base + i * 4);
+      else x = *(const VCK_GLOBAL uint16_t *)(base + i * 2);
     }
     v[j] = x;
   }
+  u32x4 r;
+  if constexpr (Tr<DT>::ES == 4) {
+    r[0] = v[0];
+    r[1] = v[1];
+    r[2] = v[2];
+    r[3] = v[3];
+  } else {
+    r[0] = v[0] | (v[1] << 16);
+    r[1] = v[2] | (v[3] << 16);
+    r[2] = v[4] | (v[5] << 16);
+    r[3] = v[6] | (v[7] << 16);
+  }
+  return r;
 }
 
 struct WaveOut {
@@ -131,6 +147,30 @@ struct WaveOut {
   double max_abs, max_rel, sum_abs, sum_rel;
 };
 
+// Member-wise copy of a case descriptor read through the constant address
+// space (scalar loads).
+__device__ __forceinline__ DevCase load_case(const VCK_CONST DevCase *t) {
+  DevCase d;
+  d.cand = t->cand;
+  d.ref = t->ref;
+#pragma unroll
+  for (int q = 0; q < VC_MAX_INPUTS; ++q) d.inp[q] = t->inp[q];
+  d.numel = t->numel;
+  d.cols = t->cols;
+  d.chunk_begin = t->chunk_begin;
+  d.tile_off = t->tile_off;
+  d.tiles_c = t->tiles_c;
+  d.n_chunks = t->n_chunks;
+  d.status = t->status;
+  d.inp_mask = t->inp_mask;
+  d.vec_ok = t->vec_ok;
+  d.orig = t->orig;
+  d.dtype = t->dtype;
+  d.unit_elems = t->unit_elems;
+  d.reserved = 0;
+  return d;
+}
+
 __device__ __forceinline__ void max_merge(double &v, uint32_t &i, double ov, uint32_t oi) {
   if (ov > v || (ov == v && oi < i)) {
     v = ov;
@@ -138,79 +178,145 @@ __device__ __forceinline__ void max_merge(double &v, uint32_t &i, double ov, uin
   }
 }
 
+__device__ __forceinline__ double readfirstlane_f64(double x) {
+  const uint64_t b = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Wave-wide (largest value, smallest index) of the lanes' (v, i), returned
+// as wave-uniform values. Lanes with nothing pass v = -1 (real values are
+// >= 0) and i = 0xffffffff.
+__device__ __forceinline__ void wave_max(double &v, uint32_t &i) {
+#pragma unroll
+  for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
+    const double ov = __shfl_xor(v, m);
+    const uint32_t oi = __shfl_xor(i, m);
+    max_merge(v, i, ov, oi);
+  }
+  v = readfirstlane_f64(v);
+  i = __builtin_amdgcn_readfirstlane(i);
+}
+
+#ifndef VCK_WAVES_PER_EU
+#define VCK_WAVES_PER_EU 4
+#endif
+
 template <int DT, int NT, bool INTEG>
-__global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(VCK_WAVES_PER_EU)))
+void main_kernel(const Params P) {
   constexpr int V = Tr<DT>::V;
   constexpr int ES = Tr<DT>::ES;
-  constexpr uint32_t ITER = kWaveSize * V;
+  constexpr uint32_t ITER = kWaveSize * V;  // elements per wave step
+  constexpr uint32_t ALL = (1u << V) - 1u;
 
-  __shared__ uint32_t s_win[kWavesPerBlock][kTileWindow];
+  __shared__ uint32_t s_win[kTileWindow];   // block tile-count window
+  __shared__ uint32_t s_merged[VC_MAX_K];   // first-k merge of the four waves
   __shared__ WaveOut s_out[kWavesPerBlock];
+  // counters touched only by the exact path, per wave (kept out of scalar
+  // registers): nan_c, inf_c, nan_r, inf_r, n_fin, n_rel, n_rel_undef
+  __shared__ uint32_t s_rare[kWavesPerBlock][8];
 
   const uint32_t lane = threadIdx.x & (kWaveSize - 1);
-  const uint32_t wave = threadIdx.x / kWaveSize;
+  // wave index: uniform per wave (keeps every range bound in scalar registers)
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
   const uint64_t chunk = P.chunk_lo + blockIdx.x;
 
-  // Locate the case: the last table entry whose first chunk is <= chunk.
-  const DevCase *cs = &P.single;
-  if (P.cases != nullptr) {
+  // Locate the case: the last table entry whose first chunk is <= chunk
+  // (scalar loads through the constant address space).
+  const VCK_CONST DevCase *table = (const VCK_CONST DevCase *)P.cases;
+  uint64_t ci = 0;
+  if (table != nullptr) {
     uint64_t lo = P.case_lo, hi = P.case_hi - 1;
     while (lo < hi) {
       const uint64_t mid = (lo + hi + 1) / 2;
-      if (P.cases[mid].chunk_begin <= chunk) lo = mid;
+      if (table[mid].chunk_begin <= chunk) lo = mid;
       else hi = mid - 1;
     }
-    cs = &P.cases[lo];
+    ci = lo;
   }
-  const uint8_t *const cand = cs->cand;
-  const uint8_t *const ref = cs->ref;
-  const uint64_t numel = cs->numel;
-  const uint64_t cols = cs->cols;
-  const uint64_t tiles_c = cs->tiles_c;
-  const uint64_t tile_off = cs->tile_off;
-  const bool vec = cs->vec_ok != 0;
+  // a value copy (an lvalue selecting between the table and the by-value
+  // argument would force the whole argument struct into private memory)
+  DevCase dcs;
+  if (table != nullptr) dcs = load_case(table + ci);
+  else dcs = P.single;
+  const uint8_t *const cand = dcs.cand;
+  const uint8_t *const ref = dcs.ref;
+  const uint64_t numel = dcs.numel;
+  const uint64_t cols = dcs.cols;
+  const uint64_t tiles_c = dcs.tiles_c;
+  const uint64_t tile_off = dcs.tile_off;
+  const uint64_t chunk_begin = dcs.chunk_begin;
+  const bool vec = dcs.vec_ok != 0;
+  const uint32_t inp_mask = dcs.inp_mask;
   const uint64_t U = P.unit_elems;
-  const uint64_t cstart = (chunk - cs->chunk_begin) * (4 * U);
+  const uint64_t cstart = (chunk - chunk_begin) * (4 * U);
   const uint64_t cend = min(cstart + 4 * U, numel);
-  const uint64_t wlo = min(cstart + wave * U, cend);
-  const uint64_t whi = min(wlo + U, cend);
+  const int prim = P.primary;
+  // Params fields used by the step lambdas, as locals: the lambdas capture by
+  // reference, and a captured by-value argument would live in private memory.
+  const int32_t kk = P.k;
+  const bool do_tiles = P.do_tiles != 0;
+  const uint32_t eqnan_mask = P.eqnan_mask;
+  uint32_t *const tile_maps = P.tile_maps;
+  // tolerance pairs in registers (constant indices only: a runtime index into
+  // the kernel-argument struct would copy it to private memory)
+  double atol[NT], rtol[NT];
+#pragma unroll
+  for (int p = 0; p < NT; ++p) {
+    atol[p] = P.atol[p];
+    rtol[p] = P.rtol[p];
+  }
 
-  // per-lane running state
-  double run_abs = -1.0, run_rel = -1.0;
+
+  // per-lane binary64 sums
+  double acc_abs = 0.0, acc_rel = 0.0;
+  // wave-uniform exact running maxima (value, chunk offset)
+  double best_abs = -1.0, best_rel = -1.0;
   uint32_t arg_abs = 0xffffffffu, arg_rel = 0xffffffffu;
-  double sabs = 0.0, srel = 0.0;
+  // merge lane-local candidates into the wave's running maximum
+  auto merge_abs = [&](double v, uint32_t i) __attribute__((always_inline)) {
+    wave_max(v, i);
+    max_merge(best_abs, arg_abs, v, i);
+  };
+  auto merge_rel = [&](double v, uint32_t i) __attribute__((always_inline)) {
+    wave_max(v, i);
+    max_merge(best_rel, arg_rel, v, i);
+  };
   // wave-uniform counters
   uint32_t mism[NT];
 #pragma unroll
   for (int p = 0; p < NT; ++p) mism[p] = 0;
-  uint32_t nan_c = 0, inf_c = 0, nan_r = 0, inf_r = 0, n_fin = 0, n_rel = 0, n_rel_undef = 0;
+  uint32_t fast_steps = 0;  // steps committed by the fast path
+  if (lane < 8) s_rare[wave][lane] = 0;
   uint32_t zc = 0, zr = 0, efc = 0, efr = 0, bfc = 0, bfr = 0, hfc = 0, hfr = 0;
   uint64_t diff_cr = 0;
-  uint32_t eqc = INTEG ? cs->inp_mask : 0u, eqr = eqc;
+  uint32_t eqc = INTEG ? inp_mask : 0u, eqr = eqc;
   uint32_t nfound = 0;
   uint32_t first_c = 0, first_r = 0;
   if constexpr (INTEG) {
     if (numel > 0) {
       if constexpr (ES == 4) {
-        first_c = *reinterpret_cast<const uint32_t *>(cand);
-        first_r = *reinterpret_cast<const uint32_t *>(ref);
+        first_c = *(const VCK_GLOBAL uint32_t *)cand;
+        first_r = *(const VCK_GLOBAL uint32_t *)ref;
       } else {
-        first_c = *reinterpret_cast<const uint16_t *>(cand);
-        first_r = *reinterpret_cast<const uint16_t *>(ref);
+        first_c = *(const VCK_GLOBAL uint16_t *)cand;
+        first_r = *(const VCK_GLOBAL uint16_t *)ref;
       }
     }
   }
 
-  // Tile window: LDS counters for the tile-id range this wave can touch.
+  // Tile window: LDS counters for the tile-id range this chunk can touch.
   const uint32_t th = (uint32_t)P.tile_h, tw = (uint32_t)P.tile_w;
   bool win_ok = false;
   uint64_t win_base = 0;
-  if (P.do_tiles && wlo < whi) {
-    const uint64_t row_lo = wlo / cols, row_hi = (whi - 1) / cols;
+  if (do_tiles) {
+    const uint64_t row_lo = cstart / cols, row_hi = (cend - 1) / cols;
     uint64_t t_min, t_max;
     if (row_lo == row_hi) {
-      t_min = (row_lo / th) * tiles_c + (wlo - row_lo * cols) / tw;
-      t_max = (row_lo / th) * tiles_c + (whi - 1 - row_lo * cols) / tw;
+      t_min = (row_lo / th) * tiles_c + (cstart - row_lo * cols) / tw;
+      t_max = (row_lo / th) * tiles_c + (cend - 1 - row_lo * cols) / tw;
     } else {
       t_min = (row_lo / th) * tiles_c;
       t_max = (row_hi / th) * tiles_c + tiles_c - 1;
@@ -218,288 +324,338 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     win_ok = (t_max - t_min) < (uint64_t)kTileWindow;
     win_base = t_min;
     if (win_ok)
-      for (uint32_t e = lane; e < (uint32_t)kTileWindow; e += kWaveSize) s_win[wave][e] = 0;
-    __builtin_amdgcn_wave_barrier();
+      for (uint32_t e = threadIdx.x; e < (uint32_t)kTileWindow; e += kBlockThreads) s_win[e] = 0;
+    __syncthreads();
   }
   uint32_t *const stage =
-      P.stage + ((uint64_t)chunk * kWavesPerBlock + wave) * (uint64_t)(P.k > 0 ? P.k : 0);
+      P.stage + ((uint64_t)chunk * kWavesPerBlock + wave) * (uint64_t)(kk > 0 ? kk : 0);
 
-  // Evaluate one step: V elements per lane starting at case index i0;
-  // element j is present iff bit j of vmask is set.
-  auto step = [&](const uint32_t (&cv)[V], const uint32_t (&rv)[V], uint32_t vmask, bool full,
-                  uint64_t i0) {
+  // Localization of the primary-pair mismatches given by per-lane bit mask
+  // pb (bit j = element i0 + j): ordered first-k staging and tile counts.
+  auto localize = [&](uint32_t pb, uint64_t i0) __attribute__((always_inline)) {
     const uint32_t off0 = (uint32_t)(i0 - cstart);
-    uint32_t fb[NT];
-    bool done = false;
-    if (full) {
-      double dd[V], ar[V];
-      double s_a = 0.0, s_r = 0.0, dmax = 0.0;
-#pragma unroll
-      for (int p = 0; p < NT; ++p) fb[p] = 0;
+    if (kk > 0 && nfound < (uint32_t)kk) {
+      uint32_t before = 0, total = 0;
 #pragma unroll
       for (int j = 0; j < V; ++j) {
-        const double c = decode<DT>(cv[j]);
-        const double r = decode<DT>(rv[j]);
-        const double d = __builtin_fabs(c - r);
-        const double a = __builtin_fabs(r);
-        dd[j] = d;
-        ar[j] = a;
-#pragma unroll
-        for (int p = 0; p < NT; ++p) {
-          const double t = P.atol[p] + P.rtol[p] * a;
-          fb[p] |= (d <= t ? 0u : 1u) << j;
-        }
-        s_a += d;
-        s_r += d * __builtin_amdgcn_rcp(a);
-        dmax = __builtin_fmax(dmax, d);
+        const uint64_t b = ballot((pb >> j) & 1u);
+        before += lanes_below(b);
+        total += popc(b);
       }
-      // s_r is finite iff every c and r of the lane is finite and every r != 0
-      if (ballot(!__builtin_isfinite(s_r)) == 0) {
-        done = true;
-        n_fin += ITER;
-        n_rel += ITER;
-        sabs += s_a;
-        srel += s_r;
-        if (ballot(dmax > run_abs) != 0) {
-          if (dmax > run_abs) {
-#pragma unroll
-            for (int j = 0; j < V; ++j)
-              if (dd[j] > run_abs) {
-                run_abs = dd[j];
-                arg_abs = off0 + j;
-              }
-          }
-        }
-        bool rc = false;
-#pragma unroll
-        for (int j = 0; j < V; ++j) rc |= __builtin_fma(-run_rel, ar[j], dd[j]) > 0.0;
-        if (ballot(rc) != 0) {
-          if (rc) {
-#pragma unroll
-            for (int j = 0; j < V; ++j)
-              if (__builtin_fma(-run_rel, ar[j], dd[j]) > 0.0) {
-                const double q = dd[j] / ar[j];
-                if (q > run_rel) {
-                  run_rel = q;
-                  arg_rel = off0 + j;
-                }
-              }
-          }
-        }
+      uint32_t pos = nfound + before;
+      uint32_t bits = pb;
+      while (bits != 0) {
+        const int j = __builtin_ctz(bits);
+        bits &= bits - 1;
+        if (pos < (uint32_t)kk) stage[pos] = off0 + j;
+        ++pos;
       }
+      nfound = min(nfound + total, (uint32_t)kk);
     }
-    if (!done) {
-      // exact element-by-element path
-#pragma unroll
-      for (int p = 0; p < NT; ++p) fb[p] = 0;
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const bool valid = (vmask >> j) & 1u;
-        const double c = decode<DT>(cv[j]);
-        const double r = decode<DT>(rv[j]);
-        const bool c_nan = __builtin_isnan(c), c_inf = __builtin_isinf(c);
-        const bool r_nan = __builtin_isnan(r), r_inf = __builtin_isinf(r);
-        nan_c += popc(ballot(valid && c_nan));
-        inf_c += popc(ballot(valid && c_inf));
-        nan_r += popc(ballot(valid && r_nan));
-        inf_r += popc(ballot(valid && r_inf));
-        const bool fin = valid && !(c_nan || c_inf || r_nan || r_inf);
-        const double d = __builtin_fabs(c - r);
-        const double a = __builtin_fabs(r);
-#pragma unroll
-        for (int p = 0; p < NT; ++p) {
-          const double t = P.atol[p] + P.rtol[p] * a;
-          const bool close =
-              (c == r) || (fin && d <= t) || (((P.eqnan_mask >> p) & 1u) && c_nan && r_nan);
-          fb[p] |= ((valid && !close) ? 1u : 0u) << j;
-        }
-        const bool relok = fin && r != 0.0;
-        n_fin += popc(ballot(fin));
-        n_rel += popc(ballot(relok));
-        n_rel_undef += popc(ballot(fin && r == 0.0 && c != 0.0));
-        if (fin) {
-          sabs += d;
-          if (d > run_abs) {
-            run_abs = d;
-            arg_abs = off0 + j;
-          }
-        }
-        if (relok) {
-          const double q = d / a;
-          srel += q;
-          if (q > run_rel) {
-            run_rel = q;
-            arg_rel = off0 + j;
-          }
-        }
-      }
-    }
-    // mismatch counts for every pair
-#pragma unroll
-    for (int p = 0; p < NT; ++p)
-#pragma unroll
-      for (int j = 0; j < V; ++j) mism[p] += popc(ballot((fb[p] >> j) & 1u));
-
-    // localization at the primary pair
-    uint32_t pb = 0;
-#pragma unroll
-    for (int p = 0; p < NT; ++p)
-      if (p == P.primary) pb = fb[p];
-    if (ballot(pb != 0) != 0) {
-      if (P.k > 0 && nfound < (uint32_t)P.k) {
-        uint32_t before = 0, total = 0;
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const uint64_t b = ballot((pb >> j) & 1u);
-          before += lanes_below(b);
-          total += popc(b);
-        }
-        uint32_t pos = nfound + before;
-#pragma unroll
-        for (int j = 0; j < V; ++j)
-          if ((pb >> j) & 1u) {
-            if (pos < (uint32_t)P.k) stage[pos] = off0 + j;
-            ++pos;
-          }
-        nfound = min(nfound + total, (uint32_t)P.k);
-      }
-      if (P.do_tiles && pb != 0) {
-#pragma unroll
-        for (int j = 0; j < V; ++j)
-          if ((pb >> j) & 1u) {
-            const uint64_t i = i0 + j;
-            const uint64_t row = i / cols;
-            const uint64_t col = i - row * cols;
-            const uint64_t t = (row / th) * tiles_c + col / tw;
-            if (win_ok && t >= win_base && t - win_base < (uint64_t)kTileWindow)
-              atomicAdd(&s_win[wave][t - win_base], 1u);
-            else
-              atomicAdd(&P.tile_maps[tile_off + t], 1u);
-          }
-      }
-    }
-
-    // degenerate-output detector counts
-    if constexpr (INTEG) {
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const bool valid = (vmask >> j) & 1u;
-        const uint32_t c = cv[j], r = rv[j];
-        zc += popc(ballot(valid && is_zero_bits<DT>(c)));
-        zr += popc(ballot(valid && is_zero_bits<DT>(r)));
-        efc += popc(ballot(valid && c == first_c));
-        efr += popc(ballot(valid && r == first_r));
-        if constexpr (DT == VC_F32) {
-          bfc += popc(ballot(valid && (c & 0xffffu) == 0));
-          bfr += popc(ballot(valid && (r & 0xffffu) == 0));
-          hfc += popc(ballot(valid && fp16_exact(c)));
-          hfr += popc(ballot(valid && fp16_exact(r)));
-        }
-        diff_cr |= ballot(valid && c != r);
-      }
-      // operator inputs: read only while cand or ref is still bit-equal
-      uint32_t need = eqc | eqr;
-      while (need != 0) {
-        const int jx = __builtin_ctz(need);
-        need &= need - 1;
-        const uint8_t *xp = cs->inp[jx];
-        uint32_t xv[V];
-        if (vec && full) load_vec<DT>(xp + i0 * ES, xv);
-        else load_guarded<DT>(xp, i0, whi, xv);
-        bool dc = false, dr = false;
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const bool valid = (vmask >> j) & 1u;
-          dc |= valid && cv[j] != xv[j];
-          dr |= valid && rv[j] != xv[j];
-        }
-        if (ballot(dc) != 0) eqc &= ~(1u << jx);
-        if (ballot(dr) != 0) eqr &= ~(1u << jx);
+    if (do_tiles) {
+      uint32_t bits = pb;
+      while (bits != 0) {
+        const int j = __builtin_ctz(bits);
+        bits &= bits - 1;
+        const uint64_t i = i0 + j;
+        const uint64_t row = i / cols;
+        const uint64_t col = i - row * cols;
+        const uint64_t t = (row / th) * tiles_c + col / tw;
+        if (win_ok && t >= win_base && t - win_base < (uint64_t)kTileWindow)
+          atomicAdd(&s_win[t - win_base], 1u);
+        else
+          atomicAdd(&tile_maps[tile_off + t], 1u);
       }
     }
   };
 
-  const uint64_t n_elems = whi - wlo;
-  const uint64_t n_full = n_elems / ITER;
-  const uint64_t lane_off = (uint64_t)lane * V;
-  uint32_t c_cur[V], r_cur[V];
-  const uint32_t all = (1u << V) - 1u;
-  if (n_full > 0) {
-    const uint64_t i0 = wlo + lane_off;
-    if (vec) {
-      load_vec<DT>(cand + i0 * ES, c_cur);
-      load_vec<DT>(ref + i0 * ES, r_cur);
-    } else {
-      load_guarded<DT>(cand, i0, whi, c_cur);
-      load_guarded<DT>(ref, i0, whi, r_cur);
-    }
-  }
-  for (uint64_t it = 0; it < n_full; ++it) {
-    const uint64_t i0 = wlo + it * ITER + lane_off;
-    uint32_t c_nxt[V], r_nxt[V];
-    const bool more = it + 1 < n_full;
-    if (more) {
-      const uint64_t i1 = i0 + ITER;
-      if (vec) {
-        load_vec<DT>(cand + i1 * ES, c_nxt);
-        load_vec<DT>(ref + i1 * ES, r_nxt);
-      } else {
-        load_guarded<DT>(cand, i1, whi, c_nxt);
-        load_guarded<DT>(ref, i1, whi, r_nxt);
+  // Exact binary64 evaluation of one step (element by element).
+  auto exact_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, uint64_t i0) __attribute__((always_inline)) {
+    const uint32_t off0 = (uint32_t)(i0 - cstart);
+    uint32_t pb = 0;
+    uint32_t nan_c_step = 0, nan_r_step = 0, inf_c_step = 0, inf_r_step = 0;
+    uint32_t fin_step = 0, rel_step = 0, undef_step = 0;
+    double lb_abs = -1.0, lb_rel = -1.0;  // lane-local maxima of this step
+    uint32_t li_abs = 0xffffffffu, li_rel = 0xffffffffu;
+#pragma unroll 1
+    for (int j = 0; j < V; ++j) {
+      const bool valid = (vmask >> j) & 1u;
+      const double c = dec64<DT>(elem<DT>(cq, j));
+      const double r = dec64<DT>(elem<DT>(rq, j));
+      const bool c_nan = __builtin_isnan(c), c_inf = __builtin_isinf(c);
+      const bool r_nan = __builtin_isnan(r), r_inf = __builtin_isinf(r);
+      nan_c_step += popc(ballot(valid && c_nan));
+      inf_c_step += popc(ballot(valid && c_inf));
+      nan_r_step += popc(ballot(valid && r_nan));
+      inf_r_step += popc(ballot(valid && r_inf));
+      const bool fin = valid && !(c_nan || c_inf || r_nan || r_inf);
+      const double d = __builtin_fabs(c - r);
+      const double a = __builtin_fabs(r);
+#pragma unroll
+      for (int p = 0; p < NT; ++p) {
+        const double t = atol[p] + rtol[p] * a;
+        const bool close =
+            (c == r) || (fin && d <= t) || (((eqnan_mask >> p) & 1u) && c_nan && r_nan);
+        const bool f = valid && !close;
+        mism[p] += popc(ballot(f));
+        if (p == prim && f) pb |= 1u << j;
+      }
+      const bool relok = fin && r != 0.0;
+      fin_step += popc(ballot(fin));
+      rel_step += popc(ballot(relok));
+      undef_step += popc(ballot(fin && r == 0.0 && c != 0.0));
+      if (fin) {
+        acc_abs += d;
+        if (d > lb_abs) {
+          lb_abs = d;
+          li_abs = off0 + j;
+        }
+      }
+      if (relok) {
+        const double q = d / a;
+        acc_rel += q;
+        if (q > lb_rel) {
+          lb_rel = q;
+          li_rel = off0 + j;
+        }
       }
     }
-    step(c_cur, r_cur, all, true, i0);
-    if (more) {
+    merge_abs(lb_abs, li_abs);
+    merge_rel(lb_rel, li_rel);
+    if (lane == 0) {
+      uint32_t *const rc = s_rare[wave];
+      rc[0] += nan_c_step;
+      rc[1] += inf_c_step;
+      rc[2] += nan_r_step;
+      rc[3] += inf_r_step;
+      rc[4] += fin_step;
+      rc[5] += rel_step;
+      rc[6] += undef_step;
+    }
+    if constexpr (DT == VC_F32) {
+      // NaN is binary16-representable: count it with the representability tests
+      hfc += nan_c_step;
+      hfr += nan_r_step;
+    }
+    if (ballot(pb != 0) != 0) localize(pb, i0);
+  };
+
+  // Fast path for a full step; returns false (and changes nothing) when the
+  // step holds a NaN, an infinity or a zero reference (the exact path then
+  // does the per-element class tests). The gate, the running maxima and
+  // sum_abs are exact binary64; the lane's quotient estimates feed sum_rel.
+  auto fast_step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0) __attribute__((always_inline)) -> bool {
+    float sq0 = 0.f, sq1 = 0.f;
+    double sa = 0.0;
+    uint32_t fcnt[NT];
+#pragma unroll
+    for (int p = 0; p < NT; ++p) fcnt[p] = 0;
+    uint64_t pany = 0;
+    // lanes with an element whose |c - r| exceeds best_abs / whose exact
+    // quotient exceeds best_rel (per-element compares into wave masks; a
+    // per-lane OR would be rewritten by the compiler into a max reduction)
+    uint64_t absm = 0, relm = 0;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const float c32 = dec32<DT>(elem<DT>(cq, j));
+      const float r32 = dec32<DT>(elem<DT>(rq, j));
+      const double c = c32, r = r32;
+      const double d = __builtin_fabs(c - r);
+      const double a = __builtin_fabs(r);
+#pragma unroll
+      for (int p = 0; p < NT; ++p) {
+        const double t = atol[p] + rtol[p] * a;
+        const uint64_t f = ballot(!(d <= t));
+        fcnt[p] += popc(f);
+        if (p == prim) pany |= f;
+      }
+      sa += d;
+      absm |= ballot(d > best_abs);
+      relm |= ballot(__builtin_fma(-best_rel, a, d) > 0.0);
+      const float q = __builtin_fabsf((float)d * __builtin_amdgcn_rcpf(r32));
+      if (j & 1) sq1 += q;
+      else sq0 += q;
+    }
+    // finite iff every c and r of the lane is finite and every r != 0
+    if (ballot(!__builtin_isfinite(sq0 + sq1)) != 0) return false;
+#pragma unroll
+    for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
+    ++fast_steps;
+    acc_abs += sa;
+    acc_rel += (double)sq0 + (double)sq1;
+    const uint32_t off0 = (uint32_t)(i0 - cstart);
+    const uint64_t lane_bit = 1ull << lane;
+    if (absm != 0) {
+      double lb = -1.0;
+      uint32_t li = 0xffffffffu;
+      if (absm & lane_bit) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) {  // lane max, smallest j on ties
+          const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - dec64<DT>(elem<DT>(rq, j)));
+          if (d > lb) {
+            lb = d;
+            li = off0 + j;
+          }
+        }
+      }
+      merge_abs(lb, li);
+    }
+    if (relm != 0) {
+      double lb = -1.0;
+      uint32_t li = 0xffffffffu;
+      if (relm & lane_bit) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const double r = dec64<DT>(elem<DT>(rq, j));
+          const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
+          const double a = __builtin_fabs(r);
+          // exact sign test: d / a > best_rel  <=>  d - best_rel * a > 0
+          if (__builtin_fma(-best_rel, a, d) > 0.0) {
+            const double q = d / a;
+            if (q > lb) {
+              lb = q;
+              li = off0 + j;
+            }
+          }
+        }
+      }
+      merge_rel(lb, li);
+    }
+    if (pany != 0) {
+      uint32_t pb = 0;
+#pragma unroll 1
+      for (int j = 0; j < V; ++j) {
+        const double r = dec64<DT>(elem<DT>(rq, j));
+        const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
+        double t = 0.0;
+#pragma unroll
+        for (int p = 0; p < NT; ++p)
+          if (p == prim) t = atol[p] + rtol[p] * __builtin_fabs(r);
+        if (!(d <= t)) pb |= 1u << j;
+      }
+      localize(pb, i0);
+    }
+    return true;
+  };
+
+  // Degenerate-output detector counts of one step (bitwise; NaN handling of
+  // the binary16 test is added by the exact path).
+  auto integ_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, bool full,
+                        uint64_t i0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const bool valid = (vmask >> j) & 1u;
+      const uint32_t c = elem<DT>(cq, j), r = elem<DT>(rq, j);
+      const float cf = dec32<DT>(c), rf = dec32<DT>(r);
+      zc += popc(ballot(valid && cf == 0.0f));
+      zr += popc(ballot(valid && rf == 0.0f));
+      efc += popc(ballot(valid && c == first_c));
+      efr += popc(ballot(valid && r == first_r));
+      if constexpr (DT == VC_F32) {
+        bfc += popc(ballot(valid && (c & 0xffffu) == 0));
+        bfr += popc(ballot(valid && (r & 0xffffu) == 0));
+        hfc += popc(ballot(valid && (float)(_Float16)cf == cf));
+        hfr += popc(ballot(valid && (float)(_Float16)rf == rf));
+      }
+      diff_cr |= ballot(valid && c != r);
+    }
+    // operator inputs: read only while cand or ref is still bit-equal
+    uint32_t need = eqc | eqr;
+    while (need != 0) {
+      const int jx = __builtin_ctz(need);
+      need &= need - 1;
+      const uint8_t *xp = nullptr;
+#pragma unroll
+      for (int q = 0; q < VC_MAX_INPUTS; ++q)
+        if (q == jx) xp = dcs.inp[q];
+      const u32x4 xq = (vec && full) ? load16(xp + i0 * ES) : load_guarded<DT>(xp, i0, cend);
+      bool dc = false, dr = false;
 #pragma unroll
       for (int j = 0; j < V; ++j) {
-        c_cur[j] = c_nxt[j];
-        r_cur[j] = r_nxt[j];
+        const bool valid = (vmask >> j) & 1u;
+        const uint32_t x = elem<DT>(xq, j);
+        dc |= valid && elem<DT>(cq, j) != x;
+        dr |= valid && elem<DT>(rq, j) != x;
       }
+      if (ballot(dc) != 0) eqc &= ~(1u << jx);
+      if (ballot(dr) != 0) eqr &= ~(1u << jx);
+    }
+  };
+
+  auto step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0) __attribute__((always_inline)) {
+    if (!fast_step(cq, rq, i0)) exact_step(cq, rq, ALL, i0);
+    if constexpr (INTEG) integ_step(cq, rq, ALL, true, i0);
+  };
+
+  // Steps of ITER elements; wave w takes steps w, w+4, w+8, ... of the chunk,
+  // so the block streams its chunk front to back, one KiB per wave and tensor.
+  const uint64_t n_steps = (cend - cstart) / ITER;  // full steps in the chunk
+  const uint64_t n_full = n_steps > wave ? (n_steps - wave + 3) / 4 : 0;
+  const uint64_t lane_off = (uint64_t)lane * V;
+  auto step_i0 = [&](uint64_t st) __attribute__((always_inline)) { return cstart + (wave + 4 * st) * ITER + lane_off; };
+  if (vec) {
+    // Two steps per trip with the next step's loads in flight. The loads are
+    // unconditional (past the end they re-read the last step, a cache hit) so
+    // the wait counters stay exact across the loop.
+    const uint8_t *const cb = cand + cstart * ES;  // block-uniform bases
+    const uint8_t *const rb = ref + cstart * ES;
+    const uint32_t lane_b = lane * 16u;
+    const uint64_t last = n_full > 0 ? n_full - 1 : 0;
+    auto off = [&](uint64_t st) __attribute__((always_inline)) {
+      return (uint32_t)((wave + 4 * min(st, last)) * ITER * ES) + lane_b;
+    };
+    u32x4 ca = {0, 0, 0, 0}, ra = ca, cn = ca, rn = ca;
+    if (n_full > 0) {
+      ca = load16(cb + off(0));
+      ra = load16(rb + off(0));
+    }
+    for (uint64_t st = 0; st < n_full; st += 2) {
+      cn = load16(cb + off(st + 1));
+      rn = load16(rb + off(st + 1));
+      step(ca, ra, step_i0(st));
+      if (st + 1 >= n_full) break;
+      ca = load16(cb + off(st + 2));
+      ra = load16(rb + off(st + 2));
+      step(cn, rn, step_i0(st + 1));
+    }
+  } else {
+    for (uint64_t st = 0; st < n_full; ++st) {
+      const uint64_t i0 = step_i0(st);
+      const u32x4 cq = load_guarded<DT>(cand, i0, cend);
+      const u32x4 rq = load_guarded<DT>(ref, i0, cend);
+      step(cq, rq, i0);
     }
   }
-  if (n_elems % ITER != 0) {
-    const uint64_t i0 = wlo + n_full * ITER + lane_off;
-    load_guarded<DT>(cand, i0, whi, c_cur);
-    load_guarded<DT>(ref, i0, whi, r_cur);
+  if ((cend - cstart) % ITER != 0 && n_steps % 4 == wave) {
+    const uint64_t i0 = cstart + n_steps * ITER + lane_off;
+    const u32x4 ct = load_guarded<DT>(cand, i0, cend);
+    const u32x4 rt = load_guarded<DT>(ref, i0, cend);
     uint32_t vmask = 0;
 #pragma unroll
-    for (int j = 0; j < V; ++j) vmask |= (i0 + j < whi ? 1u : 0u) << j;
-    step(c_cur, r_cur, vmask, false, i0);
+    for (int j = 0; j < V; ++j) vmask |= (i0 + j < cend ? 1u : 0u) << j;
+    exact_step(ct, rt, vmask, i0);
+    if constexpr (INTEG) integ_step(ct, rt, vmask, false, i0);
   }
 
-  // flush the tile window
-  if (P.do_tiles && win_ok) {
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    for (uint32_t e = lane; e < (uint32_t)kTileWindow; e += kWaveSize) {
-      const uint32_t v = s_win[wave][e];
-      if (v != 0) atomicAdd(&P.tile_maps[tile_off + win_base + e], v);
-    }
-  }
 
   // wave reduction (fixed butterfly order)
 #pragma unroll
   for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
-    sabs += __shfl_xor(sabs, m);
-    srel += __shfl_xor(srel, m);
-    const double oa = __shfl_xor(run_abs, m);
-    const uint32_t ia = __shfl_xor(arg_abs, m);
-    max_merge(run_abs, arg_abs, oa, ia);
-    const double orl = __shfl_xor(run_rel, m);
-    const uint32_t irl = __shfl_xor(arg_rel, m);
-    max_merge(run_rel, arg_rel, orl, irl);
+    acc_abs += __shfl_xor(acc_abs, m);
+    acc_rel += __shfl_xor(acc_rel, m);
   }
   if (lane == 0) {
     WaveOut &o = s_out[wave];
 #pragma unroll
     for (int p = 0; p < VC_MAX_TOLS; ++p) o.mism[p] = p < NT ? mism[p] : 0u;
-    o.nan_c = nan_c;
-    o.inf_c = inf_c;
-    o.nan_r = nan_r;
-    o.inf_r = inf_r;
-    o.n_fin = n_fin;
-    o.n_rel = n_rel;
-    o.n_rel_undef = n_rel_undef;
+    const uint32_t *const rc = s_rare[wave];
+    o.nan_c = rc[0];
+    o.inf_c = rc[1];
+    o.nan_r = rc[2];
+    o.inf_r = rc[3];
+    o.n_fin = rc[4] + fast_steps * ITER;
+    o.n_rel = rc[5] + fast_steps * ITER;
+    o.n_rel_undef = rc[6];
     o.eq_bits = (diff_cr == 0 ? kEqCandRef : 0u) | (eqc << kEqCandInpShift) |
                 (eqr << kEqRefInpShift);
     o.nfound = nfound;
@@ -511,14 +667,57 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     o.bfr = bfr;
     o.hfc = hfc;
     o.hfr = hfr;
-    o.max_abs = run_abs;
+    o.max_abs = best_abs;
     o.amax_abs = arg_abs;
-    o.max_rel = run_rel;
+    o.max_rel = best_rel;
     o.amax_rel = arg_rel;
-    o.sum_abs = sabs;
-    o.sum_rel = srel;
+    o.sum_abs = acc_abs;
+    o.sum_rel = acc_rel;
   }
   __syncthreads();
+  // flush the tile window (all four waves are done with it)
+  if (do_tiles && win_ok) {
+    for (uint32_t e = threadIdx.x; e < (uint32_t)kTileWindow; e += kBlockThreads) {
+      const uint32_t v = s_win[e];
+      if (v != 0) atomicAdd(&tile_maps[tile_off + win_base + e], v);
+    }
+  }
+  // Merge the four waves' ascending first-k lists (disjoint index sets) into
+  // the k smallest: an entry's rank is its position in its own list plus the
+  // number of smaller entries in the other three.
+  uint32_t merged = 0;
+  if (kk > 0) {
+    const uint32_t k = (uint32_t)kk;
+    uint32_t nf[kWavesPerBlock], total = 0;
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      nf[w] = s_out[w].nfound;
+      total += nf[w];
+    }
+    if (total > 0) {
+      const uint32_t *base = P.stage + (uint64_t)chunk * kWavesPerBlock * k;
+      for (uint32_t e = threadIdx.x; e < kWavesPerBlock * k; e += kBlockThreads) {
+        const uint32_t w = e / k, i = e % k;
+        if (i >= nf[w]) continue;
+        const uint32_t x = base[w * k + i];
+        uint32_t rank = i;
+        for (uint32_t v = 0; v < (uint32_t)kWavesPerBlock; ++v) {
+          if (v == w) continue;
+          uint32_t lo = 0, hi = nf[v];  // count of list v below x
+          while (lo < hi) {
+            const uint32_t mid = (lo + hi) / 2;
+            if (base[v * k + mid] < x) lo = mid + 1;
+            else hi = mid;
+          }
+          rank += lo;
+        }
+        if (rank < k) s_merged[rank] = x;
+      }
+      merged = min(total, k);
+      __syncthreads();
+      for (uint32_t e = threadIdx.x; e < merged; e += kBlockThreads)
+        P.stage[(uint64_t)chunk * kWavesPerBlock * k + e] = s_merged[e];
+    }
+  }
   if (threadIdx.x == 0) {
     ChunkRec rec;
     const WaveOut &w0 = s_out[0];
@@ -546,7 +745,6 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     rec.amax_rel = w0.amax_rel;
     rec.sum_abs = w0.sum_abs;
     rec.sum_rel = w0.sum_rel;
-    rec.nfound[0] = w0.nfound;
     for (int w = 1; w < kWavesPerBlock; ++w) {
       const WaveOut &o = s_out[w];
 #pragma unroll
@@ -571,8 +769,9 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       max_merge(rec.max_rel, rec.amax_rel, o.max_rel, o.amax_rel);
       rec.sum_abs += o.sum_abs;
       rec.sum_rel += o.sum_rel;
-      rec.nfound[w] = o.nfound;
     }
+    rec.nfound[0] = merged;
+    for (int w = 1; w < kWavesPerBlock; ++w) rec.nfound[w] = 0;
     rec.pad0 = rec.pad1 = 0;
     P.recs[chunk] = rec;
   }
@@ -680,7 +879,9 @@ __device__ uint32_t block_exscan_u32(FinScratch &s, uint32_t x, uint32_t &total)
 __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P) {
   __shared__ FinScratch s;
   const uint64_t ci = P.case_lo + blockIdx.x;
-  const DevCase &cs = P.cases != nullptr ? P.cases[ci] : P.single;
+  DevCase cs;
+  if (P.cases != nullptr) cs = load_case((const VCK_CONST DevCase *)P.cases + ci);
+  else cs = P.single;
   const uint32_t oi = cs.orig;
   const int nt = P.n_tols;
   const uint64_t CH = 4ull * cs.unit_elems;
