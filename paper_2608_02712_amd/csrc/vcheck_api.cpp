@@ -2,6 +2,7 @@
 // argument validation (before anything is enqueued), work planning, workspace
 // layout, descriptor upload and kernel launches.
 #include <algorithm>
+#include <cfloat>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -93,22 +94,35 @@ struct Group {
 
 struct Plan {
   std::vector<vck::DevCase> table;
+  std::vector<uint64_t> case_chunk;  // chunk_begin per table entry
+  std::vector<uint64_t> case_group;  // group_begin per table entry
   std::vector<Group> groups;
   uint64_t total_chunks = 0;
+  uint64_t total_groups = 0;
   uint64_t tiles_total = 0;
   int32_t n_cases = 0, n_tols = 1, nt_class = 1, k = 0, primary = 0, tile_h = 1, tile_w = 1;
   bool do_tiles = false, do_firstk = false, do_integ = false;
-  size_t off_table = 0, off_recs = 0, off_stage = 0, off_pass = 0, off_flags = 0, bytes = 0;
+  // workspace layout: [table | case_chunk | case_group] (the blob the
+  // prologue copies), chunk records, chunk staging, group records, group
+  // staging, then the counter area the prologue clears: Counters, case_cnt
+  size_t off_table = 0, off_cc = 0, off_cg = 0, blob_bytes = 0;
+  size_t off_recs = 0, off_stage = 0, off_grecs = 0, off_gstage = 0;
+  size_t off_ctr = 0, off_case_cnt = 0, ctr_bytes = 0;
+  size_t bytes = 0;
 };
 
-// Elements per wave (a chunk is four of them): about 8K waves over the
+// Elements per wave (a chunk is four of them): about 32K waves over the
 // group, between 1 Ki elements and 64 KiB of each tensor per wave, a power of
-// two (so every step is 16-byte aligned). Long wave ranges amortize the
-// per-wave setup and the running-maximum records (about ln(steps) of them).
+// two (so every step is 16-byte aligned). Many short chunks keep every CU
+// streaming until the end of the launch; longer ones amortize the per-block
+// setup and the running-maximum records.
+#ifndef VCK_WAVE_TARGET
+#define VCK_WAVE_TARGET 32768
+#endif
 uint32_t unit_for(uint64_t group_elems, int32_t dtype) {
   const uint64_t lo = 1024, hi = 65536 / elem_size(dtype);
   uint64_t u = lo;
-  while (u < hi && u * 2 * 16384 <= group_elems) u *= 2;
+  while (u < hi && u * 2 * VCK_WAVE_TARGET <= group_elems) u *= 2;
   return (uint32_t)u;
 }
 
@@ -222,7 +236,7 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
     plan.tiles_total = acc;
   }
   // group by dtype (stable): F32, F16, BF16; chunks numbered in table order
-  uint64_t chunk = 0;
+  uint64_t chunk = 0, group = 0;
   for (int32_t dt : {VC_F32, VC_F16, VC_BF16}) {
     Group g{};
     g.dtype = dt;
@@ -237,41 +251,60 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
       vck::DevCase d = dc[i];
       d.unit_elems = g.unit;
       d.chunk_begin = chunk;
+      d.group_begin = group;
       const uint64_t ch = 4ull * g.unit;
-      const uint64_t nc = d.status == 0 ? (d.numel + ch - 1) / ch : 0;
+      // a case that is not evaluated, or is empty, still owns one (empty)
+      // chunk: its results are written by the same completion path
+      uint64_t nc = d.status == 0 ? (d.numel + ch - 1) / ch : 0;
+      if (nc == 0) nc = 1;
       if (nc > 0xffffffffull) return fail(VC_ERR_LIMIT, "case %d is too large", (int)d.orig);
       d.n_chunks = (uint32_t)nc;
+      d.n_groups = (uint32_t)((nc + vck::kGroupChunks - 1) / vck::kGroupChunks);
       chunk += nc;
+      group += d.n_groups;
       plan.table.push_back(d);
+      plan.case_chunk.push_back(d.chunk_begin);
+      plan.case_group.push_back(d.group_begin);
     }
     g.case_hi = plan.table.size();
     g.n_chunks = chunk - g.chunk_lo;
     if (g.case_hi > g.case_lo) plan.groups.push_back(g);
   }
   plan.total_chunks = chunk;
+  plan.total_groups = group;
 
   // workspace layout
+  const size_t nc = (size_t)n_cases;
   size_t off = 0;
   plan.off_table = off;
-  off += align_up(sizeof(vck::DevCase) * (size_t)n_cases);
+  plan.off_cc = off + sizeof(vck::DevCase) * nc;  // 160 * n: 16-byte aligned
+  plan.off_cg = plan.off_cc + sizeof(uint64_t) * nc;
+  plan.blob_bytes = (sizeof(vck::DevCase) * nc + 2 * sizeof(uint64_t) * nc + 15) / 16 * 16;
+  off += align_up(plan.blob_bytes);
   plan.off_recs = off;
   off += align_up(sizeof(vck::ChunkRec) * (size_t)plan.total_chunks);
   plan.off_stage = off;
   off += align_up(sizeof(uint32_t) * (size_t)plan.total_chunks * vck::kWavesPerBlock *
                   (size_t)plan.k);
-  plan.off_pass = off;
-  off += align_up((size_t)n_cases * (size_t)n_tols);
-  plan.off_flags = off;
-  off += align_up(sizeof(uint32_t) * (size_t)n_cases);
+  plan.off_grecs = off;
+  off += align_up(sizeof(vck::ChunkRec) * (size_t)plan.total_groups);
+  plan.off_gstage = off;
+  off += align_up(sizeof(uint32_t) * (size_t)plan.total_groups * (size_t)plan.k);
+  plan.off_ctr = off;
+  plan.off_case_cnt = off + sizeof(vck::Counters);
+  plan.ctr_bytes = plan.off_case_cnt + sizeof(uint32_t) * nc - off;
+  off += align_up(plan.ctr_bytes);
   plan.bytes = off + kAlign;  // slack for aligning the caller's base pointer
   return VC_OK;
 }
 
 // ---- pinned staging for descriptor uploads ---------------------------------
-// A small ring of pinned host buffers per device. A slot is reused only after
-// the event recorded behind its previous copy has completed.
+// A small ring of pinned host buffers per device. The prologue kernel reads
+// the descriptor blob straight from the pinned buffer; a slot is reused only
+// after the event recorded behind that kernel has completed.
 struct Slot {
   void *host = nullptr;
+  void *dev = nullptr;  // device-visible address of `host`
   size_t cap = 0;
   hipEvent_t ev = nullptr;
   bool pending = false;
@@ -284,45 +317,51 @@ struct DeviceStaging {
 constexpr int kMaxDevices = 64;
 DeviceStaging g_staging[kMaxDevices];
 
-vc_status upload(void *dst, const void *src, size_t bytes, hipStream_t s) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(VC_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
-  if (dev < 0 || dev >= kMaxDevices) return fail(VC_ERR_HIP, "device id %d out of range", dev);
-  DeviceStaging &ds = g_staging[dev];
-  std::lock_guard<std::mutex> lock(ds.mu);
-  Slot &sl = ds.slots[ds.next];
-  ds.next = (ds.next + 1) % 8;
-  if (sl.pending) {
-    e = hipEventSynchronize(sl.ev);
-    if (e != hipSuccess) return fail(VC_ERR_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
-    sl.pending = false;
-  }
-  if (sl.ev == nullptr) {
-    e = hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming);
-    if (e != hipSuccess) return fail(VC_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(e));
-  }
-  if (sl.cap < bytes) {
-    if (sl.host != nullptr) (void)hipHostFree(sl.host);
-    sl.host = nullptr;
-    sl.cap = 0;
-    const size_t cap = std::max<size_t>(bytes, 64 * 1024);
-    e = hipHostMalloc(&sl.host, cap, hipHostMallocDefault);
-    if (e != hipSuccess) return fail(VC_ERR_HIP, "hipHostMalloc: %s", hipGetErrorString(e));
-    sl.cap = cap;
-  }
-  memcpy(sl.host, src, bytes);
-  e = hipMemcpyAsync(dst, sl.host, bytes, hipMemcpyHostToDevice, s);
-  if (e != hipSuccess) return fail(VC_ERR_HIP, "hipMemcpyAsync: %s", hipGetErrorString(e));
-  e = hipEventRecord(sl.ev, s);
-  if (e != hipSuccess) return fail(VC_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
-  sl.pending = true;
-  return VC_OK;
-}
-
 vc_status hip_check(hipError_t e, const char *what) {
   if (e == hipSuccess) return VC_OK;
   return fail(VC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Takes the next slot of the current device (waiting for its previous use)
+// and fills it with `bytes` bytes of `src`. The caller holds `lock` until it
+// has recorded the slot's event behind the kernel that reads it.
+vc_status stage_blob(const void *src, size_t bytes, std::unique_lock<std::mutex> &lock,
+                     Slot *&slot) {
+  int dev = 0;
+  vc_status st = hip_check(hipGetDevice(&dev), "hipGetDevice");
+  if (st != VC_OK) return st;
+  if (dev < 0 || dev >= kMaxDevices) return fail(VC_ERR_HIP, "device id %d out of range", dev);
+  DeviceStaging &ds = g_staging[dev];
+  lock = std::unique_lock<std::mutex>(ds.mu);
+  Slot &sl = ds.slots[ds.next];
+  ds.next = (ds.next + 1) % 8;
+  if (sl.pending) {
+    st = hip_check(hipEventSynchronize(sl.ev), "hipEventSynchronize");
+    if (st != VC_OK) return st;
+    sl.pending = false;
+  }
+  if (sl.ev == nullptr) {
+    st = hip_check(hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming), "hipEventCreate");
+    if (st != VC_OK) return st;
+  }
+  if (sl.cap < bytes) {
+    if (sl.host != nullptr) (void)hipHostFree(sl.host);
+    sl.host = sl.dev = nullptr;
+    sl.cap = 0;
+    const size_t cap = std::max<size_t>(bytes, 64 * 1024);
+    st = hip_check(hipHostMalloc(&sl.host, cap, hipHostMallocDefault), "hipHostMalloc");
+    if (st != VC_OK) return st;
+    st = hip_check(hipHostGetDevicePointer(&sl.dev, sl.host, 0), "hipHostGetDevicePointer");
+    if (st != VC_OK) {
+      (void)hipHostFree(sl.host);
+      sl.host = nullptr;
+      return st;
+    }
+    sl.cap = cap;
+  }
+  memcpy(sl.host, src, bytes);
+  slot = &sl;
+  return VC_OK;
 }
 
 struct Outputs {
@@ -336,8 +375,23 @@ struct Outputs {
   vc_integrity *integ = nullptr;
 };
 
+// Binary32 bounds of a binary64 value x >= 0: largest float <= x, smallest
+// float >= x (FLT_MAX / +Inf beyond the binary32 range).
+float f32_below(double x) {
+  if (x >= (double)FLT_MAX) return FLT_MAX;
+  float f = (float)x;
+  if ((double)f > x) f = std::nextafter(f, 0.0f);
+  return f;
+}
+float f32_above(double x) {
+  if (x > (double)FLT_MAX) return INFINITY;
+  float f = (float)x;
+  if ((double)f < x) f = std::nextafter(f, INFINITY);
+  return f;
+}
+
 // Enqueues the planned work. `single` passes the one descriptor by value
-// (no upload).
+// (no table).
 vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws, size_t ws_bytes,
               hipStream_t stream, bool single) {
   if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
@@ -361,34 +415,76 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
     P.rtol[p] = t.rtol;
     if (t.equal_nan) P.eqnan_mask |= 1u << p;
   }
+  // The binary32 tier evaluates several pairs in binary64; a single pair
+  // uses binary32 bounds shrunk / grown by 2^-20, valid while the thresholds
+  // stay in the normal binary32 range: atol = 0 or >= 2^-100, rtol = 0 or
+  // >= 2^-60 (the kernel requires |r| >= 2^-60 for this tier).
+  P.tier1 = 1;
+  if (plan.n_tols == 1) {
+    const double a = tols[0].atol, r = tols[0].rtol;
+    const bool a_ok = a == 0.0 || a >= 0x1p-100, r_ok = r == 0.0 || r >= 0x1p-60;
+    P.tier1 = (a_ok && r_ok) ? 1 : 0;
+    P.rlo = f32_below(r - r * 0x1p-20);
+    P.alo = f32_below(a - a * 0x1p-20);
+    P.rhi = f32_above(r + r * 0x1p-20);
+    P.ahi = f32_above(a + a * 0x1p-20);
+  }
   P.recs = (vck::ChunkRec *)(base + plan.off_recs);
   P.stage = (uint32_t *)(base + plan.off_stage);
+  P.grecs = (vck::ChunkRec *)(base + plan.off_grecs);
+  P.gstage = (uint32_t *)(base + plan.off_gstage);
+  P.ctr = (vck::Counters *)(base + plan.off_ctr);
+  P.case_cnt = (uint32_t *)(base + plan.off_case_cnt);
   P.tile_maps = plan.do_tiles ? out.tile_maps : nullptr;
   P.stats = out.stats;
   P.mismatches = out.mismatches;
   P.pass_out = out.pass;
   P.first_k = plan.do_firstk ? out.first_k : nullptr;
   P.integ = out.integ;
-  P.ws_pass = base + plan.off_pass;
-  P.ws_flags = (uint32_t *)(base + plan.off_flags);
   P.match_rate = out.match_rate;
   P.numeric_rate = out.numeric_rate;
-  P.tiles_total = plan.tiles_total;
+
+  vck::Prologue Q;
+  memset(&Q, 0, sizeof Q);
+  Q.zero = (uint32_t *)(base + plan.off_ctr);
+  Q.zero_words = plan.ctr_bytes / sizeof(uint32_t);
+  Q.tiles = P.tile_maps;
+  Q.n_tiles = P.tile_maps != nullptr ? plan.tiles_total : 0;
+  Q.match_rate = out.match_rate;
+  Q.numeric_rate = out.numeric_rate;
+  Q.n_cases = plan.n_cases;
+  Q.n_tols = plan.n_tols;
+
+  std::unique_lock<std::mutex> lock;
+  Slot *slot = nullptr;
+  std::vector<uint8_t> blob;
   if (single) {
     P.cases = nullptr;
     P.single = plan.table[0];
   } else if (plan.n_cases > 0) {
     P.cases = (const vck::DevCase *)(base + plan.off_table);
-    const vc_status st =
-        upload(base + plan.off_table, plan.table.data(), sizeof(vck::DevCase) * plan.table.size(),
-               stream);
+    P.case_chunk = (const uint64_t *)(base + plan.off_cc);
+    P.case_group = (const uint64_t *)(base + plan.off_cg);
+    blob.assign(plan.blob_bytes, 0);
+    memcpy(blob.data(), plan.table.data(), sizeof(vck::DevCase) * plan.table.size());
+    memcpy(blob.data() + (plan.off_cc - plan.off_table), plan.case_chunk.data(),
+           sizeof(uint64_t) * plan.case_chunk.size());
+    memcpy(blob.data() + (plan.off_cg - plan.off_table), plan.case_group.data(),
+           sizeof(uint64_t) * plan.case_group.size());
+    const vc_status st = stage_blob(blob.data(), blob.size(), lock, slot);
     if (st != VC_OK) return st;
+    Q.blob_src = (const uint8_t *)slot->dev;
+    Q.blob_dst = base + plan.off_table;
+    Q.blob_bytes = plan.blob_bytes;
   }
-  vc_status st = VC_OK;
-  if (plan.do_tiles && plan.tiles_total > 0) {
-    st = hip_check(vck::launch_fill_u32(out.tile_maps, plan.tiles_total, stream), "tile-map fill");
-    if (st != VC_OK) return st;
+  vc_status st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  if (st == VC_OK && slot != nullptr) {
+    st = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
+    if (st == VC_OK) slot->pending = true;
   }
+  if (lock.owns_lock()) lock.unlock();
+  if (st != VC_OK) return st;
+
   hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
   g_prof_begin = g_prof_end = nullptr;
   if (prof_begin != nullptr) {
@@ -396,12 +492,12 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
     if (st != VC_OK) return st;
   }
   for (const Group &g : plan.groups) {
-    vck::Params Q = P;
-    Q.chunk_lo = g.chunk_lo;
-    Q.case_lo = g.case_lo;
-    Q.case_hi = g.case_hi;
-    Q.unit_elems = g.unit;
-    st = hip_check(vck::launch_main(g.dtype, plan.nt_class, plan.do_integ ? 1 : 0, Q, g.n_chunks,
+    vck::Params G = P;
+    G.chunk_lo = g.chunk_lo;
+    G.case_lo = g.case_lo;
+    G.case_hi = g.case_hi;
+    G.unit_elems = g.unit;
+    st = hip_check(vck::launch_main(g.dtype, plan.nt_class, plan.do_integ ? 1 : 0, G, g.n_chunks,
                                     stream),
                    "main kernel launch");
     if (st != VC_OK) return st;
@@ -410,16 +506,7 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
     st = hip_check(hipEventRecord(prof_end, stream), "profile end event");
     if (st != VC_OK) return st;
   }
-  if (plan.n_cases > 0) {
-    vck::Params Q = P;
-    Q.case_lo = 0;
-    Q.case_hi = plan.table.size();
-    st = hip_check(vck::launch_finalize(Q, plan.table.size(), stream), "finalize launch");
-    if (st != VC_OK) return st;
-  }
-  if (out.match_rate != nullptr || out.numeric_rate != nullptr)
-    st = hip_check(vck::launch_rates(P, stream), "rates launch");
-  return st;
+  return hip_check(vck::launch_finalize(P, plan.total_groups, stream), "finalize launch");
 }
 
 vc_case one_case(const vc_tensor *cand, const vc_tensor *ref, const vc_tensor *inputs,

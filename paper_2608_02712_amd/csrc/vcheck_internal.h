@@ -13,9 +13,13 @@ constexpr int kWaveSize = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWaveSize * kWavesPerBlock;
 constexpr int kTileWindow = 2048;  // LDS tile counters per block
+constexpr int kGroupChunks = 64;   // chunks merged by one group record
 
 // Device-side case descriptor. The host builds one per case, in launch
-// order (grouped by dtype), and uploads the table into the workspace.
+// order (grouped by dtype), and the prologue kernel copies the table into
+// the workspace. Every case owns at least one chunk: a case that is not
+// evaluated (status != 0) or is empty gets one chunk with no elements, so
+// its results are written by the same completion path as every other case.
 struct DevCase {
   const uint8_t *cand;
   const uint8_t *ref;
@@ -25,77 +29,115 @@ struct DevCase {
   uint64_t chunk_begin;  // global index of the case's first chunk
   uint64_t tile_off;     // offset of the case's tile map in the output
   uint64_t tiles_c;      // tiles per tile row: ceil(C / tile_w)
-  uint32_t n_chunks;
+  uint64_t group_begin;  // global index of the case's first chunk group
+  uint32_t n_chunks;     // >= 1
+  uint32_t n_groups;     // ceil(n_chunks / kGroupChunks)
   int32_t status;        // 0, or a negative vc_status (case not evaluated)
   uint32_t inp_mask;     // bit j: input j takes part in the copy detector
   uint32_t vec_ok;       // 1: every pointer of the case is 16-byte aligned
   uint32_t orig;         // index of the case in the caller's arrays
   uint32_t dtype;
   uint32_t unit_elems;   // elements per wave range; a chunk is 4 of them
-  uint32_t reserved;
 };
-static_assert(sizeof(DevCase) == 152, "DevCase layout");
+static_assert(sizeof(DevCase) == 160, "DevCase layout");
 
 // Partial result of one chunk (one block of the main kernel; its four waves
-// interleave over the chunk). Offsets are element offsets within the chunk.
+// interleave over the chunk), or of one group of up to kGroupChunks chunks.
+// Offsets are element offsets within the record's own range. The first
+// kRecCounts words are counters that merge by addition.
 struct ChunkRec {
-  uint32_t mism[VC_MAX_TOLS];
-  uint32_t nan_c, inf_c, nan_r, inf_r;
-  uint32_t n_fin, n_rel, n_rel_undef, eq_bits;  // eq_bits: see kEq* below
-  uint32_t nfound[kWavesPerBlock];              // staged first-k entries (all in slot 0)
-  uint32_t zero_c, zero_r, eqf_c, eqf_r;
-  uint32_t bf_c, bf_r, f16_c, f16_r;
-  double max_abs, max_rel;  // -1.0 when the chunk has no finite / no rel pair
-  uint32_t amax_abs, amax_rel;  // 0xffffffff when none
-  uint32_t pad0, pad1;
+  uint32_t mism[VC_MAX_TOLS];              // words 0..7
+  uint32_t nan_c, inf_c, nan_r, inf_r;     // 8..11
+  uint32_t n_fin, n_rel, n_rel_undef;      // 12..14
+  uint32_t zero_c, zero_r, eqf_c, eqf_r;   // 15..18
+  uint32_t bf_c, bf_r, f16_c, f16_r;       // 19..22
+  uint32_t nfound;                         // staged first-k entries (<= k)
+  uint32_t eq_bits;                        // see kEq* below; merges by AND
+  uint32_t amax_abs, amax_rel;             // 0xffffffff when none
+  uint32_t pad;
+  double max_abs, max_rel;                 // -1.0 when none
   double sum_abs, sum_rel;
 };
-static_assert(sizeof(ChunkRec) == 160, "ChunkRec layout");
+static_assert(sizeof(ChunkRec) == 144, "ChunkRec layout");
+constexpr int kRecCounts = 23;
 
 constexpr uint32_t kEqCandRef = 1u;        // bit 0: cand bit-equal to ref
 constexpr int kEqCandInpShift = 8;         // bits 8..15: cand bit-equal to input j
 constexpr int kEqRefInpShift = 16;         // bits 16..23: ref bit-equal to input j
 
+// Completion counters at the start of the counter area of the workspace;
+// the per-case counters follow.
+struct Counters {
+  uint32_t cases_done;
+  uint32_t pass[VC_MAX_TOLS];       // cases passing pair p numerically
+  uint32_t cert[VC_MAX_TOLS];       // ... and with no integrity flag
+  uint32_t pad[15];
+};
+static_assert(sizeof(Counters) == 128, "Counters layout");
+
 // Kernel parameters (passed by value).
 struct Params {
-  const DevCase *cases;  // device table, or nullptr: use `single`
-  int32_t n_cases;
-  int32_t n_tols;        // 1 .. 8 (the kernel evaluates NT >= n_tols pairs)
+  const DevCase *cases;        // device table, or nullptr: use `single`
+  const uint64_t *case_chunk;  // [table entries] chunk_begin, for the case lookup
+  const uint64_t *case_group;  // [table entries] group_begin, for the case lookup
+  int32_t n_cases;             // table entries (= caller cases)
+  int32_t n_tols;              // 1 .. 8 (the kernel evaluates NT >= n_tols pairs)
   int32_t primary;
   int32_t tile_h, tile_w;
-  int32_t k;             // first-k length (0: none)
-  int32_t do_tiles;      // 1: tile maps requested
+  int32_t k;                   // first-k length (0: none)
+  int32_t do_tiles;            // 1: tile maps requested
   int32_t do_integ;
-  uint32_t unit_elems;   // elements per wave range (one quarter of a chunk)
-  uint32_t eqnan_mask;   // bit p: equal_nan of pair p
-  uint64_t chunk_lo;     // first global chunk of this launch
-  uint64_t case_lo;      // first table index of this launch's cases
+  int32_t tier1;               // 1: the binary32 fast path is valid for these pairs
+  uint32_t unit_elems;         // elements per wave range (one quarter of a chunk)
+  uint32_t eqnan_mask;         // bit p: equal_nan of pair p
+  uint32_t pad0;
+  uint64_t chunk_lo;           // first global chunk of this launch
+  uint64_t case_lo;            // first table index of this launch's cases
   uint64_t case_hi;
   double atol[VC_MAX_TOLS];
   double rtol[VC_MAX_TOLS];
+  // binary32 gate bounds of pair 0 (used when n_tols == 1):
+  // fma(|r|, rlo, alo) <= atol + rtol |r| <= fma(|r|, rhi, ahi)
+  float rlo, alo, rhi, ahi;
 
-  ChunkRec *recs;        // [total chunks]
-  uint32_t *stage;       // [total chunks * 4 * k] first-k staging (offsets)
-  uint32_t *tile_maps;   // user tile maps (nullable)
-  // finalize outputs
+  ChunkRec *recs;              // [total chunks]
+  uint32_t *stage;             // [total chunks * 4 * k] first-k staging (offsets)
+  ChunkRec *grecs;             // [total groups]
+  uint32_t *gstage;            // [total groups * k]
+  Counters *ctr;
+  uint32_t *case_cnt;          // [table entries] groups completed
+  uint32_t *tile_maps;         // user tile maps (nullable)
+  // outputs
   vc_stats *stats;
   uint64_t *mismatches;
   uint8_t *pass_out;
   int64_t *first_k;
   vc_integrity *integ;
-  uint8_t *ws_pass;      // [n_cases * n_tols] always written by finalize
-  uint32_t *ws_flags;    // [n_cases]
   double *match_rate;
   double *numeric_rate;
-  uint64_t tiles_total;
   DevCase single;
 };
 
+// Work of the prologue kernel: copy the descriptor blob from pinned host
+// memory, clear the counter area and the tile maps.
+struct Prologue {
+  const uint8_t *blob_src;  // device-visible pinned host pointer (or nullptr)
+  uint8_t *blob_dst;
+  uint64_t blob_bytes;      // multiple of 16
+  uint32_t *zero;           // counter area
+  uint64_t zero_words;
+  uint32_t *tiles;
+  uint64_t n_tiles;
+  double *match_rate;       // written (0) when the sweep has no cases
+  double *numeric_rate;
+  int32_t n_cases;
+  int32_t n_tols;
+};
+
 // Launchers (vcheck_kernels.hip). Each returns the HIP error of its launch.
-hipError_t launch_fill_u32(uint32_t *p, uint64_t n, hipStream_t s);
+hipError_t launch_prologue(const Prologue &p, hipStream_t s);
 hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint64_t n_chunks,
                        hipStream_t s);
-hipError_t launch_finalize(const Params &p, uint64_t n_cases_in_table, hipStream_t s);
-hipError_t launch_rates(const Params &p, hipStream_t s);
+hipError_t launch_finalize(const Params &p, uint64_t n_groups, hipStream_t s);
 
 }  // namespace vck

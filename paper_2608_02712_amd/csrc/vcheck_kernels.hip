@@ -6,35 +6,44 @@
 // full-coverage evidence): the tolerance gate for up to 8 pairs, NaN/Inf
 // counts, exact max/argmax of |c-r| and |c-r|/|r|, binary64 error sums, the
 // per-tile mismatch map, the ordered first-k mismatch indices and the
-// degenerate-output detector counts.
+// degenerate-output detector counts. The same launch also reduces the per-
+// chunk results: the last block to finish a group of chunks merges the
+// group, the last group of a case writes the case's results, and the last
+// case writes the suite match rates (completion counters, fixed merge order).
 //
 // Work decomposition: a case is cut into chunks of 4 * U elements; one block
 // (4 waves) owns one chunk and streams it front to back: a step is 64 lanes x
 // 16 bytes (one fully coalesced 1 KiB non-temporal load per tensor) and the
 // four waves take steps round robin, so the block's loads always target one
-// contiguous stretch of memory (this interleave reads HBM markedly faster
-// than one contiguous range per wave). The loop is unrolled twice so the
-// next step's loads are in flight while the current step is evaluated.
-// Per-wave results carry chunk offsets, so ties and first-k are resolved by
-// index, not by which wave saw an element first.
+// contiguous stretch of memory. The loop is unrolled twice so the next
+// step's loads are in flight while the current step is evaluated.
 //
-// Exactness. The definition is binary64 on exactly decoded values (every
-// storage type widens exactly to binary32, and binary32 to binary64). Each
-// step first runs a fast path that evaluates the gate, |c - r| and |r| in
-// binary64 exactly as the definition (separately rounded rtol*|r| and
-// atol + (.), no contraction anywhere in this file), keeps the lane maximum
-// of |c - r| in binary64 and tests every element against the wave's exact
-// running maximum of |c - r|/|r| with the exact sign test
-// fma(-M, |r|, d) > 0 <=> d/|r| > M. Only an element that strictly beats a
-// running maximum reaches the update path (a correctly rounded division and a
-// wave reduction that keeps the smallest index on ties), so ties cost
-// nothing. The fast path assumes every value finite and every r non-zero
-// (checked through the finiteness of the lane's quotient estimates); a step
-// that breaks this is evaluated element by element with the class tests (the
-// exact path) from the registers it already holds. Only sum_rel uses binary32
-// quotient estimates (relative error below 5e-7, within the 1e-6 contract).
-// Counts come from wave ballots and popcounts; no floating-point atomics are
-// used, so every result is bit-reproducible.
+// Exactness. The definition is binary64 on exactly decoded values. Each step
+// is evaluated by the cheapest of three tiers that is exact for it:
+//  1. binary32 tier. When every element of the step has |c - r| <= 0.998 |r|
+//     (binary16/bfloat16 storage) or <= 0.49 |r| (binary32 storage), the
+//     binary32 difference c - r is exact (the exponents of c and r differ by
+//     at most 10; for binary32 by Sterbenz's lemma), so |c - r| equals its
+//     binary64 value. The gate then compares it with binary64 thresholds
+//     (several pairs) or, for a single pair, with binary32 bounds
+//     fma(|r|, rlo, alo) <= atol + rtol |r| <= fma(|r|, rhi, ahi) (the host
+//     shrinks / grows the pair by 2^-20 and only enables this when the
+//     thresholds stay in the normal binary32 range); an element between the
+//     bounds sends the step to tier 2. Running-maximum tests are exact
+//     binary32 comparisons against thresholds rounded down to binary32, and
+//     fma(-M, |r|, d) > 0 (exact sign) for the quotient.
+//  2. binary64 tier: the same evaluation in binary64 for steps with finite
+//     values and non-zero references.
+//  3. exact tier: element by element with the class tests (NaN, Inf, r = 0,
+//     partial tail steps).
+// Each lane keeps its exact best (value, offset) of |c - r| and of the
+// quotient; a wave-uniform threshold (the wave's best so far) filters
+// elements, so only an element that strictly beats it reaches the update
+// (ties never do, since later elements have larger indices). Only sum_rel
+// uses quotient estimates (binary32 or binary64 reciprocals, relative error
+// below 5e-7, within the 1e-6 contract). Counts come from wave ballots and
+// popcounts; no floating-point atomics are used, so every result is
+// bit-reproducible.
 #pragma clang fp contract(off)
 
 #include "vcheck_internal.h"
@@ -59,6 +68,8 @@ struct Tr<VC_BF16> {
   static constexpr int V = 8;
   static constexpr int ES = 2;
 };
+
+constexpr uint32_t kNone = 0xffffffffu;
 
 // 16 bytes of raw storage held by one lane.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -139,13 +150,22 @@ __device__ __forceinline__ u32x4 load_guarded(const uint8_t *base, uint64_t idx0
   return r;
 }
 
-struct WaveOut {
-  uint32_t mism[VC_MAX_TOLS];
-  uint32_t nan_c, inf_c, nan_r, inf_r, n_fin, n_rel, n_rel_undef, eq_bits;
-  uint32_t nfound, zc, zr, efc, efr, bfc, bfr, hfc, hfr;
-  uint32_t amax_abs, amax_rel;
-  double max_abs, max_rel, sum_abs, sum_rel;
-};
+// Row of element i in the (R, C) view, and the tile of element i. `narrow`
+// (every index of the case below 2^32) selects 32-bit divisions, which are
+// several times cheaper than 64-bit ones.
+__device__ __forceinline__ uint64_t row_of(uint64_t i, uint64_t cols, bool narrow) {
+  return narrow ? (uint64_t)((uint32_t)i / (uint32_t)cols) : i / cols;
+}
+__device__ __forceinline__ uint64_t tile_of(uint64_t i, uint64_t cols, uint32_t th, uint32_t tw,
+                                            uint64_t tiles_c, bool narrow) {
+  if (narrow) {
+    const uint32_t ii = (uint32_t)i, cc = (uint32_t)cols;
+    const uint32_t row = ii / cc, col = ii - row * cc;
+    return (uint64_t)(row / th) * tiles_c + col / tw;
+  }
+  const uint64_t row = i / cols, col = i - row * cols;
+  return (row / th) * tiles_c + col / tw;
+}
 
 // Member-wise copy of a case descriptor read through the constant address
 // space (scalar loads).
@@ -160,18 +180,20 @@ __device__ __forceinline__ DevCase load_case(const VCK_CONST DevCase *t) {
   d.chunk_begin = t->chunk_begin;
   d.tile_off = t->tile_off;
   d.tiles_c = t->tiles_c;
+  d.group_begin = t->group_begin;
   d.n_chunks = t->n_chunks;
+  d.n_groups = t->n_groups;
   d.status = t->status;
   d.inp_mask = t->inp_mask;
   d.vec_ok = t->vec_ok;
   d.orig = t->orig;
   d.dtype = t->dtype;
   d.unit_elems = t->unit_elems;
-  d.reserved = 0;
   return d;
 }
 
-__device__ __forceinline__ void max_merge(double &v, uint32_t &i, double ov, uint32_t oi) {
+template <typename I>
+__device__ __forceinline__ void max_merge(double &v, I &i, double ov, I oi) {
   if (ov > v || (ov == v && oi < i)) {
     v = ov;
     i = oi;
@@ -185,9 +207,16 @@ __device__ __forceinline__ double readfirstlane_f64(double x) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+__device__ __forceinline__ double readlane_f64(double x, uint32_t l) {
+  const uint64_t b = (uint64_t)__double_as_longlong(x);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, l);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), l);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 // Wave-wide (largest value, smallest index) of the lanes' (v, i), returned
 // as wave-uniform values. Lanes with nothing pass v = -1 (real values are
-// >= 0) and i = 0xffffffff.
+// >= 0) and i = kNone.
 __device__ __forceinline__ void wave_max(double &v, uint32_t &i) {
 #pragma unroll
   for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
@@ -199,22 +228,352 @@ __device__ __forceinline__ void wave_max(double &v, uint32_t &i) {
   i = __builtin_amdgcn_readfirstlane(i);
 }
 
-#ifndef VCK_WAVES_PER_EU
-#define VCK_WAVES_PER_EU 4
-#endif
+// Wave-wide maximum of v (values only), wave-uniform.
+__device__ __forceinline__ double wave_max_val(double v) {
+#pragma unroll
+  for (int m = kWaveSize / 2; m >= 1; m >>= 1) v = __builtin_fmax(v, __shfl_xor(v, m));
+  return readfirstlane_f64(v);
+}
+
+// Largest binary32 value <= x, for x = -1 or x >= 0 (the running-maximum
+// thresholds); values above the binary32 range give FLT_MAX.
+__device__ __forceinline__ float f32_down(double x) {
+  if (x < 0.0) return -1.0f;
+  float f = (float)x;
+  if ((double)f > x) f = __uint_as_float(__float_as_uint(f) - 1u);
+  return f;
+}
+
+// ------------------------------------------------------------ merge helpers
+
+// Completion handshake of a block on `counter`: once every thread's stores
+// are complete, thread 0 publishes them device-wide (agent-scope release: one
+// L2 write-back per block, not per wave) and counts the block in; the block that arrives last acquires before it reads the other
+// blocks' records. Returns true (block-uniformly) for the last block.
+__device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t last, uint32_t &s_flag) {
+  // each wave waits until its own stores are performed in L2 (the barrier
+  // alone does not wait for them), so thread 0's write-back covers them all
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    s_flag = atomicAdd(counter, 1u) == last ? 1u : 0u;
+  }
+  __syncthreads();
+  const bool is_last = s_flag != 0;
+  if (is_last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  return is_last;
+}
+
+struct MergeScratch {
+  uint64_t part[8][32];
+  uint64_t cnt[32];
+  double dpart[kBlockThreads];
+  uint32_t scan[kBlockThreads];
+  double mv[kWavesPerBlock];
+  uint64_t mi[kWavesPerBlock];
+  uint32_t eq[kWavesPerBlock];
+  double max_abs, max_rel, sum_abs, sum_rel;
+  uint64_t amax_abs, amax_rel;
+  uint32_t eq_all;
+};
+
+// Block-wide (max value, smallest index); idx = UINT64_MAX marks "none".
+// Every thread gets the result.
+__device__ __forceinline__ void block_max(MergeScratch &s, double &v, uint64_t &idx) {
+#pragma unroll
+  for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
+    const double ov = __shfl_xor(v, m);
+    const uint64_t oi = __shfl_xor(idx, m);
+    max_merge(v, idx, ov, oi);
+  }
+  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
+  __syncthreads();
+  if (lane == 0) {
+    s.mv[wave] = v;
+    s.mi[wave] = idx;
+  }
+  __syncthreads();
+  v = s.mv[0];
+  idx = s.mi[0];
+  for (int w = 1; w < kWavesPerBlock; ++w) max_merge(v, idx, s.mv[w], s.mi[w]);
+}
+
+__device__ __forceinline__ uint32_t block_and_u32(MergeScratch &s, uint32_t x) {
+#pragma unroll
+  for (int m = kWaveSize / 2; m >= 1; m >>= 1) x &= __shfl_xor(x, m);
+  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
+  __syncthreads();
+  if (lane == 0) s.eq[wave] = x;
+  __syncthreads();
+  uint32_t t = 0xffffffffu;
+  for (int w = 0; w < kWavesPerBlock; ++w) t &= s.eq[w];
+  return t;
+}
+
+// Exclusive prefix of x over the block (thread order); returns the total too.
+__device__ __forceinline__ uint32_t block_exscan_u32(MergeScratch &s, uint32_t x, uint32_t &total) {
+  __syncthreads();
+  s.scan[threadIdx.x] = x;
+  __syncthreads();
+  for (uint32_t off = 1; off < (uint32_t)kBlockThreads; off <<= 1) {
+    const uint32_t v = threadIdx.x >= off ? s.scan[threadIdx.x - off] : 0u;
+    __syncthreads();
+    s.scan[threadIdx.x] += v;
+    __syncthreads();
+  }
+  total = s.scan[kBlockThreads - 1];
+  return s.scan[threadIdx.x] - x;
+}
+
+// Merges records recs[0..n) (record i covers elements [i*span, (i+1)*span)
+// of the parent range) in a fixed order; the totals land in s. Called by the
+// whole block; the records were written by other blocks, so the caller has
+// issued an acquire fence.
+__device__ __forceinline__ void merge_recs(MergeScratch &s, const ChunkRec *recs, uint32_t n, uint64_t span) {
+  const uint32_t t = threadIdx.x;
+  {
+    // counters: thread t sums word (t % 32) over records t/32, t/32 + 8, ...
+    const uint32_t f = t & 31, r0 = t >> 5;
+    uint64_t acc = 0;
+    if (f < (uint32_t)kRecCounts)
+      for (uint32_t r = r0; r < n; r += 8) acc += ((const uint32_t *)(recs + r))[f];
+    s.part[r0][f] = acc;
+  }
+  {
+    // binary64 sums: thread t sums field t % 2 over records t/2, t/2 + 128, ...
+    const uint32_t f = t & 1;
+    double acc = 0.0;
+    for (uint32_t r = t >> 1; r < n; r += kBlockThreads / 2)
+      acc += f ? recs[r].sum_rel : recs[r].sum_abs;
+    s.dpart[t] = acc;
+  }
+  double va = -1.0, vr = -1.0;
+  uint64_t ia = UINT64_MAX, ir = UINT64_MAX;
+  uint32_t eq = 0xffffffffu;
+  for (uint32_t r = t; r < n; r += kBlockThreads) {
+    const ChunkRec &x = recs[r];
+    eq &= x.eq_bits;
+    if (x.amax_abs != kNone) max_merge(va, ia, x.max_abs, (uint64_t)r * span + x.amax_abs);
+    if (x.amax_rel != kNone) max_merge(vr, ir, x.max_rel, (uint64_t)r * span + x.amax_rel);
+  }
+  __syncthreads();
+  if (t < 32) {
+    uint64_t a = 0;
+    for (int q = 0; q < 8; ++q) a += s.part[q][t];
+    s.cnt[t] = a;
+  }
+  if (t < 2) {
+    double a = 0.0;
+    for (uint32_t u = t; u < (uint32_t)kBlockThreads; u += 2) a += s.dpart[u];
+    if (t == 0) s.sum_abs = a;
+    else s.sum_rel = a;
+  }
+  block_max(s, va, ia);
+  block_max(s, vr, ir);
+  eq = block_and_u32(s, eq);
+  if (t == 0) {
+    s.max_abs = va;
+    s.amax_abs = ia;
+    s.max_rel = vr;
+    s.amax_rel = ir;
+    s.eq_all = eq;
+  }
+  __syncthreads();
+}
+
+// Copies the staged first-k lists of recs[0..n) in record order: entry e of
+// record r becomes element r * span + e of the parent range. Returns the
+// number of entries written (<= k); block-uniform.
+template <bool FINAL>
+__device__ __forceinline__ uint32_t gather_firstk(MergeScratch &s, const ChunkRec *recs, uint32_t n,
+                                  uint64_t span, const uint32_t *stage, uint64_t stage_stride,
+                                  uint32_t k, uint32_t *out32, int64_t *out64) {
+  uint32_t carry = 0;
+  for (uint32_t b = 0; b < n && carry < k; b += kBlockThreads) {
+    const uint32_t r = b + threadIdx.x;
+    const uint32_t c = r < n ? recs[r].nfound : 0u;
+    uint32_t total;
+    const uint32_t ex = block_exscan_u32(s, c, total);
+    if (c != 0 && carry + ex < k) {
+      const uint32_t *st = stage + (uint64_t)r * stage_stride;
+      uint32_t pos = carry + ex;
+      for (uint32_t e = 0; e < c && pos < k; ++e, ++pos) {
+        const uint64_t gi = (uint64_t)r * span + st[e];
+        if constexpr (FINAL) out64[pos] = (int64_t)gi;
+        else out32[pos] = (uint32_t)gi;
+      }
+    }
+    carry = min(carry + total, k);
+  }
+  return carry;
+}
+
+// Output pointers and options of the completion path (copied field by field
+// from the kernel argument: a reference to the by-value argument would force
+// it into private memory).
+struct FinArgs {
+  vc_stats *stats;
+  uint64_t *mismatches;
+  uint8_t *pass_out;
+  int64_t *first_k;
+  vc_integrity *integ;
+  double *match_rate;
+  double *numeric_rate;
+  Counters *ctr;
+  int32_t n_cases, n_tols, primary, k, do_integ;
+};
+
+// Writes the results of a case from its records (chunk records when the case
+// has one group, else group records) and, for the last case of the call, the
+// suite match rates. Called by the whole block.
+__device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P, const DevCase &cs,
+                              const ChunkRec *recs, uint32_t n, uint64_t span,
+                              const uint32_t *stage, uint64_t stage_stride) {
+  merge_recs(s, recs, n, span);
+  const bool ok = cs.status == 0;
+  const uint32_t oi = cs.orig;
+  if (P.first_k != nullptr && P.k > 0) {
+    const uint32_t k = (uint32_t)P.k;
+    int64_t *const fk = P.first_k + (uint64_t)oi * k;
+    uint32_t nf = 0;
+    if (ok) nf = gather_firstk<true>(s, recs, n, span, stage, stage_stride, k, nullptr, fk);
+    for (uint32_t pos = nf + threadIdx.x; pos < k; pos += kBlockThreads) fk[pos] = -1;
+  }
+  if (threadIdx.x != 0) return;
+  const int nt = P.n_tols;
+  const int prim = P.primary;
+  const uint64_t n_el = ok ? cs.numel : 0;
+  auto cnt = [&](int w) -> uint64_t { return ok ? s.cnt[w] : 0; };
+  vc_stats st;
+  st.numel = cs.numel;
+  st.mismatches = cnt(prim);
+  st.nan_cand = cnt(8);
+  st.inf_cand = cnt(9);
+  st.nan_ref = cnt(10);
+  st.inf_ref = cnt(11);
+  st.n_finite = cnt(12);
+  st.n_rel = cnt(13);
+  st.n_rel_undef = cnt(14);
+  const bool has_abs = ok && s.amax_abs != UINT64_MAX;
+  const bool has_rel = ok && s.amax_rel != UINT64_MAX;
+  st.max_abs = has_abs ? s.max_abs : 0.0;
+  st.argmax_abs = has_abs ? (int64_t)s.amax_abs : -1;
+  st.max_rel = has_rel ? s.max_rel : 0.0;
+  st.argmax_rel = has_rel ? (int64_t)s.amax_rel : -1;
+  st.sum_abs = ok ? s.sum_abs : 0.0;
+  st.sum_rel = ok ? s.sum_rel : 0.0;
+  st.case_status = cs.status;
+  st.pass = (ok && cnt(prim) == 0) ? 1 : 0;
+  if (P.stats != nullptr) P.stats[oi] = st;
+  for (int p = 0; p < nt; ++p) {
+    const uint8_t pass = (ok && cnt(p) == 0) ? 1 : 0;
+    if (P.pass_out != nullptr) P.pass_out[(uint64_t)oi * nt + p] = pass;
+    if (P.mismatches != nullptr) P.mismatches[(uint64_t)oi * nt + p] = cnt(p);
+  }
+  uint32_t flags = 0;
+  if (P.do_integ) {
+    const uint64_t zc = cnt(15), zr = cnt(16), efc = cnt(17), efr = cnt(18);
+    const uint64_t bfc = cnt(19), bfr = cnt(20), hfc = cnt(21), hfr = cnt(22);
+    vc_integrity g;
+    g.zero_cand = zc;
+    g.zero_ref = zr;
+    g.eqfirst_cand = efc;
+    g.eqfirst_ref = efr;
+    g.bf16rep_cand = bfc;
+    g.bf16rep_ref = bfr;
+    g.fp16rep_cand = hfc;
+    g.fp16rep_ref = hfr;
+    const uint32_t eqb = ok ? s.eq_all : 0u;
+    const uint32_t inp_mask = ok ? cs.inp_mask : 0u;
+    const uint32_t eq_c = (eqb >> kEqCandInpShift) & 0xffu & inp_mask;
+    const uint32_t eq_r = (eqb >> kEqRefInpShift) & 0xffu & inp_mask;
+    g.cand_eq_input_mask = eq_c;
+    g.ref_eq_input_mask = eq_r;
+    g.cand_eq_ref = eqb & kEqCandRef;
+    g.copy_input = -1;
+    if (ok) {
+      const bool f32 = cs.dtype == VC_F32;
+      if (zc == n_el && n_el >= 1 && zr < n_el) flags |= VC_FLAG_ALL_ZERO;
+      if (efc == n_el && n_el >= 2 && zc < n_el && efr < n_el) flags |= VC_FLAG_CONSTANT;
+      const uint32_t copy = eq_c & ~eq_r;
+      if (copy != 0) {
+        flags |= VC_FLAG_INPUT_COPY;
+        g.copy_input = __builtin_ctz(copy);
+      }
+      if (f32 && bfc == n_el && n_el >= 2 && zc < n_el && efc < n_el && bfr < n_el)
+        flags |= VC_FLAG_LOWPREC_BF16;
+      if (f32 && hfc == n_el && bfc < n_el && n_el >= 2 && zc < n_el && efc < n_el &&
+          hfr < n_el)
+        flags |= VC_FLAG_LOWPREC_FP16;
+    }
+    g.flags = flags;
+    g.reserved = 0;
+    if (P.integ != nullptr) P.integ[oi] = g;
+  }
+  // suite counters; the last case of the call writes the rates
+  for (int p = 0; p < nt; ++p) {
+    if (ok && cnt(p) == 0) {
+      atomicAdd(&P.ctr->pass[p], 1u);
+      if (flags == 0) atomicAdd(&P.ctr->cert[p], 1u);
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  const uint32_t done = atomicAdd(&P.ctr->cases_done, 1u) + 1u;
+  if (done == (uint32_t)P.n_cases) {
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const double nc = (double)P.n_cases;
+    for (int p = 0; p < nt; ++p) {
+      const uint32_t num = __hip_atomic_load(&P.ctr->pass[p], __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t cert = __hip_atomic_load(&P.ctr->cert[p], __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+      if (P.match_rate != nullptr) P.match_rate[p] = (double)cert / nc;
+      if (P.numeric_rate != nullptr) P.numeric_rate[p] = (double)num / nc;
+    }
+  }
+}
+
+// Last table entry (in [lo, hi)) whose value in `first` is <= x; `first`
+// ascends strictly and first[lo] <= x. A 64-way search: each lane tests one
+// probe and the ballot counts the probes at or below x. Wave-uniform.
+__device__ __forceinline__ uint64_t find_entry(const uint64_t *first, uint64_t lo, uint64_t hi,
+                                               uint64_t x) {
+  const VCK_GLOBAL uint64_t *f = (const VCK_GLOBAL uint64_t *)first;
+  const uint64_t lane = threadIdx.x & (kWaveSize - 1);
+  uint64_t n = hi - lo;
+  while (n > (uint64_t)kWaveSize) {
+    const uint64_t stride = (n + kWaveSize - 1) / kWaveSize;
+    const uint64_t idx = lo + lane * stride;
+    const bool le = idx < lo + n ? f[idx] <= x : false;
+    const uint64_t kx = popc(ballot(le)) - 1u;
+    lo += kx * stride;
+    n = min(stride, n - kx * stride);
+  }
+  const bool le = lane < n ? f[lo + lane] <= x : false;
+  return lo + popc(ballot(le)) - 1u;
+}
+
+// ------------------------------------------------------------ main kernel
 
 template <int DT, int NT, bool INTEG>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(VCK_WAVES_PER_EU)))
-void main_kernel(const Params P) {
+__global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   constexpr int V = Tr<DT>::V;
   constexpr int ES = Tr<DT>::ES;
   constexpr uint32_t ITER = kWaveSize * V;  // elements per wave step
   constexpr uint32_t ALL = (1u << V) - 1u;
+  // binary32 tier: bound on the estimate of |c - r| / |r| under which c - r
+  // is exact in binary32 (with a margin for the estimate's error)
+  constexpr float QT = ES == 4 ? 0.49f : 0.998f;
 
-  __shared__ uint32_t s_win[kTileWindow];   // block tile-count window
-  __shared__ uint32_t s_merged[VC_MAX_K];   // first-k merge of the four waves
-  __shared__ WaveOut s_out[kWavesPerBlock];
-  // counters touched only by the exact path, per wave (kept out of scalar
+  struct StreamLds {
+    uint32_t win[kTileWindow];    // block tile-count window
+    uint32_t merged[VC_MAX_K];    // first-k merge of the four waves
+  };
+  __shared__ StreamLds sh_st;
+  __shared__ ChunkRec s_out[kWavesPerBlock];
+  // counters touched only by the exact tier, per wave (kept out of scalar
   // registers): nan_c, inf_c, nan_r, inf_r, n_fin, n_rel, n_rel_undef
   __shared__ uint32_t s_rare[kWavesPerBlock][8];
 
@@ -223,19 +582,12 @@ void main_kernel(const Params P) {
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
   const uint64_t chunk = P.chunk_lo + blockIdx.x;
 
-  // Locate the case: the last table entry whose first chunk is <= chunk
-  // (scalar loads through the constant address space).
+  // Locate the case: the last table entry whose first chunk is <= chunk. A
+  // 64-way search: each lane tests one probe, the ballot counts the probes at
+  // or below the chunk (the first chunks ascend strictly).
   const VCK_CONST DevCase *table = (const VCK_CONST DevCase *)P.cases;
   uint64_t ci = 0;
-  if (table != nullptr) {
-    uint64_t lo = P.case_lo, hi = P.case_hi - 1;
-    while (lo < hi) {
-      const uint64_t mid = (lo + hi + 1) / 2;
-      if (table[mid].chunk_begin <= chunk) lo = mid;
-      else hi = mid - 1;
-    }
-    ci = lo;
-  }
+  if (table != nullptr) ci = find_entry(P.case_chunk, P.case_lo, P.case_hi, chunk);
   // a value copy (an lvalue selecting between the table and the by-value
   // argument would force the whole argument struct into private memory)
   DevCase dcs;
@@ -251,14 +603,17 @@ void main_kernel(const Params P) {
   const bool vec = dcs.vec_ok != 0;
   const uint32_t inp_mask = dcs.inp_mask;
   const uint64_t U = P.unit_elems;
-  const uint64_t cstart = (chunk - chunk_begin) * (4 * U);
-  const uint64_t cend = min(cstart + 4 * U, numel);
+  const uint64_t CH = 4 * U;
+  const uint64_t rel_chunk = chunk - chunk_begin;
+  const uint64_t cstart = rel_chunk * CH;
+  const uint64_t cend = dcs.status != 0 ? cstart : min(cstart + CH, numel);
   const int prim = P.primary;
   // Params fields used by the step lambdas, as locals: the lambdas capture by
   // reference, and a captured by-value argument would live in private memory.
   const int32_t kk = P.k;
   const bool do_tiles = P.do_tiles != 0;
   const uint32_t eqnan_mask = P.eqnan_mask;
+  const bool t1ok = P.tier1 != 0;
   uint32_t *const tile_maps = P.tile_maps;
   // tolerance pairs in registers (constant indices only: a runtime index into
   // the kernel-argument struct would copy it to private memory)
@@ -268,27 +623,21 @@ void main_kernel(const Params P) {
     atol[p] = P.atol[p];
     rtol[p] = P.rtol[p];
   }
+  const float rlo = P.rlo, alo = P.alo, rhi = P.rhi, ahi = P.ahi;
 
-
-  // per-lane binary64 sums
+  // per-lane exact best (value, chunk offset) and binary64 sums
+  double lb_abs = -1.0, lb_rel = -1.0;
+  uint32_t li_abs = kNone, li_rel = kNone;
   double acc_abs = 0.0, acc_rel = 0.0;
-  // wave-uniform exact running maxima (value, chunk offset)
-  double best_abs = -1.0, best_rel = -1.0;
-  uint32_t arg_abs = 0xffffffffu, arg_rel = 0xffffffffu;
-  // merge lane-local candidates into the wave's running maximum
-  auto merge_abs = [&](double v, uint32_t i) __attribute__((always_inline)) {
-    wave_max(v, i);
-    max_merge(best_abs, arg_abs, v, i);
-  };
-  auto merge_rel = [&](double v, uint32_t i) __attribute__((always_inline)) {
-    wave_max(v, i);
-    max_merge(best_rel, arg_rel, v, i);
-  };
+  // wave-uniform thresholds: the wave's best values so far (-1: none), and
+  // their binary32 images rounded down
+  double T_abs = -1.0, T_rel = -1.0;
+  float thr_abs = -1.0f, b_rel = -1.0f;
   // wave-uniform counters
   uint32_t mism[NT];
 #pragma unroll
   for (int p = 0; p < NT; ++p) mism[p] = 0;
-  uint32_t fast_steps = 0;  // steps committed by the fast path
+  uint32_t fast_steps = 0;  // steps committed by tiers 1 and 2
   if (lane < 8) s_rare[wave][lane] = 0;
   uint32_t zc = 0, zr = 0, efc = 0, efr = 0, bfc = 0, bfr = 0, hfc = 0, hfr = 0;
   uint64_t diff_cr = 0;
@@ -296,7 +645,7 @@ void main_kernel(const Params P) {
   uint32_t nfound = 0;
   uint32_t first_c = 0, first_r = 0;
   if constexpr (INTEG) {
-    if (numel > 0) {
+    if (numel > 0 && dcs.status == 0) {
       if constexpr (ES == 4) {
         first_c = *(const VCK_GLOBAL uint32_t *)cand;
         first_r = *(const VCK_GLOBAL uint32_t *)ref;
@@ -311,22 +660,24 @@ void main_kernel(const Params P) {
   const uint32_t th = (uint32_t)P.tile_h, tw = (uint32_t)P.tile_w;
   bool win_ok = false;
   uint64_t win_base = 0;
-  if (do_tiles) {
-    const uint64_t row_lo = cstart / cols, row_hi = (cend - 1) / cols;
+  uint32_t win_len = 0;
+  const bool narrow = numel <= 0xffffffffull;
+  if (do_tiles && cend > cstart) {
+    const uint64_t row_lo = row_of(cstart, cols, narrow), row_hi = row_of(cend - 1, cols, narrow);
     uint64_t t_min, t_max;
     if (row_lo == row_hi) {
-      t_min = (row_lo / th) * tiles_c + (cstart - row_lo * cols) / tw;
-      t_max = (row_lo / th) * tiles_c + (cend - 1 - row_lo * cols) / tw;
+      t_min = tile_of(cstart, cols, th, tw, tiles_c, narrow);
+      t_max = tile_of(cend - 1, cols, th, tw, tiles_c, narrow);
     } else {
       t_min = (row_lo / th) * tiles_c;
       t_max = (row_hi / th) * tiles_c + tiles_c - 1;
     }
     win_ok = (t_max - t_min) < (uint64_t)kTileWindow;
     win_base = t_min;
-    if (win_ok)
-      for (uint32_t e = threadIdx.x; e < (uint32_t)kTileWindow; e += kBlockThreads) s_win[e] = 0;
-    __syncthreads();
+    win_len = win_ok ? (uint32_t)(t_max - t_min + 1) : 0u;
+    for (uint32_t e = threadIdx.x; e < win_len; e += kBlockThreads) sh_st.win[e] = 0;
   }
+  __syncthreads();
   uint32_t *const stage =
       P.stage + ((uint64_t)chunk * kWavesPerBlock + wave) * (uint64_t)(kk > 0 ? kk : 0);
 
@@ -357,26 +708,116 @@ void main_kernel(const Params P) {
       while (bits != 0) {
         const int j = __builtin_ctz(bits);
         bits &= bits - 1;
-        const uint64_t i = i0 + j;
-        const uint64_t row = i / cols;
-        const uint64_t col = i - row * cols;
-        const uint64_t t = (row / th) * tiles_c + col / tw;
-        if (win_ok && t >= win_base && t - win_base < (uint64_t)kTileWindow)
-          atomicAdd(&s_win[t - win_base], 1u);
+        const uint64_t t = tile_of(i0 + j, cols, th, tw, tiles_c, narrow);
+        if (win_ok && t >= win_base && t - win_base < (uint64_t)win_len)
+          atomicAdd(&sh_st.win[t - win_base], 1u);
         else
           atomicAdd(&tile_maps[tile_off + t], 1u);
       }
     }
   };
 
+  // Raise the wave thresholds to the lanes' bests (after an update).
+  auto raise_abs = [&](uint64_t lanes) __attribute__((always_inline)) {
+    const double v = popc(lanes) == 1 ? readlane_f64(lb_abs, (uint32_t)__builtin_ctzll(lanes))
+                                      : wave_max_val(lb_abs);
+    if (v > T_abs) {
+      T_abs = v;
+      thr_abs = f32_down(v);
+    }
+  };
+  auto raise_rel = [&](uint64_t lanes) __attribute__((always_inline)) {
+    const double v = popc(lanes) == 1 ? readlane_f64(lb_rel, (uint32_t)__builtin_ctzll(lanes))
+                                      : wave_max_val(lb_rel);
+    if (v > T_rel) {
+      T_rel = v;
+      b_rel = f32_down(v);
+    }
+  };
+  // Tier-1 update of the lane bests for the lanes in absm | relm. Every
+  // |c - r| of the step is exact in binary32, so the quotients of two
+  // elements compare exactly through binary64 cross products (products of
+  // two binary32 values are exact), and distinct quotients differ by more
+  // than a binary64 rounding: the lane picks its best quotient of the step
+  // that way and divides once.
+  auto t1_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t absm, uint64_t relm,
+                       uint32_t off0) __attribute__((always_inline)) {
+    const bool la = (absm >> lane) & 1ull, lr = (relm >> lane) & 1ull;
+    if (la || lr) {
+      double sd = 0.0, sa = 1.0;
+      int sj = -1;
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float c = dec32<DT>(elem<DT>(cq, j));
+        const float r = dec32<DT>(elem<DT>(rq, j));
+        const double d = (double)__builtin_fabsf(c - r);
+        const double a = (double)__builtin_fabsf(r);
+        if (la && d > lb_abs) {
+          lb_abs = d;
+          li_abs = off0 + j;
+        }
+        if (lr && (sj < 0 || d * sa > sd * a)) {
+          sd = d;
+          sa = a;
+          sj = j;
+        }
+      }
+      if (lr) {
+        const double q = sd / sa;
+        if (q > lb_rel) {
+          lb_rel = q;
+          li_rel = off0 + (uint32_t)sj;
+        }
+      }
+    }
+    if (absm != 0) raise_abs(absm);
+    if (relm != 0) raise_rel(relm);
+  };
+
+  // Exact updates of the lane bests for the lanes in `lanes` (every element
+  // of those lanes is finite with r != 0: tiers 1 and 2 only).
+  auto abs_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
+                        __attribute__((always_inline)) {
+    if ((lanes >> lane) & 1ull) {
+#pragma unroll 1
+      for (int j = 0; j < V; ++j) {
+        const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - dec64<DT>(elem<DT>(rq, j)));
+        if (d > lb_abs) {
+          lb_abs = d;
+          li_abs = off0 + j;
+        }
+      }
+    }
+    raise_abs(lanes);
+  };
+  auto rel_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
+                        __attribute__((always_inline)) {
+    if ((lanes >> lane) & 1ull) {
+#pragma unroll 1
+      for (int j = 0; j < V; ++j) {
+        const double r = dec64<DT>(elem<DT>(rq, j));
+        const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
+        const double a = __builtin_fabs(r);
+        // exact sign test: d / a > lb  <=>  d - lb * a > 0
+        if (a != 0.0 && __builtin_fma(-lb_rel, a, d) > 0.0) {
+          const double q = d / a;
+          if (q > lb_rel) {
+            lb_rel = q;
+            li_rel = off0 + j;
+          }
+        }
+      }
+    }
+    raise_rel(lanes);
+  };
+
   // Exact binary64 evaluation of one step (element by element).
-  auto exact_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, uint64_t i0) __attribute__((always_inline)) {
+  auto exact_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, uint64_t i0)
+                        __attribute__((always_inline)) {
     const uint32_t off0 = (uint32_t)(i0 - cstart);
     uint32_t pb = 0;
     uint32_t nan_c_step = 0, nan_r_step = 0, inf_c_step = 0, inf_r_step = 0;
     uint32_t fin_step = 0, rel_step = 0, undef_step = 0;
-    double lb_abs = -1.0, lb_rel = -1.0;  // lane-local maxima of this step
-    uint32_t li_abs = 0xffffffffu, li_rel = 0xffffffffu;
 #pragma unroll 1
     for (int j = 0; j < V; ++j) {
       const bool valid = (vmask >> j) & 1u;
@@ -420,8 +861,8 @@ void main_kernel(const Params P) {
         }
       }
     }
-    merge_abs(lb_abs, li_abs);
-    merge_rel(lb_rel, li_rel);
+    raise_abs(~0ull);
+    raise_rel(~0ull);
     if (lane == 0) {
       uint32_t *const rc = s_rare[wave];
       rc[0] += nan_c_step;
@@ -440,26 +881,109 @@ void main_kernel(const Params P) {
     if (ballot(pb != 0) != 0) localize(pb, i0);
   };
 
-  // Fast path for a full step; returns false (and changes nothing) when the
-  // step holds a NaN, an infinity or a zero reference (the exact path then
-  // does the per-element class tests). The gate, the running maxima and
-  // sum_abs are exact binary64; the lane's quotient estimates feed sum_rel.
-  auto fast_step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0) __attribute__((always_inline)) -> bool {
-    float sq0 = 0.f, sq1 = 0.f;
-    double sa = 0.0;
+  // Tier 1 (binary32) for a full step; returns false (and changes nothing)
+  // when some element is not finite, has r = 0, is outside the exactness
+  // bound, or (single pair) falls between the gate bounds.
+  auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0)
+                     __attribute__((always_inline)) -> bool {
+    float sa0 = 0.f, sa1 = 0.f, sq0 = 0.f, sq1 = 0.f;
+    float md = 0.f, me = -__builtin_inff(), mq = 0.f, mr = 0.f;
     uint32_t fcnt[NT];
 #pragma unroll
     for (int p = 0; p < NT; ++p) fcnt[p] = 0;
-    uint64_t pany = 0;
-    // lanes with an element whose |c - r| exceeds best_abs / whose exact
-    // quotient exceeds best_rel (per-element compares into wave masks; a
-    // per-lane OR would be rewritten by the compiler into a max reduction)
-    uint64_t absm = 0, relm = 0;
+    uint64_t fany = 0;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      const float c32 = dec32<DT>(elem<DT>(cq, j));
-      const float r32 = dec32<DT>(elem<DT>(rq, j));
-      const double c = c32, r = r32;
+      const float c = dec32<DT>(elem<DT>(cq, j));
+      const float r = dec32<DT>(elem<DT>(rq, j));
+      const float d = __builtin_fabsf(c - r);
+      const float a = __builtin_fabsf(r);
+      if constexpr (NT == 1) {
+        const uint64_t f = ballot(d > __builtin_fmaf(a, rlo, alo));
+        fcnt[0] += popc(f);
+        fany |= f;
+      } else {
+        const double d64 = d, a64 = a;
+#pragma unroll
+        for (int p = 0; p < NT; ++p) {
+          const double t = atol[p] + rtol[p] * a64;
+          const uint64_t f = ballot(d64 > t);
+          fcnt[p] += popc(f);
+          if (p == prim) fany |= f;
+        }
+      }
+      const float ra = __builtin_amdgcn_rcpf(a);
+      const float q = d * ra;
+      if (j & 1) {
+        sa1 += d;
+        sq1 += q;
+      } else {
+        sa0 += d;
+        sq0 += q;
+      }
+      md = __builtin_fmaxf(md, d);
+      mq = __builtin_fmaxf(mq, q);
+      me = __builtin_fmaxf(me, __builtin_fmaf(-b_rel, a, d));
+      // |r| in [2^-60, 2^124]: the reciprocal, the quotient and the gate
+      // thresholds stay in the normal binary32 range
+      if constexpr (DT != VC_F16) mr = __builtin_fmaxf(mr, __builtin_fmaf(a, 0x1p-64f, ra));
+    }
+    const float sa = sa0 + sa1, sq = sq0 + sq1;
+    bool ok = __builtin_isfinite(sa + sq) && mq <= QT;
+    if constexpr (DT != VC_F16) ok = ok && mr <= 0x1p60f;
+    if (ballot(!ok) != 0) return false;
+    uint32_t pb = 0;
+    if (fany != 0) {
+      // primary-pair bits, and (single pair) the elements between the bounds
+      uint64_t amb = 0;
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float c = dec32<DT>(elem<DT>(cq, j));
+        const float r = dec32<DT>(elem<DT>(rq, j));
+        const float d = __builtin_fabsf(c - r);
+        const float a = __builtin_fabsf(r);
+        bool f;
+        if constexpr (NT == 1) {
+          f = d > __builtin_fmaf(a, rlo, alo);
+          amb |= ballot(f && !(d > __builtin_fmaf(a, rhi, ahi)));
+        } else {
+          const double a64 = a;
+          double t = 0.0;
+#pragma unroll
+          for (int p = 0; p < NT; ++p)
+            if (p == prim) t = atol[p] + rtol[p] * a64;
+          f = (double)d > t;
+        }
+        pb |= (f ? 1u : 0u) << j;
+      }
+      if (amb != 0) return false;
+    }
+#pragma unroll
+    for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
+    ++fast_steps;
+    acc_abs += (double)sa;
+    acc_rel += (double)sq;
+    const uint32_t off0 = (uint32_t)(i0 - cstart);
+    const uint64_t absm = ballot(md > thr_abs);
+    const uint64_t relm = ballot(me > 0.0f);
+    if ((absm | relm) != 0) t1_update(cq, rq, absm, relm, off0);
+    if (fany != 0) localize(pb, i0);
+    return true;
+  };
+
+  // Tier 2 (binary64) for a full step; returns false (and changes nothing)
+  // when the step holds a NaN, an infinity or a zero reference.
+  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0)
+                     __attribute__((always_inline)) -> bool {
+    double sa = 0.0, sq = 0.0;
+    uint32_t fcnt[NT];
+#pragma unroll
+    for (int p = 0; p < NT; ++p) fcnt[p] = 0;
+    uint64_t pany = 0, absm = 0, relm = 0;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const double c = dec64<DT>(elem<DT>(cq, j));
+      const double r = dec64<DT>(elem<DT>(rq, j));
       const double d = __builtin_fabs(c - r);
       const double a = __builtin_fabs(r);
 #pragma unroll
@@ -470,57 +994,19 @@ void main_kernel(const Params P) {
         if (p == prim) pany |= f;
       }
       sa += d;
-      absm |= ballot(d > best_abs);
-      relm |= ballot(__builtin_fma(-best_rel, a, d) > 0.0);
-      const float q = __builtin_fabsf((float)d * __builtin_amdgcn_rcpf(r32));
-      if (j & 1) sq1 += q;
-      else sq0 += q;
+      sq += d * __builtin_amdgcn_rcp(a);
+      absm |= ballot(d > T_abs);
+      relm |= ballot(__builtin_fma(-T_rel, a, d) > 0.0);
     }
-    // finite iff every c and r of the lane is finite and every r != 0
-    if (ballot(!__builtin_isfinite(sq0 + sq1)) != 0) return false;
+    if (ballot(!__builtin_isfinite(sa + sq)) != 0) return false;
 #pragma unroll
     for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
     ++fast_steps;
     acc_abs += sa;
-    acc_rel += (double)sq0 + (double)sq1;
+    acc_rel += sq;
     const uint32_t off0 = (uint32_t)(i0 - cstart);
-    const uint64_t lane_bit = 1ull << lane;
-    if (absm != 0) {
-      double lb = -1.0;
-      uint32_t li = 0xffffffffu;
-      if (absm & lane_bit) {
-#pragma unroll
-        for (int j = 0; j < V; ++j) {  // lane max, smallest j on ties
-          const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - dec64<DT>(elem<DT>(rq, j)));
-          if (d > lb) {
-            lb = d;
-            li = off0 + j;
-          }
-        }
-      }
-      merge_abs(lb, li);
-    }
-    if (relm != 0) {
-      double lb = -1.0;
-      uint32_t li = 0xffffffffu;
-      if (relm & lane_bit) {
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const double r = dec64<DT>(elem<DT>(rq, j));
-          const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
-          const double a = __builtin_fabs(r);
-          // exact sign test: d / a > best_rel  <=>  d - best_rel * a > 0
-          if (__builtin_fma(-best_rel, a, d) > 0.0) {
-            const double q = d / a;
-            if (q > lb) {
-              lb = q;
-              li = off0 + j;
-            }
-          }
-        }
-      }
-      merge_rel(lb, li);
-    }
+    if (absm != 0) abs_update(cq, rq, absm, off0);
+    if (relm != 0) rel_update(cq, rq, relm, off0);
     if (pany != 0) {
       uint32_t pb = 0;
 #pragma unroll 1
@@ -539,7 +1025,7 @@ void main_kernel(const Params P) {
   };
 
   // Degenerate-output detector counts of one step (bitwise; NaN handling of
-  // the binary16 test is added by the exact path).
+  // the binary16 test is added by the exact tier).
   auto integ_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, bool full,
                         uint64_t i0) __attribute__((always_inline)) {
 #pragma unroll
@@ -583,7 +1069,9 @@ void main_kernel(const Params P) {
   };
 
   auto step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0) __attribute__((always_inline)) {
-    if (!fast_step(cq, rq, i0)) exact_step(cq, rq, ALL, i0);
+    bool done = t1ok && t1_step(cq, rq, i0);
+    if (!done) done = t2_step(cq, rq, i0);
+    if (!done) exact_step(cq, rq, ALL, i0);
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, i0);
   };
 
@@ -592,7 +1080,9 @@ void main_kernel(const Params P) {
   const uint64_t n_steps = (cend - cstart) / ITER;  // full steps in the chunk
   const uint64_t n_full = n_steps > wave ? (n_steps - wave + 3) / 4 : 0;
   const uint64_t lane_off = (uint64_t)lane * V;
-  auto step_i0 = [&](uint64_t st) __attribute__((always_inline)) { return cstart + (wave + 4 * st) * ITER + lane_off; };
+  auto step_i0 = [&](uint64_t st) __attribute__((always_inline)) {
+    return cstart + (wave + 4 * st) * ITER + lane_off;
+  };
   if (vec) {
     // Two steps per trip with the next step's loads in flight. The loads are
     // unconditional (past the end they re-read the last step, a cache hit) so
@@ -637,15 +1127,16 @@ void main_kernel(const Params P) {
     if constexpr (INTEG) integ_step(ct, rt, vmask, false, i0);
   }
 
-
-  // wave reduction (fixed butterfly order)
+  // wave reductions (fixed butterfly order)
+  wave_max(lb_abs, li_abs);
+  wave_max(lb_rel, li_rel);
 #pragma unroll
   for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
     acc_abs += __shfl_xor(acc_abs, m);
     acc_rel += __shfl_xor(acc_rel, m);
   }
   if (lane == 0) {
-    WaveOut &o = s_out[wave];
+    ChunkRec &o = s_out[wave];
 #pragma unroll
     for (int p = 0; p < VC_MAX_TOLS; ++p) o.mism[p] = p < NT ? mism[p] : 0u;
     const uint32_t *const rc = s_rare[wave];
@@ -656,420 +1147,187 @@ void main_kernel(const Params P) {
     o.n_fin = rc[4] + fast_steps * ITER;
     o.n_rel = rc[5] + fast_steps * ITER;
     o.n_rel_undef = rc[6];
+    o.zero_c = zc;
+    o.zero_r = zr;
+    o.eqf_c = efc;
+    o.eqf_r = efr;
+    o.bf_c = bfc;
+    o.bf_r = bfr;
+    o.f16_c = hfc;
+    o.f16_r = hfr;
+    o.nfound = nfound;
     o.eq_bits = (diff_cr == 0 ? kEqCandRef : 0u) | (eqc << kEqCandInpShift) |
                 (eqr << kEqRefInpShift);
-    o.nfound = nfound;
-    o.zc = zc;
-    o.zr = zr;
-    o.efc = efc;
-    o.efr = efr;
-    o.bfc = bfc;
-    o.bfr = bfr;
-    o.hfc = hfc;
-    o.hfr = hfr;
-    o.max_abs = best_abs;
-    o.amax_abs = arg_abs;
-    o.max_rel = best_rel;
-    o.amax_rel = arg_rel;
+    o.amax_abs = li_abs;
+    o.amax_rel = li_rel;
+    o.pad = 0;
+    o.max_abs = li_abs == kNone ? -1.0 : lb_abs;
+    o.max_rel = li_rel == kNone ? -1.0 : lb_rel;
     o.sum_abs = acc_abs;
     o.sum_rel = acc_rel;
   }
   __syncthreads();
   // flush the tile window (all four waves are done with it)
-  if (do_tiles && win_ok) {
-    for (uint32_t e = threadIdx.x; e < (uint32_t)kTileWindow; e += kBlockThreads) {
-      const uint32_t v = s_win[e];
-      if (v != 0) atomicAdd(&tile_maps[tile_off + win_base + e], v);
-    }
+  for (uint32_t e = threadIdx.x; e < win_len; e += kBlockThreads) {
+    const uint32_t v = sh_st.win[e];
+    if (v != 0) atomicAdd(&tile_maps[tile_off + win_base + e], v);
   }
   // Merge the four waves' ascending first-k lists (disjoint index sets) into
   // the k smallest: an entry's rank is its position in its own list plus the
   // number of smaller entries in the other three.
   uint32_t merged = 0;
+  const uint32_t *const stage0 = P.stage + (uint64_t)chunk * kWavesPerBlock * (uint64_t)(kk > 0 ? kk : 0);
   if (kk > 0) {
     const uint32_t k = (uint32_t)kk;
-    uint32_t nf[kWavesPerBlock], total = 0;
-    for (int w = 0; w < kWavesPerBlock; ++w) {
-      nf[w] = s_out[w].nfound;
-      total += nf[w];
-    }
+    const uint32_t total =
+        s_out[0].nfound + s_out[1].nfound + s_out[2].nfound + s_out[3].nfound;
     if (total > 0) {
-      const uint32_t *base = P.stage + (uint64_t)chunk * kWavesPerBlock * k;
       for (uint32_t e = threadIdx.x; e < kWavesPerBlock * k; e += kBlockThreads) {
         const uint32_t w = e / k, i = e % k;
-        if (i >= nf[w]) continue;
-        const uint32_t x = base[w * k + i];
+        if (i >= s_out[w].nfound) continue;
+        const uint32_t x = stage0[w * k + i];
         uint32_t rank = i;
         for (uint32_t v = 0; v < (uint32_t)kWavesPerBlock; ++v) {
           if (v == w) continue;
-          uint32_t lo = 0, hi = nf[v];  // count of list v below x
+          uint32_t lo = 0, hi = s_out[v].nfound;  // count of list v below x
           while (lo < hi) {
             const uint32_t mid = (lo + hi) / 2;
-            if (base[v * k + mid] < x) lo = mid + 1;
+            if (stage0[v * k + mid] < x) lo = mid + 1;
             else hi = mid;
           }
           rank += lo;
         }
-        if (rank < k) s_merged[rank] = x;
+        if (rank < k) sh_st.merged[rank] = x;
       }
       merged = min(total, k);
       __syncthreads();
       for (uint32_t e = threadIdx.x; e < merged; e += kBlockThreads)
-        P.stage[(uint64_t)chunk * kWavesPerBlock * k + e] = s_merged[e];
+        P.stage[(uint64_t)chunk * kWavesPerBlock * k + e] = sh_st.merged[e];
     }
   }
-  if (threadIdx.x == 0) {
-    ChunkRec rec;
-    const WaveOut &w0 = s_out[0];
-#pragma unroll
-    for (int p = 0; p < VC_MAX_TOLS; ++p) rec.mism[p] = w0.mism[p];
-    rec.nan_c = w0.nan_c;
-    rec.inf_c = w0.inf_c;
-    rec.nan_r = w0.nan_r;
-    rec.inf_r = w0.inf_r;
-    rec.n_fin = w0.n_fin;
-    rec.n_rel = w0.n_rel;
-    rec.n_rel_undef = w0.n_rel_undef;
-    rec.eq_bits = w0.eq_bits;
-    rec.zero_c = w0.zc;
-    rec.zero_r = w0.zr;
-    rec.eqf_c = w0.efc;
-    rec.eqf_r = w0.efr;
-    rec.bf_c = w0.bfc;
-    rec.bf_r = w0.bfr;
-    rec.f16_c = w0.hfc;
-    rec.f16_r = w0.hfr;
-    rec.max_abs = w0.max_abs;
-    rec.amax_abs = w0.amax_abs;
-    rec.max_rel = w0.max_rel;
-    rec.amax_rel = w0.amax_rel;
-    rec.sum_abs = w0.sum_abs;
-    rec.sum_rel = w0.sum_rel;
-    for (int w = 1; w < kWavesPerBlock; ++w) {
-      const WaveOut &o = s_out[w];
-#pragma unroll
-      for (int p = 0; p < VC_MAX_TOLS; ++p) rec.mism[p] += o.mism[p];
-      rec.nan_c += o.nan_c;
-      rec.inf_c += o.inf_c;
-      rec.nan_r += o.nan_r;
-      rec.inf_r += o.inf_r;
-      rec.n_fin += o.n_fin;
-      rec.n_rel += o.n_rel;
-      rec.n_rel_undef += o.n_rel_undef;
-      rec.eq_bits &= o.eq_bits;
-      rec.zero_c += o.zc;
-      rec.zero_r += o.zr;
-      rec.eqf_c += o.efc;
-      rec.eqf_r += o.efr;
-      rec.bf_c += o.bfc;
-      rec.bf_r += o.bfr;
-      rec.f16_c += o.hfc;
-      rec.f16_r += o.hfr;
-      max_merge(rec.max_abs, rec.amax_abs, o.max_abs, o.amax_abs);
-      max_merge(rec.max_rel, rec.amax_rel, o.max_rel, o.amax_rel);
-      rec.sum_abs += o.sum_abs;
-      rec.sum_rel += o.sum_rel;
-    }
-    rec.nfound[0] = merged;
-    for (int w = 1; w < kWavesPerBlock; ++w) rec.nfound[w] = 0;
-    rec.pad0 = rec.pad1 = 0;
-    P.recs[chunk] = rec;
-  }
-}
-
-// ---------------------------------------------------------------- finalize
-
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) x += __shfl_xor(x, m);
-  return x;
-}
-
-__device__ __forceinline__ double wave_sum_f64(double x) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) x += __shfl_xor(x, m);
-  return x;
-}
-
-struct FinScratch {
-  uint64_t u[kWavesPerBlock];
-  double d[kWavesPerBlock];
-  uint64_t idx[kWavesPerBlock];
-  uint32_t scan[kBlockThreads];
-  uint32_t eq[kWavesPerBlock];
-};
-
-// Block-wide sums in a fixed order: wave butterfly, then waves 0..3.
-__device__ uint64_t block_sum_u64(FinScratch &s, uint64_t x) {
-  x = wave_sum_u64(x);
-  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
-  __syncthreads();
-  if (lane == 0) s.u[wave] = x;
-  __syncthreads();
-  uint64_t t = 0;
-  for (int w = 0; w < kWavesPerBlock; ++w) t += s.u[w];
-  return t;
-}
-
-__device__ double block_sum_f64(FinScratch &s, double x) {
-  x = wave_sum_f64(x);
-  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
-  __syncthreads();
-  if (lane == 0) s.d[wave] = x;
-  __syncthreads();
-  double t = 0.0;
-  for (int w = 0; w < kWavesPerBlock; ++w) t += s.d[w];
-  return t;
-}
-
-// Block-wide (max value, smallest index); idx = UINT64_MAX marks "none".
-__device__ void block_max(FinScratch &s, double &v, uint64_t &idx) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
-    const double ov = __shfl_xor(v, m);
-    const uint64_t oi = __shfl_xor(idx, m);
-    if (ov > v || (ov == v && oi < idx)) {
-      v = ov;
-      idx = oi;
+  // the chunk record: counter word q by thread q, the rest by thread 32
+  {
+    ChunkRec *const rec = P.recs + chunk;
+    const uint32_t q = threadIdx.x;
+    if (q < (uint32_t)kRecCounts) {
+      uint32_t a = 0;
+      for (int w = 0; w < kWavesPerBlock; ++w) a += ((const uint32_t *)&s_out[w])[q];
+      ((uint32_t *)rec)[q] = a;
+    } else if (q == 32) {
+      uint32_t eqb = s_out[0].eq_bits;
+      double ma = s_out[0].max_abs, mr = s_out[0].max_rel;
+      uint32_t ia = s_out[0].amax_abs, ir = s_out[0].amax_rel;
+      double sa = s_out[0].sum_abs, sr = s_out[0].sum_rel;
+      for (int w = 1; w < kWavesPerBlock; ++w) {
+        eqb &= s_out[w].eq_bits;
+        max_merge(ma, ia, s_out[w].max_abs, s_out[w].amax_abs);
+        max_merge(mr, ir, s_out[w].max_rel, s_out[w].amax_rel);
+        sa += s_out[w].sum_abs;
+        sr += s_out[w].sum_rel;
+      }
+      rec->nfound = merged;
+      rec->eq_bits = eqb;
+      rec->amax_abs = ia;
+      rec->amax_rel = ir;
+      rec->pad = 0;
+      rec->max_abs = ma;
+      rec->max_rel = mr;
+      rec->sum_abs = sa;
+      rec->sum_rel = sr;
     }
   }
-  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
-  __syncthreads();
-  if (lane == 0) {
-    s.d[wave] = v;
-    s.idx[wave] = idx;
-  }
-  __syncthreads();
-  v = s.d[0];
-  idx = s.idx[0];
-  for (int w = 1; w < kWavesPerBlock; ++w)
-    if (s.d[w] > v || (s.d[w] == v && s.idx[w] < idx)) {
-      v = s.d[w];
-      idx = s.idx[w];
-    }
+
 }
 
-__device__ uint32_t block_and_u32(FinScratch &s, uint32_t x) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) x &= __shfl_xor(x, m);
-  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
-  __syncthreads();
-  if (lane == 0) s.eq[wave] = x;
-  __syncthreads();
-  uint32_t t = 0xffffffffu;
-  for (int w = 0; w < kWavesPerBlock; ++w) t &= s.eq[w];
-  return t;
-}
+// ------------------------------------------------------------ finalize
 
-// Exclusive prefix of x over the block (thread order); returns the total too.
-__device__ uint32_t block_exscan_u32(FinScratch &s, uint32_t x, uint32_t &total) {
-  __syncthreads();
-  s.scan[threadIdx.x] = x;
-  __syncthreads();
-  for (uint32_t off = 1; off < (uint32_t)kBlockThreads; off <<= 1) {
-    const uint32_t v = threadIdx.x >= off ? s.scan[threadIdx.x - off] : 0u;
-    __syncthreads();
-    s.scan[threadIdx.x] += v;
-    __syncthreads();
-  }
-  total = s.scan[kBlockThreads - 1];
-  return s.scan[threadIdx.x] - x;
-}
-
+// One block per chunk group (every group of the call, one launch after the
+// streaming kernels). A case with one group is written directly from its
+// chunk records; otherwise the group's chunk records are merged into a group
+// record and the last group of the case (completion counter) writes the
+// case from the group records.
 __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P) {
-  __shared__ FinScratch s;
-  const uint64_t ci = P.case_lo + blockIdx.x;
+  __shared__ MergeScratch M;
+  __shared__ uint32_t s_flag;
+  const uint64_t g = blockIdx.x;
+  const VCK_CONST DevCase *table = (const VCK_CONST DevCase *)P.cases;
+  uint64_t ci = 0;
   DevCase cs;
-  if (P.cases != nullptr) cs = load_case((const VCK_CONST DevCase *)P.cases + ci);
-  else cs = P.single;
-  const uint32_t oi = cs.orig;
-  const int nt = P.n_tols;
+  if (table != nullptr) {
+    ci = find_entry(P.case_group, 0, (uint64_t)P.n_cases, g);
+    cs = load_case(table + ci);
+  } else {
+    cs = P.single;
+  }
+  FinArgs F;
+  F.stats = P.stats;
+  F.mismatches = P.mismatches;
+  F.pass_out = P.pass_out;
+  F.first_k = P.first_k;
+  F.integ = P.integ;
+  F.match_rate = P.match_rate;
+  F.numeric_rate = P.numeric_rate;
+  F.ctr = P.ctr;
+  F.n_cases = P.n_cases;
+  F.n_tols = P.n_tols;
+  F.primary = P.primary;
+  F.k = P.k;
+  F.do_integ = P.do_integ;
   const uint64_t CH = 4ull * cs.unit_elems;
-  const uint32_t n_chunks = cs.n_chunks;
-
-  uint64_t mism[VC_MAX_TOLS];
-  for (int p = 0; p < VC_MAX_TOLS; ++p) mism[p] = 0;
-  uint64_t cnt[7] = {0, 0, 0, 0, 0, 0, 0};
-  uint64_t ic[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  double sa = 0.0, sr = 0.0;
-  double mav = -1.0, mrv = -1.0;
-  uint64_t mai = UINT64_MAX, mri = UINT64_MAX;
-  uint32_t eqb = 0xffffffffu;
-  for (uint32_t c = threadIdx.x; c < n_chunks; c += kBlockThreads) {
-    const ChunkRec &r = P.recs[cs.chunk_begin + c];
-    for (int p = 0; p < VC_MAX_TOLS; ++p) mism[p] += r.mism[p];
-    cnt[0] += r.nan_c;
-    cnt[1] += r.inf_c;
-    cnt[2] += r.nan_r;
-    cnt[3] += r.inf_r;
-    cnt[4] += r.n_fin;
-    cnt[5] += r.n_rel;
-    cnt[6] += r.n_rel_undef;
-    ic[0] += r.zero_c;
-    ic[1] += r.zero_r;
-    ic[2] += r.eqf_c;
-    ic[3] += r.eqf_r;
-    ic[4] += r.bf_c;
-    ic[5] += r.bf_r;
-    ic[6] += r.f16_c;
-    ic[7] += r.f16_r;
-    eqb &= r.eq_bits;
-    sa += r.sum_abs;
-    sr += r.sum_rel;
-    if (r.amax_abs != 0xffffffffu) {
-      const uint64_t gi = (uint64_t)c * CH + r.amax_abs;
-      if (r.max_abs > mav || (r.max_abs == mav && gi < mai)) {
-        mav = r.max_abs;
-        mai = gi;
-      }
-    }
-    if (r.amax_rel != 0xffffffffu) {
-      const uint64_t gi = (uint64_t)c * CH + r.amax_rel;
-      if (r.max_rel > mrv || (r.max_rel == mrv && gi < mri)) {
-        mrv = r.max_rel;
-        mri = gi;
-      }
+  const uint32_t k = P.k > 0 ? (uint32_t)P.k : 0u;
+  const uint64_t cstride = (uint64_t)kWavesPerBlock * k;
+  if (cs.n_groups == 1) {
+    finalize_case(M, F, cs, P.recs + cs.chunk_begin, cs.n_chunks, CH,
+                  P.stage + cs.chunk_begin * cstride, cstride);
+    return;
+  }
+  const uint32_t g_local = (uint32_t)(g - cs.group_begin);
+  const uint32_t gc0 = g_local * kGroupChunks;
+  const uint32_t gchunks = min((uint32_t)kGroupChunks, cs.n_chunks - gc0);
+  const ChunkRec *const grp = P.recs + cs.chunk_begin + gc0;
+  merge_recs(M, grp, gchunks, CH);
+  uint32_t gnf = 0;
+  if (k > 0)
+    gnf = gather_firstk<false>(M, grp, gchunks, CH, P.stage + (cs.chunk_begin + gc0) * cstride,
+                               cstride, k, P.gstage + g * k, nullptr);
+  {
+    ChunkRec *const gr = P.grecs + g;
+    const uint32_t q = threadIdx.x;
+    if (q < (uint32_t)kRecCounts) {
+      ((uint32_t *)gr)[q] = (uint32_t)M.cnt[q];
+    } else if (q == 32) {
+      gr->nfound = gnf;
+      gr->eq_bits = M.eq_all;
+      gr->amax_abs = M.amax_abs == UINT64_MAX ? kNone : (uint32_t)M.amax_abs;
+      gr->amax_rel = M.amax_rel == UINT64_MAX ? kNone : (uint32_t)M.amax_rel;
+      gr->pad = 0;
+      gr->max_abs = M.max_abs;
+      gr->max_rel = M.max_rel;
+      gr->sum_abs = M.sum_abs;
+      gr->sum_rel = M.sum_rel;
     }
   }
-  for (int p = 0; p < VC_MAX_TOLS; ++p) mism[p] = block_sum_u64(s, mism[p]);
-  for (int q = 0; q < 7; ++q) cnt[q] = block_sum_u64(s, cnt[q]);
-  for (int q = 0; q < 8; ++q) ic[q] = block_sum_u64(s, ic[q]);
-  sa = block_sum_f64(s, sa);
-  sr = block_sum_f64(s, sr);
-  block_max(s, mav, mai);
-  block_max(s, mrv, mri);
-  eqb = block_and_u32(s, eqb);
-
-  const bool ok = cs.status == 0;
-  if (!ok) {
-    for (int p = 0; p < VC_MAX_TOLS; ++p) mism[p] = 0;
-    for (int q = 0; q < 7; ++q) cnt[q] = 0;
-    for (int q = 0; q < 8; ++q) ic[q] = 0;
-    sa = sr = 0.0;
-    mai = mri = UINT64_MAX;
-    eqb = 0;
-  }
-  const uint64_t n = ok ? cs.numel : 0;
-
-  // ordered first-k: walk chunks in order, waves in order
-  if (P.first_k != nullptr && P.k > 0) {
-    const uint32_t k = (uint32_t)P.k;
-    int64_t *const fk = P.first_k + (uint64_t)oi * k;
-    uint32_t carry = 0;
-    if (ok) {
-      for (uint32_t b = 0; b < n_chunks && carry < k; b += kBlockThreads) {
-        const uint32_t c = b + threadIdx.x;
-        uint32_t cntc = 0;
-        const ChunkRec *r = c < n_chunks ? &P.recs[cs.chunk_begin + c] : nullptr;
-        if (r != nullptr)
-          for (int w = 0; w < kWavesPerBlock; ++w) cntc += r->nfound[w];
-        uint32_t total;
-        const uint32_t ex = block_exscan_u32(s, cntc, total);
-        if (cntc != 0 && carry + ex < k) {
-          uint32_t pos = carry + ex;
-          for (int w = 0; w < kWavesPerBlock && pos < k; ++w) {
-            const uint32_t *st = P.stage + ((cs.chunk_begin + c) * kWavesPerBlock + w) * k;
-            for (uint32_t e = 0; e < r->nfound[w] && pos < k; ++e, ++pos)
-              fk[pos] = (int64_t)((uint64_t)c * CH + st[e]);
-          }
-        }
-        carry = min(carry + total, k);
-      }
-    }
-    for (uint32_t pos = carry + threadIdx.x; pos < k; pos += kBlockThreads) fk[pos] = -1;
-  }
-
-  if (threadIdx.x != 0) return;
-  const int prim = P.primary;
-  vc_stats st;
-  st.numel = cs.numel;
-  st.mismatches = mism[prim];
-  st.nan_cand = cnt[0];
-  st.inf_cand = cnt[1];
-  st.nan_ref = cnt[2];
-  st.inf_ref = cnt[3];
-  st.n_finite = cnt[4];
-  st.n_rel = cnt[5];
-  st.n_rel_undef = cnt[6];
-  st.max_abs = mai == UINT64_MAX ? 0.0 : mav;
-  st.argmax_abs = mai == UINT64_MAX ? -1 : (int64_t)mai;
-  st.max_rel = mri == UINT64_MAX ? 0.0 : mrv;
-  st.argmax_rel = mri == UINT64_MAX ? -1 : (int64_t)mri;
-  st.sum_abs = sa;
-  st.sum_rel = sr;
-  st.case_status = cs.status;
-  st.pass = (ok && mism[prim] == 0) ? 1 : 0;
-  if (P.stats != nullptr) P.stats[oi] = st;
-  for (int p = 0; p < nt; ++p) {
-    const uint8_t pass = (ok && mism[p] == 0) ? 1 : 0;
-    P.ws_pass[(uint64_t)oi * nt + p] = pass;
-    if (P.pass_out != nullptr) P.pass_out[(uint64_t)oi * nt + p] = pass;
-    if (P.mismatches != nullptr) P.mismatches[(uint64_t)oi * nt + p] = mism[p];
-  }
-  uint32_t flags = 0;
-  if (P.do_integ) {
-    vc_integrity g;
-    g.zero_cand = ic[0];
-    g.zero_ref = ic[1];
-    g.eqfirst_cand = ic[2];
-    g.eqfirst_ref = ic[3];
-    g.bf16rep_cand = ic[4];
-    g.bf16rep_ref = ic[5];
-    g.fp16rep_cand = ic[6];
-    g.fp16rep_ref = ic[7];
-    const uint32_t inp_mask = ok ? cs.inp_mask : 0u;
-    const uint32_t eq_c = (eqb >> kEqCandInpShift) & 0xffu & inp_mask;
-    const uint32_t eq_r = (eqb >> kEqRefInpShift) & 0xffu & inp_mask;
-    g.cand_eq_input_mask = eq_c;
-    g.ref_eq_input_mask = eq_r;
-    g.cand_eq_ref = ok ? (eqb & kEqCandRef) : 0u;
-    g.copy_input = -1;
-    if (ok) {
-      const bool f32 = cs.dtype == VC_F32;
-      if (ic[0] == n && n >= 1 && ic[1] < n) flags |= VC_FLAG_ALL_ZERO;
-      if (ic[2] == n && n >= 2 && ic[0] < n && ic[3] < n) flags |= VC_FLAG_CONSTANT;
-      const uint32_t copy = eq_c & ~eq_r;
-      if (copy != 0) {
-        flags |= VC_FLAG_INPUT_COPY;
-        g.copy_input = __builtin_ctz(copy);
-      }
-      if (f32 && ic[4] == n && n >= 2 && ic[0] < n && ic[2] < n && ic[5] < n)
-        flags |= VC_FLAG_LOWPREC_BF16;
-      if (f32 && ic[6] == n && ic[4] < n && n >= 2 && ic[0] < n && ic[2] < n && ic[7] < n)
-        flags |= VC_FLAG_LOWPREC_FP16;
-    }
-    g.flags = flags;
-    g.reserved = 0;
-    if (P.integ != nullptr) P.integ[oi] = g;
-  }
-  P.ws_flags[oi] = flags;
+  if (!arrive_last(&P.case_cnt[ci], cs.n_groups - 1u, s_flag)) return;
+  finalize_case(M, F, cs, P.grecs + cs.group_begin, cs.n_groups, CH * kGroupChunks,
+                P.gstage + cs.group_begin * k, k);
 }
 
-// Suite match rates: certified (and numerically passing) cases per pair.
-__global__ __launch_bounds__(kBlockThreads) void rates_kernel(const Params P) {
-  __shared__ FinScratch s;
-  const int nt = P.n_tols;
-  for (int p = 0; p < nt; ++p) {
-    uint64_t cert = 0, num = 0;
-    for (uint64_t c = threadIdx.x; c < (uint64_t)P.n_cases; c += kBlockThreads) {
-      const bool pass = P.ws_pass[c * nt + p] != 0;
-      num += pass;
-      cert += pass && (!P.do_integ || P.ws_flags[c] == 0);
-    }
-    cert = block_sum_u64(s, cert);
-    num = block_sum_u64(s, num);
-    if (threadIdx.x == 0) {
-      const double n = (double)P.n_cases;
-      if (P.match_rate != nullptr) P.match_rate[p] = P.n_cases > 0 ? (double)cert / n : 0.0;
-      if (P.numeric_rate != nullptr) P.numeric_rate[p] = P.n_cases > 0 ? (double)num / n : 0.0;
-    }
+// Copies the descriptor blob from pinned host memory, clears the counter
+// area and the tile maps; writes zero rates for a sweep without cases.
+__global__ __launch_bounds__(256) void prologue_kernel(const Prologue Q) {
+  const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t nth = (uint64_t)gridDim.x * blockDim.x;
+  if (Q.blob_src != nullptr) {
+    const u32x4 *src = (const u32x4 *)Q.blob_src;
+    u32x4 *dst = (u32x4 *)Q.blob_dst;
+    for (uint64_t i = tid; i < Q.blob_bytes / 16; i += nth) dst[i] = src[i];
   }
-}
-
-__global__ void fill_u32_kernel(uint32_t *p, uint64_t n) {
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (uint64_t)gridDim.x * blockDim.x)
-    p[i] = 0;
+  for (uint64_t i = tid; i < Q.zero_words; i += nth) Q.zero[i] = 0;
+  for (uint64_t i = tid; i < Q.n_tiles; i += nth) Q.tiles[i] = 0;
+  if (Q.n_cases == 0 && tid < (uint64_t)Q.n_tols) {
+    if (Q.match_rate != nullptr) Q.match_rate[tid] = 0.0;
+    if (Q.numeric_rate != nullptr) Q.numeric_rate[tid] = 0.0;
+  }
 }
 
 template <int DT, int NT, bool INTEG>
@@ -1098,10 +1356,20 @@ hipError_t launch_main_dt(int nt_class, int integ, const Params &p, uint64_t n_c
 
 }  // namespace
 
-hipError_t launch_fill_u32(uint32_t *p, uint64_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  const uint64_t blocks = (n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096;
-  hipLaunchKernelGGL(fill_u32_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p, n);
+hipError_t launch_prologue(const Prologue &p, hipStream_t s) {
+  uint64_t work = p.blob_bytes / 16;
+  if (p.zero_words > work) work = p.zero_words;
+  if (p.n_tiles > work) work = p.n_tiles;
+  uint64_t blocks = (work + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL(prologue_kernel, dim3((uint32_t)blocks), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const Params &p, uint64_t n_groups, hipStream_t s) {
+  if (n_groups == 0) return hipSuccess;
+  hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)n_groups), dim3(kBlockThreads), 0, s, p);
   return hipGetLastError();
 }
 
@@ -1113,18 +1381,6 @@ hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint
     case VC_F16: return launch_main_dt<VC_F16>(nt_class, integ, p, n_chunks, s);
     default: return launch_main_dt<VC_BF16>(nt_class, integ, p, n_chunks, s);
   }
-}
-
-hipError_t launch_finalize(const Params &p, uint64_t n_cases_in_table, hipStream_t s) {
-  if (n_cases_in_table == 0) return hipSuccess;
-  hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)n_cases_in_table), dim3(kBlockThreads), 0,
-                     s, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_rates(const Params &p, hipStream_t s) {
-  hipLaunchKernelGGL(rates_kernel, dim3(1), dim3(kBlockThreads), 0, s, p);
-  return hipGetLastError();
 }
 
 }  // namespace vck
