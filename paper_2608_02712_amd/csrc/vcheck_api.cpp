@@ -96,18 +96,19 @@ struct Plan {
   std::vector<vck::DevCase> table;
   std::vector<uint64_t> case_chunk;  // chunk_begin per table entry
   std::vector<uint64_t> case_group;  // group_begin per table entry
+  std::vector<uint32_t> multi;       // table indices of cases with more than one group
   std::vector<Group> groups;
   uint64_t total_chunks = 0;
   uint64_t total_groups = 0;
   uint64_t tiles_total = 0;
   int32_t n_cases = 0, n_tols = 1, nt_class = 1, k = 0, primary = 0, tile_h = 1, tile_w = 1;
   bool do_tiles = false, do_firstk = false, do_integ = false;
-  // workspace layout: [table | case_chunk | case_group] (the blob the
-  // prologue copies), chunk records, chunk staging, group records, group
-  // staging, then the counter area the prologue clears: Counters, case_cnt
-  size_t off_table = 0, off_cc = 0, off_cg = 0, blob_bytes = 0;
+  // workspace layout: [table | case_chunk | case_group | multi] (the blob
+  // the prologue copies), chunk records, chunk first-k lists, group records,
+  // group first-k lists, then the Counters the prologue clears
+  size_t off_table = 0, off_cc = 0, off_cg = 0, off_multi = 0, blob_bytes = 0;
   size_t off_recs = 0, off_stage = 0, off_grecs = 0, off_gstage = 0;
-  size_t off_ctr = 0, off_case_cnt = 0, ctr_bytes = 0;
+  size_t off_ctr = 0, ctr_bytes = 0;
   size_t bytes = 0;
 };
 
@@ -265,6 +266,7 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
       plan.table.push_back(d);
       plan.case_chunk.push_back(d.chunk_begin);
       plan.case_group.push_back(d.group_begin);
+      if (d.n_groups > 1) plan.multi.push_back((uint32_t)(plan.table.size() - 1));
     }
     g.case_hi = plan.table.size();
     g.n_chunks = chunk - g.chunk_lo;
@@ -279,20 +281,20 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
   plan.off_table = off;
   plan.off_cc = off + sizeof(vck::DevCase) * nc;  // 160 * n: 16-byte aligned
   plan.off_cg = plan.off_cc + sizeof(uint64_t) * nc;
-  plan.blob_bytes = (sizeof(vck::DevCase) * nc + 2 * sizeof(uint64_t) * nc + 15) / 16 * 16;
+  plan.off_multi = plan.off_cg + sizeof(uint64_t) * nc;
+  plan.blob_bytes =
+      (plan.off_multi - off + sizeof(uint32_t) * plan.multi.size() + 15) / 16 * 16;
   off += align_up(plan.blob_bytes);
   plan.off_recs = off;
   off += align_up(sizeof(vck::ChunkRec) * (size_t)plan.total_chunks);
   plan.off_stage = off;
-  off += align_up(sizeof(uint32_t) * (size_t)plan.total_chunks * vck::kWavesPerBlock *
-                  (size_t)plan.k);
+  off += align_up(sizeof(uint32_t) * (size_t)plan.total_chunks * (size_t)plan.k);
   plan.off_grecs = off;
   off += align_up(sizeof(vck::ChunkRec) * (size_t)plan.total_groups);
   plan.off_gstage = off;
   off += align_up(sizeof(uint32_t) * (size_t)plan.total_groups * (size_t)plan.k);
   plan.off_ctr = off;
-  plan.off_case_cnt = off + sizeof(vck::Counters);
-  plan.ctr_bytes = plan.off_case_cnt + sizeof(uint32_t) * nc - off;
+  plan.ctr_bytes = sizeof(vck::Counters);
   off += align_up(plan.ctr_bytes);
   plan.bytes = off + kAlign;  // slack for aligning the caller's base pointer
   return VC_OK;
@@ -434,7 +436,6 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
   P.grecs = (vck::ChunkRec *)(base + plan.off_grecs);
   P.gstage = (uint32_t *)(base + plan.off_gstage);
   P.ctr = (vck::Counters *)(base + plan.off_ctr);
-  P.case_cnt = (uint32_t *)(base + plan.off_case_cnt);
   P.tile_maps = plan.do_tiles ? out.tile_maps : nullptr;
   P.stats = out.stats;
   P.mismatches = out.mismatches;
@@ -465,12 +466,16 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
     P.cases = (const vck::DevCase *)(base + plan.off_table);
     P.case_chunk = (const uint64_t *)(base + plan.off_cc);
     P.case_group = (const uint64_t *)(base + plan.off_cg);
+    P.multi = (const uint32_t *)(base + plan.off_multi);
     blob.assign(plan.blob_bytes, 0);
     memcpy(blob.data(), plan.table.data(), sizeof(vck::DevCase) * plan.table.size());
     memcpy(blob.data() + (plan.off_cc - plan.off_table), plan.case_chunk.data(),
            sizeof(uint64_t) * plan.case_chunk.size());
     memcpy(blob.data() + (plan.off_cg - plan.off_table), plan.case_group.data(),
            sizeof(uint64_t) * plan.case_group.size());
+    if (!plan.multi.empty())
+      memcpy(blob.data() + (plan.off_multi - plan.off_table), plan.multi.data(),
+             sizeof(uint32_t) * plan.multi.size());
     const vc_status st = stage_blob(blob.data(), blob.size(), lock, slot);
     if (st != VC_OK) return st;
     Q.blob_src = (const uint8_t *)slot->dev;
@@ -506,7 +511,10 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
     st = hip_check(hipEventRecord(prof_end, stream), "profile end event");
     if (st != VC_OK) return st;
   }
-  return hip_check(vck::launch_finalize(P, plan.total_groups, stream), "finalize launch");
+  const bool rates = out.match_rate != nullptr || out.numeric_rate != nullptr;
+  const uint64_t n_multi = single ? (plan.table[0].n_groups > 1 ? 1 : 0) : plan.multi.size();
+  return hip_check(vck::launch_finalize(P, plan.total_groups, n_multi, rates, stream),
+                   "finalize launch");
 }
 
 vc_case one_case(const vc_tensor *cand, const vc_tensor *ref, const vc_tensor *inputs,

@@ -13,7 +13,7 @@ constexpr int kWaveSize = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWaveSize * kWavesPerBlock;
 constexpr int kTileWindow = 2048;  // LDS tile counters per block
-constexpr int kGroupChunks = 64;   // chunks merged by one group record
+constexpr int kGroupChunks = 256;  // chunks merged by one group record
 
 // Device-side case descriptor. The host builds one per case, in launch
 // order (grouped by dtype), and the prologue kernel copies the table into
@@ -65,13 +65,12 @@ constexpr uint32_t kEqCandRef = 1u;        // bit 0: cand bit-equal to ref
 constexpr int kEqCandInpShift = 8;         // bits 8..15: cand bit-equal to input j
 constexpr int kEqRefInpShift = 16;         // bits 16..23: ref bit-equal to input j
 
-// Completion counters at the start of the counter area of the workspace;
-// the per-case counters follow.
+// Suite counters in the workspace (cleared by the prologue, incremented by
+// the finalize launches, read by the rates kernel).
 struct Counters {
-  uint32_t cases_done;
   uint32_t pass[VC_MAX_TOLS];       // cases passing pair p numerically
   uint32_t cert[VC_MAX_TOLS];       // ... and with no integrity flag
-  uint32_t pad[15];
+  uint32_t pad[16];
 };
 static_assert(sizeof(Counters) == 128, "Counters layout");
 
@@ -80,6 +79,7 @@ struct Params {
   const DevCase *cases;        // device table, or nullptr: use `single`
   const uint64_t *case_chunk;  // [table entries] chunk_begin, for the case lookup
   const uint64_t *case_group;  // [table entries] group_begin, for the case lookup
+  const uint32_t *multi;       // table indices of the cases with more than one group
   int32_t n_cases;             // table entries (= caller cases)
   int32_t n_tols;              // 1 .. 8 (the kernel evaluates NT >= n_tols pairs)
   int32_t primary;
@@ -101,11 +101,10 @@ struct Params {
   float rlo, alo, rhi, ahi;
 
   ChunkRec *recs;              // [total chunks]
-  uint32_t *stage;             // [total chunks * 4 * k] first-k staging (offsets)
+  uint32_t *stage;             // [total chunks * k] first-k lists (chunk offsets)
   ChunkRec *grecs;             // [total groups]
   uint32_t *gstage;            // [total groups * k]
   Counters *ctr;
-  uint32_t *case_cnt;          // [table entries] groups completed
   uint32_t *tile_maps;         // user tile maps (nullable)
   // outputs
   vc_stats *stats;
@@ -138,6 +137,7 @@ struct Prologue {
 hipError_t launch_prologue(const Prologue &p, hipStream_t s);
 hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint64_t n_chunks,
                        hipStream_t s);
-hipError_t launch_finalize(const Params &p, uint64_t n_groups, hipStream_t s);
+hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi, bool rates,
+                           hipStream_t s);
 
 }  // namespace vck

@@ -246,168 +246,171 @@ __device__ __forceinline__ float f32_down(double x) {
 
 // ------------------------------------------------------------ merge helpers
 
-// Completion handshake of a block on `counter`: once every thread's stores
-// are complete, thread 0 publishes them device-wide (agent-scope release: one
-// L2 write-back per block, not per wave) and counts the block in; the block that arrives last acquires before it reads the other
-// blocks' records. Returns true (block-uniformly) for the last block.
-__device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t last, uint32_t &s_flag) {
-  // each wave waits until its own stores are performed in L2 (the barrier
-  // alone does not wait for them), so thread 0's write-back covers them all
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    s_flag = atomicAdd(counter, 1u) == last ? 1u : 0u;
-  }
-  __syncthreads();
-  const bool is_last = s_flag != 0;
-  if (is_last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return is_last;
-}
+// Merge of up to kBlockThreads records per pass: records are staged in LDS
+// with independent 16-byte loads, then reduced column by column in 8 fixed
+// parts of 32 records (a fixed order, so the binary64 sums are reproducible).
+constexpr int kParts = 8;
+constexpr int kPartLen = kBlockThreads / kParts;
 
 struct MergeScratch {
-  uint64_t part[8][32];
-  uint64_t cnt[32];
-  double dpart[kBlockThreads];
-  uint32_t scan[kBlockThreads];
-  double mv[kWavesPerBlock];
-  uint64_t mi[kWavesPerBlock];
-  uint32_t eq[kWavesPerBlock];
-  double max_abs, max_rel, sum_abs, sum_rel;
+  ChunkRec rec[kBlockThreads];
+  uint64_t part[kParts][kRecCounts];
+  double dpart[2][kParts];
+  double mv[2][kParts];
+  uint64_t mi[2][kParts];
+  uint32_t eqp[kParts];
+  uint32_t nfp[kParts];      // first-k entries per part (saturated at k)
+  uint32_t nfpre[kParts];    // exclusive prefix of nfp (saturated at k)
+  uint32_t nfstart[kBlockThreads];  // first output position of each record
+  // running totals over the passes
+  uint64_t cnt[kRecCounts];
+  double sum_abs, sum_rel, max_abs, max_rel;
   uint64_t amax_abs, amax_rel;
-  uint32_t eq_all;
+  uint32_t eq_all, nf_total;
 };
 
-// Block-wide (max value, smallest index); idx = UINT64_MAX marks "none".
-// Every thread gets the result.
-__device__ __forceinline__ void block_max(MergeScratch &s, double &v, uint64_t &idx) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
-    const double ov = __shfl_xor(v, m);
-    const uint64_t oi = __shfl_xor(idx, m);
-    max_merge(v, idx, ov, oi);
-  }
-  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
-  __syncthreads();
-  if (lane == 0) {
-    s.mv[wave] = v;
-    s.mi[wave] = idx;
-  }
-  __syncthreads();
-  v = s.mv[0];
-  idx = s.mi[0];
-  for (int w = 1; w < kWavesPerBlock; ++w) max_merge(v, idx, s.mv[w], s.mi[w]);
+__device__ __forceinline__ uint32_t sat_add(uint32_t a, uint32_t b, uint32_t k) {
+  const uint32_t s = a + b;
+  return (s < a || s > k) ? k : s;
 }
 
-__device__ __forceinline__ uint32_t block_and_u32(MergeScratch &s, uint32_t x) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) x &= __shfl_xor(x, m);
-  const uint32_t lane = threadIdx.x & (kWaveSize - 1), wave = threadIdx.x / kWaveSize;
-  __syncthreads();
-  if (lane == 0) s.eq[wave] = x;
-  __syncthreads();
-  uint32_t t = 0xffffffffu;
-  for (int w = 0; w < kWavesPerBlock; ++w) t &= s.eq[w];
-  return t;
-}
-
-// Exclusive prefix of x over the block (thread order); returns the total too.
-__device__ __forceinline__ uint32_t block_exscan_u32(MergeScratch &s, uint32_t x, uint32_t &total) {
-  __syncthreads();
-  s.scan[threadIdx.x] = x;
-  __syncthreads();
-  for (uint32_t off = 1; off < (uint32_t)kBlockThreads; off <<= 1) {
-    const uint32_t v = threadIdx.x >= off ? s.scan[threadIdx.x - off] : 0u;
-    __syncthreads();
-    s.scan[threadIdx.x] += v;
-    __syncthreads();
-  }
-  total = s.scan[kBlockThreads - 1];
-  return s.scan[threadIdx.x] - x;
-}
-
-// Merges records recs[0..n) (record i covers elements [i*span, (i+1)*span)
-// of the parent range) in a fixed order; the totals land in s. Called by the
-// whole block; the records were written by other blocks, so the caller has
-// issued an acquire fence.
-__device__ __forceinline__ void merge_recs(MergeScratch &s, const ChunkRec *recs, uint32_t n, uint64_t span) {
-  const uint32_t t = threadIdx.x;
-  {
-    // counters: thread t sums word (t % 32) over records t/32, t/32 + 8, ...
-    const uint32_t f = t & 31, r0 = t >> 5;
-    uint64_t acc = 0;
-    if (f < (uint32_t)kRecCounts)
-      for (uint32_t r = r0; r < n; r += 8) acc += ((const uint32_t *)(recs + r))[f];
-    s.part[r0][f] = acc;
-  }
-  {
-    // binary64 sums: thread t sums field t % 2 over records t/2, t/2 + 128, ...
-    const uint32_t f = t & 1;
-    double acc = 0.0;
-    for (uint32_t r = t >> 1; r < n; r += kBlockThreads / 2)
-      acc += f ? recs[r].sum_rel : recs[r].sum_abs;
-    s.dpart[t] = acc;
-  }
-  double va = -1.0, vr = -1.0;
-  uint64_t ia = UINT64_MAX, ir = UINT64_MAX;
-  uint32_t eq = 0xffffffffu;
-  for (uint32_t r = t; r < n; r += kBlockThreads) {
-    const ChunkRec &x = recs[r];
-    eq &= x.eq_bits;
-    if (x.amax_abs != kNone) max_merge(va, ia, x.max_abs, (uint64_t)r * span + x.amax_abs);
-    if (x.amax_rel != kNone) max_merge(vr, ir, x.max_rel, (uint64_t)r * span + x.amax_rel);
-  }
-  __syncthreads();
-  if (t < 32) {
-    uint64_t a = 0;
-    for (int q = 0; q < 8; ++q) a += s.part[q][t];
-    s.cnt[t] = a;
-  }
-  if (t < 2) {
-    double a = 0.0;
-    for (uint32_t u = t; u < (uint32_t)kBlockThreads; u += 2) a += s.dpart[u];
-    if (t == 0) s.sum_abs = a;
-    else s.sum_rel = a;
-  }
-  block_max(s, va, ia);
-  block_max(s, vr, ir);
-  eq = block_and_u32(s, eq);
-  if (t == 0) {
-    s.max_abs = va;
-    s.amax_abs = ia;
-    s.max_rel = vr;
-    s.amax_rel = ir;
-    s.eq_all = eq;
-  }
-  __syncthreads();
-}
-
-// Copies the staged first-k lists of recs[0..n) in record order: entry e of
-// record r becomes element r * span + e of the parent range. Returns the
-// number of entries written (<= k); block-uniform.
+// Merges records recs[0..n) into the totals in s; record i covers elements
+// [i * span, (i + 1) * span) of the parent range. With k > 0 the staged
+// first-k lists are concatenated in record order (entry e of record i is
+// parent element i * span + e) into out64 (final: global indices) or out32
+// (a group: offsets within the group), at most k entries; s.nf_total is
+// their number. Called by the whole block; the totals are valid for every
+// thread on return.
 template <bool FINAL>
-__device__ __forceinline__ uint32_t gather_firstk(MergeScratch &s, const ChunkRec *recs, uint32_t n,
-                                  uint64_t span, const uint32_t *stage, uint64_t stage_stride,
-                                  uint32_t k, uint32_t *out32, int64_t *out64) {
-  uint32_t carry = 0;
-  for (uint32_t b = 0; b < n && carry < k; b += kBlockThreads) {
-    const uint32_t r = b + threadIdx.x;
-    const uint32_t c = r < n ? recs[r].nfound : 0u;
-    uint32_t total;
-    const uint32_t ex = block_exscan_u32(s, c, total);
-    if (c != 0 && carry + ex < k) {
-      const uint32_t *st = stage + (uint64_t)r * stage_stride;
-      uint32_t pos = carry + ex;
-      for (uint32_t e = 0; e < c && pos < k; ++e, ++pos) {
-        const uint64_t gi = (uint64_t)r * span + st[e];
-        if constexpr (FINAL) out64[pos] = (int64_t)gi;
-        else out32[pos] = (uint32_t)gi;
+__device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__restrict__ recs,
+                                          uint32_t n, uint64_t span,
+                                          const uint32_t *__restrict__ stage,
+                                          uint64_t stage_stride, uint32_t k,
+                                          uint32_t *__restrict__ out32,
+                                          int64_t *__restrict__ out64) {
+  const uint32_t t = threadIdx.x;
+  if (t < (uint32_t)kRecCounts) s.cnt[t] = 0;
+  if (t == 0) {
+    s.sum_abs = s.sum_rel = 0.0;
+    s.max_abs = s.max_rel = -1.0;
+    s.amax_abs = s.amax_rel = UINT64_MAX;
+    s.eq_all = 0xffffffffu;
+    s.nf_total = 0;
+  }
+  for (uint32_t base = 0; base < n; base += kBlockThreads) {
+    const uint32_t m = min(n - base, (uint32_t)kBlockThreads);
+    __syncthreads();
+    if (t < m) {
+      const u32x4 *src = (const u32x4 *)(recs + base + t);
+      u32x4 v[sizeof(ChunkRec) / 16];
+#pragma unroll
+      for (int q = 0; q < (int)(sizeof(ChunkRec) / 16); ++q) v[q] = src[q];
+      u32x4 *dst = (u32x4 *)&s.rec[t];
+#pragma unroll
+      for (int q = 0; q < (int)(sizeof(ChunkRec) / 16); ++q) dst[q] = v[q];
+    }
+    __syncthreads();
+    // part reductions: part p covers records [32p, 32p + 32) of this pass
+    if (t < (uint32_t)(kParts * kRecCounts)) {
+      const uint32_t f = t % kRecCounts, p = t / kRecCounts;
+      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
+      uint64_t a = 0;
+      for (uint32_t r = lo; r < hi; ++r) a += ((const uint32_t *)&s.rec[r])[f];
+      s.part[p][f] = a;
+    } else if (t < (uint32_t)(kParts * kRecCounts + 2 * kParts)) {
+      const uint32_t u = t - kParts * kRecCounts, f = u & 1u, p = u >> 1;
+      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
+      double a = 0.0;
+      for (uint32_t r = lo; r < hi; ++r) a += f ? s.rec[r].sum_rel : s.rec[r].sum_abs;
+      s.dpart[f][p] = a;
+    } else if (t < (uint32_t)(kParts * kRecCounts + 4 * kParts)) {
+      const uint32_t u = t - kParts * kRecCounts - 2 * kParts, f = u & 1u, p = u >> 1;
+      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
+      double v = -1.0;
+      uint64_t ix = UINT64_MAX;
+      for (uint32_t r = lo; r < hi; ++r) {
+        const ChunkRec &x = s.rec[r];
+        const uint32_t a = f ? x.amax_rel : x.amax_abs;
+        if (a != kNone) max_merge(v, ix, f ? x.max_rel : x.max_abs, (uint64_t)(base + r) * span + a);
+      }
+      s.mv[f][p] = v;
+      s.mi[f][p] = ix;
+    } else if (t < (uint32_t)(kParts * kRecCounts + 5 * kParts)) {
+      const uint32_t p = t - kParts * kRecCounts - 4 * kParts;
+      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
+      uint32_t e = 0xffffffffu, c = 0;
+      for (uint32_t r = lo; r < hi; ++r) {
+        e &= s.rec[r].eq_bits;
+        c = sat_add(c, s.rec[r].nfound, k);
+      }
+      s.eqp[p] = e;
+      s.nfp[p] = c;
+    }
+    __syncthreads();
+    if (t < (uint32_t)kRecCounts) {
+      uint64_t a = s.cnt[t];
+      for (int p = 0; p < kParts; ++p) a += s.part[p][t];
+      s.cnt[t] = a;
+    } else if (t == 32 || t == 33) {
+      const uint32_t f = t - 32;
+      double a = f ? s.sum_rel : s.sum_abs;
+      for (int p = 0; p < kParts; ++p) a += s.dpart[f][p];
+      if (f) s.sum_rel = a;
+      else s.sum_abs = a;
+    } else if (t == 34 || t == 35) {
+      const uint32_t f = t - 34;
+      double v = f ? s.max_rel : s.max_abs;
+      uint64_t ix = f ? s.amax_rel : s.amax_abs;
+      for (int p = 0; p < kParts; ++p) max_merge(v, ix, s.mv[f][p], s.mi[f][p]);
+      if (f) {
+        s.max_rel = v;
+        s.amax_rel = ix;
+      } else {
+        s.max_abs = v;
+        s.amax_abs = ix;
+      }
+    } else if (t == 36) {
+      uint32_t e = s.eq_all;
+      for (int p = 0; p < kParts; ++p) e &= s.eqp[p];
+      s.eq_all = e;
+    } else if (t == 37) {
+      uint32_t c = s.nf_total;
+      for (int p = 0; p < kParts; ++p) {
+        s.nfpre[p] = c;
+        c = sat_add(c, s.nfp[p], k);
       }
     }
-    carry = min(carry + total, k);
+    __syncthreads();
+    if (k > 0) {
+      // first output position of each record: its part's prefix plus the
+      // entries of the records before it in the part
+      if (t < m) {
+        const uint32_t p = t / kPartLen;
+        uint32_t pos = s.nfpre[p];
+        for (uint32_t r = p * kPartLen; r < t; ++r) pos = sat_add(pos, s.rec[r].nfound, k);
+        s.nfstart[t] = pos;
+      }
+      __syncthreads();
+      // one output entry per thread: entry e belongs to the last record whose
+      // first position is <= e
+      const uint32_t lo = s.nf_total, hi = sat_add(s.nfpre[kParts - 1], s.nfp[kParts - 1], k);
+      for (uint32_t e = lo + t; e < hi; e += kBlockThreads) {
+        uint32_t a = 0, b = m - 1;
+        while (a < b) {
+          const uint32_t mid = (a + b + 1) / 2;
+          if (s.nfstart[mid] <= e) a = mid;
+          else b = mid - 1;
+        }
+        const uint64_t r = base + a;
+        const uint64_t gi = r * span + stage[r * stage_stride + (e - s.nfstart[a])];
+        if constexpr (FINAL) out64[e] = (int64_t)gi;
+        else out32[e] = (uint32_t)gi;
+      }
+      __syncthreads();
+    }
+    if (t == 37) s.nf_total = sat_add(s.nfpre[kParts - 1], s.nfp[kParts - 1], k);
   }
-  return carry;
+  __syncthreads();
 }
 
 // Output pointers and options of the completion path (copied field by field
@@ -431,14 +434,14 @@ struct FinArgs {
 __device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P, const DevCase &cs,
                               const ChunkRec *recs, uint32_t n, uint64_t span,
                               const uint32_t *stage, uint64_t stage_stride) {
-  merge_recs(s, recs, n, span);
   const bool ok = cs.status == 0;
   const uint32_t oi = cs.orig;
-  if (P.first_k != nullptr && P.k > 0) {
-    const uint32_t k = (uint32_t)P.k;
-    int64_t *const fk = P.first_k + (uint64_t)oi * k;
-    uint32_t nf = 0;
-    if (ok) nf = gather_firstk<true>(s, recs, n, span, stage, stage_stride, k, nullptr, fk);
+  const bool want_fk = P.first_k != nullptr && P.k > 0;
+  const uint32_t k = want_fk ? (uint32_t)P.k : 0u;
+  int64_t *const fk = want_fk ? P.first_k + (uint64_t)oi * k : nullptr;
+  merge_all<true>(s, recs, n, span, stage, stage_stride, ok ? k : 0u, nullptr, fk);
+  if (want_fk) {
+    const uint32_t nf = ok ? s.nf_total : 0u;
     for (uint32_t pos = nf + threadIdx.x; pos < k; pos += kBlockThreads) fk[pos] = -1;
   }
   if (threadIdx.x != 0) return;
@@ -512,25 +515,11 @@ __device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P,
     g.reserved = 0;
     if (P.integ != nullptr) P.integ[oi] = g;
   }
-  // suite counters; the last case of the call writes the rates
+  // suite counters (the rates kernel reads them after this launch)
   for (int p = 0; p < nt; ++p) {
     if (ok && cnt(p) == 0) {
       atomicAdd(&P.ctr->pass[p], 1u);
       if (flags == 0) atomicAdd(&P.ctr->cert[p], 1u);
-    }
-  }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  const uint32_t done = atomicAdd(&P.ctr->cases_done, 1u) + 1u;
-  if (done == (uint32_t)P.n_cases) {
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    const double nc = (double)P.n_cases;
-    for (int p = 0; p < nt; ++p) {
-      const uint32_t num = __hip_atomic_load(&P.ctr->pass[p], __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT);
-      const uint32_t cert = __hip_atomic_load(&P.ctr->cert[p], __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_AGENT);
-      if (P.match_rate != nullptr) P.match_rate[p] = (double)cert / nc;
-      if (P.numeric_rate != nullptr) P.numeric_rate[p] = (double)num / nc;
     }
   }
 }
@@ -569,9 +558,11 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
 
   struct StreamLds {
     uint32_t win[kTileWindow];    // block tile-count window
-    uint32_t merged[VC_MAX_K];    // first-k merge of the four waves
   };
   __shared__ StreamLds sh_st;
+  // dynamic LDS (launched with 5 * k words): each wave's ordered first-k
+  // list, then the merged list of the block
+  extern __shared__ uint32_t dyn_lds[];
   __shared__ ChunkRec s_out[kWavesPerBlock];
   // counters touched only by the exact tier, per wave (kept out of scalar
   // registers): nan_c, inf_c, nan_r, inf_r, n_fin, n_rel, n_rel_undef
@@ -678,8 +669,9 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     for (uint32_t e = threadIdx.x; e < win_len; e += kBlockThreads) sh_st.win[e] = 0;
   }
   __syncthreads();
-  uint32_t *const stage =
-      P.stage + ((uint64_t)chunk * kWavesPerBlock + wave) * (uint64_t)(kk > 0 ? kk : 0);
+  const uint32_t kq = kk > 0 ? (uint32_t)kk : 0u;
+  uint32_t *const lstage = dyn_lds + wave * kq;      // this wave's list
+  uint32_t *const lmerged = dyn_lds + kWavesPerBlock * kq;
 
   // Localization of the primary-pair mismatches given by per-lane bit mask
   // pb (bit j = element i0 + j): ordered first-k staging and tile counts.
@@ -698,7 +690,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       while (bits != 0) {
         const int j = __builtin_ctz(bits);
         bits &= bits - 1;
-        if (pos < (uint32_t)kk) stage[pos] = off0 + j;
+        if (pos < (uint32_t)kk) lstage[pos] = off0 + j;
         ++pos;
       }
       nfound = min(nfound + total, (uint32_t)kk);
@@ -883,14 +875,15 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
 
   // Tier 1 (binary32) for a full step; returns false (and changes nothing)
   // when some element is not finite, has r = 0, is outside the exactness
-  // bound, or (single pair) falls between the gate bounds.
+  // bound, or (single pair) falls between the gate bounds. One pass computes
+  // the sums, the running-maximum tests and whether any element fails a
+  // gate; the common step (valid, nothing failing, no new maximum) then
+  // commits with one uniform branch, and the counts of failing elements are
+  // taken in a second pass over the step only when some element failed.
   auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0)
                      __attribute__((always_inline)) -> bool {
     float sa0 = 0.f, sa1 = 0.f, sq0 = 0.f, sq1 = 0.f;
     float md = 0.f, me = -__builtin_inff(), mq = 0.f, mr = 0.f;
-    uint32_t fcnt[NT];
-#pragma unroll
-    for (int p = 0; p < NT; ++p) fcnt[p] = 0;
     uint64_t fany = 0;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
@@ -899,18 +892,11 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       const float d = __builtin_fabsf(c - r);
       const float a = __builtin_fabsf(r);
       if constexpr (NT == 1) {
-        const uint64_t f = ballot(d > __builtin_fmaf(a, rlo, alo));
-        fcnt[0] += popc(f);
-        fany |= f;
+        fany |= ballot(d > __builtin_fmaf(a, rlo, alo));
       } else {
         const double d64 = d, a64 = a;
 #pragma unroll
-        for (int p = 0; p < NT; ++p) {
-          const double t = atol[p] + rtol[p] * a64;
-          const uint64_t f = ballot(d64 > t);
-          fcnt[p] += popc(f);
-          if (p == prim) fany |= f;
-        }
+        for (int p = 0; p < NT; ++p) fany |= ballot(d64 > atol[p] + rtol[p] * a64);
       }
       const float ra = __builtin_amdgcn_rcpf(a);
       const float q = d * ra;
@@ -931,10 +917,23 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     const float sa = sa0 + sa1, sq = sq0 + sq1;
     bool ok = __builtin_isfinite(sa + sq) && mq <= QT;
     if constexpr (DT != VC_F16) ok = ok && mr <= 0x1p60f;
-    if (ballot(!ok) != 0) return false;
+    const uint64_t bad = ballot(!ok);
+    const uint64_t absm = ballot(md > thr_abs);
+    const uint64_t relm = ballot(me > 0.0f);
+    if ((bad | absm | relm | fany) == 0) {
+      ++fast_steps;
+      acc_abs += (double)sa;
+      acc_rel += (double)sq;
+      return true;
+    }
+    if (bad != 0) return false;
     uint32_t pb = 0;
     if (fany != 0) {
-      // primary-pair bits, and (single pair) the elements between the bounds
+      // exact counts, the primary pair's bits and (single pair) the elements
+      // between the bounds
+      uint32_t fcnt[NT];
+#pragma unroll
+      for (int p = 0; p < NT; ++p) fcnt[p] = 0;
       uint64_t amb = 0;
 #pragma unroll
       for (int j = 0; j < V; ++j) {
@@ -942,32 +941,30 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
         const float r = dec32<DT>(elem<DT>(rq, j));
         const float d = __builtin_fabsf(c - r);
         const float a = __builtin_fabsf(r);
-        bool f;
         if constexpr (NT == 1) {
-          f = d > __builtin_fmaf(a, rlo, alo);
+          const bool f = d > __builtin_fmaf(a, rlo, alo);
+          fcnt[0] += popc(ballot(f));
           amb |= ballot(f && !(d > __builtin_fmaf(a, rhi, ahi)));
+          pb |= (f ? 1u : 0u) << j;
         } else {
-          const double a64 = a;
-          double t = 0.0;
+          const double d64 = d, a64 = a;
 #pragma unroll
-          for (int p = 0; p < NT; ++p)
-            if (p == prim) t = atol[p] + rtol[p] * a64;
-          f = (double)d > t;
+          for (int p = 0; p < NT; ++p) {
+            const bool f = d64 > atol[p] + rtol[p] * a64;
+            fcnt[p] += popc(ballot(f));
+            if (p == prim) pb |= (f ? 1u : 0u) << j;
+          }
         }
-        pb |= (f ? 1u : 0u) << j;
       }
       if (amb != 0) return false;
-    }
 #pragma unroll
-    for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
+      for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
+    }
     ++fast_steps;
     acc_abs += (double)sa;
     acc_rel += (double)sq;
-    const uint32_t off0 = (uint32_t)(i0 - cstart);
-    const uint64_t absm = ballot(md > thr_abs);
-    const uint64_t relm = ballot(me > 0.0f);
-    if ((absm | relm) != 0) t1_update(cq, rq, absm, relm, off0);
-    if (fany != 0) localize(pb, i0);
+    if ((absm | relm) != 0) t1_update(cq, rq, absm, relm, (uint32_t)(i0 - cstart));
+    if (ballot(pb != 0) != 0) localize(pb, i0);
     return true;
   };
 
@@ -1068,8 +1065,19 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     }
   };
 
+  // Back-off of tier 1: after a step it cannot take, the wave skips it for
+  // 1, then 3, then 7 steps while the failures go on (data that is not tame
+  // tends to stay so); a step it takes resets the back-off.
+  uint32_t t1_hold = 0, t1_next = 0;
   auto step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0) __attribute__((always_inline)) {
-    bool done = t1ok && t1_step(cq, rq, i0);
+    const bool tried = t1ok && t1_hold == 0;
+    bool done = tried && t1_step(cq, rq, i0);
+    if (tried) {
+      t1_next = done ? 0u : min(2u * t1_next + 1u, 7u);
+      t1_hold = done ? 0u : t1_next;
+    } else if (t1_hold > 0) {
+      --t1_hold;
+    }
     if (!done) done = t2_step(cq, rq, i0);
     if (!done) exact_step(cq, rq, ALL, i0);
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, i0);
@@ -1094,18 +1102,21 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     auto off = [&](uint64_t st) __attribute__((always_inline)) {
       return (uint32_t)((wave + 4 * min(st, last)) * ITER * ES) + lane_b;
     };
+    auto ld = [&](const uint8_t *base, uint64_t st) __attribute__((always_inline)) {
+      return load16(base + off(st));
+    };
     u32x4 ca = {0, 0, 0, 0}, ra = ca, cn = ca, rn = ca;
     if (n_full > 0) {
-      ca = load16(cb + off(0));
-      ra = load16(rb + off(0));
+      ca = ld(cb, 0);
+      ra = ld(rb, 0);
     }
     for (uint64_t st = 0; st < n_full; st += 2) {
-      cn = load16(cb + off(st + 1));
-      rn = load16(rb + off(st + 1));
+      cn = ld(cb, st + 1);
+      rn = ld(rb, st + 1);
       step(ca, ra, step_i0(st));
       if (st + 1 >= n_full) break;
-      ca = load16(cb + off(st + 2));
-      ra = load16(rb + off(st + 2));
+      ca = ld(cb, st + 2);
+      ra = ld(rb, st + 2);
       step(cn, rn, step_i0(st + 1));
     }
   } else {
@@ -1176,7 +1187,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   // the k smallest: an entry's rank is its position in its own list plus the
   // number of smaller entries in the other three.
   uint32_t merged = 0;
-  const uint32_t *const stage0 = P.stage + (uint64_t)chunk * kWavesPerBlock * (uint64_t)(kk > 0 ? kk : 0);
+  const uint32_t *const stage0 = dyn_lds;
   if (kk > 0) {
     const uint32_t k = (uint32_t)kk;
     const uint32_t total =
@@ -1197,12 +1208,12 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
           }
           rank += lo;
         }
-        if (rank < k) sh_st.merged[rank] = x;
+        if (rank < k) lmerged[rank] = x;
       }
       merged = min(total, k);
       __syncthreads();
       for (uint32_t e = threadIdx.x; e < merged; e += kBlockThreads)
-        P.stage[(uint64_t)chunk * kWavesPerBlock * k + e] = sh_st.merged[e];
+        P.stage[(uint64_t)chunk * k + e] = lmerged[e];
     }
   }
   // the chunk record: counter word q by thread q, the rest by thread 32
@@ -1241,14 +1252,13 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
 
 // ------------------------------------------------------------ finalize
 
-// One block per chunk group (every group of the call, one launch after the
-// streaming kernels). A case with one group is written directly from its
-// chunk records; otherwise the group's chunk records are merged into a group
-// record and the last group of the case (completion counter) writes the
-// case from the group records.
+// First finalize launch, one block per chunk group of the call: a case with
+// one group is written directly from its chunk records; the group of a
+// larger case is merged into a group record (the second launch, one block
+// per such case, merges those). Kernel boundaries order the records, so no
+// device-wide fences are needed.
 __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P) {
   __shared__ MergeScratch M;
-  __shared__ uint32_t s_flag;
   const uint64_t g = blockIdx.x;
   const VCK_CONST DevCase *table = (const VCK_CONST DevCase *)P.cases;
   uint64_t ci = 0;
@@ -1275,7 +1285,7 @@ __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P)
   F.do_integ = P.do_integ;
   const uint64_t CH = 4ull * cs.unit_elems;
   const uint32_t k = P.k > 0 ? (uint32_t)P.k : 0u;
-  const uint64_t cstride = (uint64_t)kWavesPerBlock * k;
+  const uint64_t cstride = k;
   if (cs.n_groups == 1) {
     finalize_case(M, F, cs, P.recs + cs.chunk_begin, cs.n_chunks, CH,
                   P.stage + cs.chunk_begin * cstride, cstride);
@@ -1285,11 +1295,9 @@ __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P)
   const uint32_t gc0 = g_local * kGroupChunks;
   const uint32_t gchunks = min((uint32_t)kGroupChunks, cs.n_chunks - gc0);
   const ChunkRec *const grp = P.recs + cs.chunk_begin + gc0;
-  merge_recs(M, grp, gchunks, CH);
-  uint32_t gnf = 0;
-  if (k > 0)
-    gnf = gather_firstk<false>(M, grp, gchunks, CH, P.stage + (cs.chunk_begin + gc0) * cstride,
-                               cstride, k, P.gstage + g * k, nullptr);
+  merge_all<false>(M, grp, gchunks, CH, P.stage + (cs.chunk_begin + gc0) * cstride, cstride, k,
+                   P.gstage + g * k, nullptr);
+  const uint32_t gnf = M.nf_total;
   {
     ChunkRec *const gr = P.grecs + g;
     const uint32_t q = threadIdx.x;
@@ -1307,9 +1315,46 @@ __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P)
       gr->sum_rel = M.sum_rel;
     }
   }
-  if (!arrive_last(&P.case_cnt[ci], cs.n_groups - 1u, s_flag)) return;
+}
+
+// Second finalize launch: block i writes the results of multi-group case
+// P.multi[i] (or of the single case) from its group records.
+__global__ __launch_bounds__(kBlockThreads) void finalize_multi_kernel(const Params P) {
+  __shared__ MergeScratch M;
+  DevCase cs;
+  if (P.cases != nullptr)
+    cs = load_case((const VCK_CONST DevCase *)P.cases +
+                   ((const VCK_GLOBAL uint32_t *)P.multi)[blockIdx.x]);
+  else
+    cs = P.single;
+  FinArgs F;
+  F.stats = P.stats;
+  F.mismatches = P.mismatches;
+  F.pass_out = P.pass_out;
+  F.first_k = P.first_k;
+  F.integ = P.integ;
+  F.match_rate = P.match_rate;
+  F.numeric_rate = P.numeric_rate;
+  F.ctr = P.ctr;
+  F.n_cases = P.n_cases;
+  F.n_tols = P.n_tols;
+  F.primary = P.primary;
+  F.k = P.k;
+  F.do_integ = P.do_integ;
+  const uint64_t CH = 4ull * cs.unit_elems;
+  const uint32_t k = P.k > 0 ? (uint32_t)P.k : 0u;
   finalize_case(M, F, cs, P.grecs + cs.group_begin, cs.n_groups, CH * kGroupChunks,
                 P.gstage + cs.group_begin * k, k);
+}
+
+// Suite match rates from the pass counters of the finalize launches.
+__global__ void rates_kernel(const Params P) {
+  const int p = threadIdx.x;
+  if (p >= P.n_tols) return;
+  const double nc = (double)P.n_cases;
+  const uint32_t num = P.ctr->pass[p], cert = P.ctr->cert[p];
+  if (P.match_rate != nullptr) P.match_rate[p] = P.n_cases > 0 ? (double)cert / nc : 0.0;
+  if (P.numeric_rate != nullptr) P.numeric_rate[p] = P.n_cases > 0 ? (double)num / nc : 0.0;
 }
 
 // Copies the descriptor blob from pinned host memory, clears the counter
@@ -1332,8 +1377,9 @@ __global__ __launch_bounds__(256) void prologue_kernel(const Prologue Q) {
 
 template <int DT, int NT, bool INTEG>
 hipError_t launch_main_t(const Params &p, uint64_t n_chunks, hipStream_t s) {
+  const size_t lds = (size_t)(kWavesPerBlock + 1) * (size_t)(p.k > 0 ? p.k : 0) * sizeof(uint32_t);
   hipLaunchKernelGGL((main_kernel<DT, NT, INTEG>), dim3((uint32_t)n_chunks), dim3(kBlockThreads),
-                     0, s, p);
+                     lds, s, p);
   return hipGetLastError();
 }
 
@@ -1367,10 +1413,24 @@ hipError_t launch_prologue(const Prologue &p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_finalize(const Params &p, uint64_t n_groups, hipStream_t s) {
-  if (n_groups == 0) return hipSuccess;
-  hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)n_groups), dim3(kBlockThreads), 0, s, p);
-  return hipGetLastError();
+hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi, bool rates,
+                           hipStream_t s) {
+  if (n_groups > 0) {
+    hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)n_groups), dim3(kBlockThreads), 0, s, p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (n_multi > 0) {
+    hipLaunchKernelGGL(finalize_multi_kernel, dim3((uint32_t)n_multi), dim3(kBlockThreads), 0, s,
+                       p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (rates && n_groups > 0) {
+    hipLaunchKernelGGL(rates_kernel, dim3(1), dim3(64), 0, s, p);
+    return hipGetLastError();
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint64_t n_chunks,
