@@ -176,6 +176,9 @@ def main():
     ap.add_argument("--headline-only", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run 5 device-to-device copies of 1 GiB (a plain copy of known "
+                         "size, to scale the HBM byte counters of a profiler run)")
     ap.add_argument("--only", type=int, default=0,
                     help="measure only this workload (1-5) and report it as the headline; "
                          "for profiling single workloads")
@@ -189,6 +192,14 @@ def main():
     import torch
 
     torch.cuda.init()
+    if args.copy_probe:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy probe: 5 copies of %d bytes" % src.numel())
+        return
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     results = {}
     first = args.only or HEADLINE
