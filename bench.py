@@ -39,9 +39,18 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def kernel_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def kernel_hash(text=None):
+    """Hash of the kernel source with // comments and blank lines removed, so
+    that the stored counter readings stay valid across comment-only edits."""
+    if text is None:
+        with open(KERNEL_SRC) as f:
+            text = f.read()
+    code = []
+    for line in text.splitlines():
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            code.append(line)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
 def algorithmic_bytes(w, classes=None):
@@ -110,6 +119,11 @@ def measure(cfg, steps, warmup, flush):
     alg = algorithmic_bytes(w, w.meta.get("classes"))
     out = {
         "workload": w.name,
+        "storage": {torch.float32: "fp32", torch.float16: "fp16",
+                    torch.bfloat16: "bf16"}[w.cases[0].ref.dtype],
+        "tols": [[float(a), float(r)] for (a, r, *_) in w.tols],
+        "tile": list(w.tile) if w.tile else None,
+        "k": w.k or 0,
         "n_cases": len(w.cases),
         "elements": w.numel,
         "ref_cand_bytes": rc,
@@ -230,13 +244,15 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": head["workload"], "storage": "fp16", "n_cases": head["n_cases"],
-                   "tols": [[1e-3, 1e-3]], "tile": [64, 64], "k": 64,
+        "config": {"workload": head["workload"], "storage": head["storage"],
+                   "n_cases": head["n_cases"], "tols": head["tols"], "tile": head["tile"],
+                   "k": head["k"],
                    "pct_hbm_peak": head["pct_hbm_peak"], "cases_per_s": head["cases_per_s"],
                    "ref_cand_bytes": head["ref_cand_bytes"], "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "main_kernel (fp16, 1 tolerance pair)",
+                     "kernel": "main_kernel (%s, %d tolerance pair%s)" % (
+                         head["storage"], len(head["tols"]), "" if len(head["tols"]) == 1 else "s"),
                      "alg_bytes_per_launch": head["main_kernel_alg_bytes"],
                      "avg_launch_ms": head["main_kernel_ms"]},
         "cpu_baseline": cpu,

@@ -6,17 +6,19 @@
 // full-coverage evidence): the tolerance gate for up to 8 pairs, NaN/Inf
 // counts, exact max/argmax of |c-r| and |c-r|/|r|, binary64 error sums, the
 // per-tile mismatch map, the ordered first-k mismatch indices and the
-// degenerate-output detector counts. The same launch also reduces the per-
-// chunk results: the last block to finish a group of chunks merges the
-// group, the last group of a case writes the case's results, and the last
-// case writes the suite match rates (completion counters, fixed merge order).
+// degenerate-output detector counts. Each block of the main kernel writes
+// one chunk record; separate launches then merge the records in a fixed
+// order: a finalize kernel per group of up to 256 chunks (writing the case's
+// results directly when the case has one group), a second one for cases with
+// several groups, and a rates kernel for the suite match rates. Kernel
+// boundaries order the launches, so no device-scope fences or completion
+// counters are needed.
 //
 // Work decomposition: a case is cut into chunks of 4 * U elements; one block
 // (4 waves) owns one chunk and streams it front to back: a step is 64 lanes x
 // 16 bytes (one fully coalesced 1 KiB non-temporal load per tensor) and the
 // four waves take steps round robin, so the block's loads always target one
-// contiguous stretch of memory. The loop is unrolled twice so the next
-// step's loads are in flight while the current step is evaluated.
+// contiguous stretch of memory. Loads run two steps ahead of the evaluation.
 //
 // Exactness. The definition is binary64 on exactly decoded values. Each step
 // is evaluated by the cheapest of three tiers that is exact for it:
