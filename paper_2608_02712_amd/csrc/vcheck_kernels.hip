@@ -1095,8 +1095,10 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   };
   if (vec) {
     // Two steps per trip with the next step's loads in flight. The loads are
-    // unconditional (past the end they re-read the last step, a cache hit) so
-    // the wait counters stay exact across the loop.
+    // unconditional (past the end they re-read the last step, a cache hit) and
+    // the trip has no exit between its two steps, so on every path into the
+    // loop head the only loads in flight are the next trip's first step: the
+    // wait counters stay exact and the loads overlap the evaluation.
     const uint8_t *const cb = cand + cstart * ES;  // block-uniform bases
     const uint8_t *const rb = ref + cstart * ES;
     const uint32_t lane_b = lane * 16u;
@@ -1112,15 +1114,17 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       ca = ld(cb, 0);
       ra = ld(rb, 0);
     }
-    for (uint64_t st = 0; st < n_full; st += 2) {
+    const uint64_t n_pairs = n_full / 2;
+    for (uint64_t pr = 0; pr < n_pairs; ++pr) {
+      const uint64_t st = 2 * pr;
       cn = ld(cb, st + 1);
       rn = ld(rb, st + 1);
       step(ca, ra, step_i0(st));
-      if (st + 1 >= n_full) break;
       ca = ld(cb, st + 2);
       ra = ld(rb, st + 2);
       step(cn, rn, step_i0(st + 1));
     }
+    if (n_full & 1) step(ca, ra, step_i0(n_full - 1));
   } else {
     for (uint64_t st = 0; st < n_full; ++st) {
       const uint64_t i0 = step_i0(st);
