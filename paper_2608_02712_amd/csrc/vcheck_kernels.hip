@@ -711,6 +711,12 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     }
   };
 
+  // Whether mismatch positions are still recorded: tile maps requested, or
+  // the wave's first-k list not yet full (uniform).
+  auto loc_on = [&]() __attribute__((always_inline)) {
+    return do_tiles || nfound < kq;
+  };
+
   // Raise the wave thresholds to the lanes' bests (after an update).
   auto raise_abs = [&](uint64_t lanes) __attribute__((always_inline)) {
     const double v = popc(lanes) == 1 ? readlane_f64(lb_abs, (uint32_t)__builtin_ctzll(lanes))
@@ -872,7 +878,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       hfc += nan_c_step;
       hfr += nan_r_step;
     }
-    if (ballot(pb != 0) != 0) localize(pb, i0);
+    if (loc_on() && ballot(pb != 0) != 0) localize(pb, i0);
   };
 
   // Tier 1 (binary32) for a full step; returns false (and changes nothing)
@@ -966,7 +972,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     acc_abs += (double)sa;
     acc_rel += (double)sq;
     if ((absm | relm) != 0) t1_update(cq, rq, absm, relm, (uint32_t)(i0 - cstart));
-    if (ballot(pb != 0) != 0) localize(pb, i0);
+    if (loc_on() && ballot(pb != 0) != 0) localize(pb, i0);
     return true;
   };
 
@@ -1006,7 +1012,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     const uint32_t off0 = (uint32_t)(i0 - cstart);
     if (absm != 0) abs_update(cq, rq, absm, off0);
     if (relm != 0) rel_update(cq, rq, relm, off0);
-    if (pany != 0) {
+    if (pany != 0 && loc_on()) {
       uint32_t pb = 0;
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
@@ -1023,26 +1029,95 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     return true;
   };
 
-  // Degenerate-output detector counts of one step (bitwise; NaN handling of
-  // the binary16 test is added by the exact tier).
+  // Degenerate-output detector counts of one side (cand or ref) of a step
+  // (bitwise; NaN handling of the binary16 test is added by the exact tier).
+  // Every predicate counted here implies that the element's low 13 bits are
+  // zero (zero, bfloat16- and binary16-representable values) or that it
+  // equals the case's first element bit for bit, so one cheap per-lane
+  // summary rules out the usual step. A predicate that holds for every
+  // element of the step, or for none, is counted from lane summaries; only a
+  // mixed step counts element by element.
+  auto integ_side = [&](const u32x4 &xq, uint32_t first, uint32_t &n_zero, uint32_t &n_first,
+                        uint32_t &n_bf, uint32_t &n_hf, uint32_t vmask, bool full)
+                        __attribute__((always_inline)) {
+    constexpr uint32_t kStep = kWaveSize * V;
+    // count of valid elements with pred, given lane summaries all_p / any_p
+    auto count = [&](bool all_p, bool any_p, auto pred) __attribute__((always_inline)) {
+      if (full && ballot(!all_p) == 0) return kStep;
+      if (ballot(any_p) == 0) return 0u;
+      uint32_t n = 0;
+#pragma unroll
+      for (int j = 0; j < V; ++j) n += popc(ballot(((vmask >> j) & 1u) && pred(elem<DT>(xq, j))));
+      return n;
+    };
+    if constexpr (DT == VC_F32) {
+      uint32_t pre = 0xffffffffu;
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const uint32_t x = elem<DT>(xq, j);
+        pre = min(pre, ((vmask >> j) & 1u) ? min(x & 0x1fffu, x ^ first) : ~0u);
+      }
+      if (ballot(pre == 0) == 0) return;
+      uint32_t o = 0, of = 0, mz = ~0u, mf = ~0u, mb = ~0u, m13 = ~0u, amax = 0, mn = ~0u;
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const uint32_t x = elem<DT>(xq, j), ax = x & 0x7fffffffu, xf = x ^ first;
+        if ((vmask >> j) & 1u) {
+          o |= x;
+          of |= xf;
+          mf = min(mf, xf);
+          mz = min(mz, ax);
+          mb = min(mb, x & 0xffffu);
+          m13 = min(m13, x & 0x1fffu);
+          amax = max(amax, ax);
+          mn = min(mn, ax - 1u);
+        }
+      }
+      n_zero += count((o & 0x7fffffffu) == 0, mz == 0,
+                      [](uint32_t x) { return (x & 0x7fffffffu) == 0; });
+      n_first += count(of == 0, mf == 0, [&](uint32_t x) { return x == first; });
+      n_bf += count((o & 0xffffu) == 0, mb == 0, [](uint32_t x) { return (x & 0xffffu) == 0; });
+      // binary16-representable: 0, or |x| in [2^-14, 65504] with the low 13
+      // bits zero (the lane-wide test); subnormal binary16 values, infinities
+      // and anything else are left to the element test
+      n_hf += count((o & 0x1fffu) == 0 && amax <= 0x477fe000u && mn >= 0x387fffffu, m13 == 0,
+                    [](uint32_t x) {
+                      const float f = __uint_as_float(x);
+                      return (float)(_Float16)f == f;
+                    });
+    } else {
+      // two elements per word: a zero half word is detected by the borrow of
+      // (v - 0x00010001) into a bit that is clear in v (a conservative test)
+      const uint32_t ff = first | (first << 16);
+      uint32_t hit = 0, o = 0, of = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t wm = (vmask >> (2 * w)) & 3u;
+        const uint32_t keep = (wm & 1u ? 0x0000ffffu : 0u) | (wm & 2u ? 0xffff0000u : 0u);
+        const uint32_t z = (xq[w] & 0x7fff7fffu) | ~keep, e = (xq[w] ^ ff) | ~keep;
+        hit |= ((z - 0x00010001u) & ~z & 0x80008000u) | ((e - 0x00010001u) & ~e & 0x80008000u);
+        o |= xq[w] & keep;
+        of |= (xq[w] ^ ff) & keep;
+      }
+      if (ballot(hit != 0) == 0) return;
+      n_zero += count((o & 0x7fff7fffu) == 0, true,
+                      [](uint32_t x) { return (x & 0x7fffu) == 0; });
+      n_first += count(of == 0, true, [&](uint32_t x) { return x == first; });
+    }
+  };
+
+  // Detector counts and bit-equality evidence of one step.
   auto integ_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, bool full,
                         uint64_t i0) __attribute__((always_inline)) {
+    integ_side(cq, first_c, zc, efc, bfc, hfc, vmask, full);
+    integ_side(rq, first_r, zr, efr, bfr, hfr, vmask, full);
+    // cand bit-equal to ref: tested only while no difference has been seen
+    if (diff_cr == 0) {
+      uint32_t dx = 0;
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      const bool valid = (vmask >> j) & 1u;
-      const uint32_t c = elem<DT>(cq, j), r = elem<DT>(rq, j);
-      const float cf = dec32<DT>(c), rf = dec32<DT>(r);
-      zc += popc(ballot(valid && cf == 0.0f));
-      zr += popc(ballot(valid && rf == 0.0f));
-      efc += popc(ballot(valid && c == first_c));
-      efr += popc(ballot(valid && r == first_r));
-      if constexpr (DT == VC_F32) {
-        bfc += popc(ballot(valid && (c & 0xffffu) == 0));
-        bfr += popc(ballot(valid && (r & 0xffffu) == 0));
-        hfc += popc(ballot(valid && (float)(_Float16)cf == cf));
-        hfr += popc(ballot(valid && (float)(_Float16)rf == rf));
-      }
-      diff_cr |= ballot(valid && c != r);
+      for (int j = 0; j < V; ++j)
+        dx |= ((vmask >> j) & 1u) ? (elem<DT>(cq, j) ^ elem<DT>(rq, j)) : 0u;
+      diff_cr = ballot(dx != 0);
     }
     // operator inputs: read only while cand or ref is still bit-equal
     uint32_t need = eqc | eqr;
