@@ -246,6 +246,7 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
     }
     d.vec_ok = vec ? 1u : 0u;
     if (want_tiles && n > 0) d.tiles_c = (d.cols + opts.tile_w - 1) / opts.tile_w;
+    if (d.cols < (1ull << 31)) d.cols_div = vck::div_magic((uint32_t)d.cols);
   }
   // tile-map offsets follow the caller's case order
   if (want_tiles) {
@@ -299,7 +300,7 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
   const size_t nc = (size_t)n_cases;
   size_t off = 0;
   plan.off_table = off;
-  plan.off_cc = off + sizeof(vck::DevCase) * nc;  // 160 * n: 16-byte aligned
+  plan.off_cc = off + sizeof(vck::DevCase) * nc;  // 176 * n: 16-byte aligned
   plan.off_cg = plan.off_cc + sizeof(uint64_t) * nc;
   plan.off_multi = plan.off_cg + sizeof(uint64_t) * nc;
   plan.blob_bytes =
@@ -428,6 +429,8 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
   P.primary = plan.primary;
   P.tile_h = plan.tile_h;
   P.tile_w = plan.tile_w;
+  P.th_div = vck::div_magic((uint32_t)plan.tile_h);
+  P.tw_div = vck::div_magic((uint32_t)plan.tile_w);
   P.k = plan.k;
   P.do_tiles = plan.do_tiles ? 1 : 0;
   P.do_integ = plan.do_integ ? 1 : 0;

@@ -15,6 +15,28 @@ constexpr int kBlockThreads = kWaveSize * kWavesPerBlock;
 constexpr int kTileWindow = 2048;  // LDS tile counters per block
 constexpr int kGroupChunks = 256;  // chunks merged by one group record
 
+// Unsigned division of a 32-bit numerator by an invariant divisor d
+// (1 <= d < 2^32) as a multiply-high, an add and two shifts (Granlund and
+// Montgomery, Division by invariant integers using multiplication, PLDI 1994,
+// Sec. 4, Fig. 4.1): with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
+// t = mulhi(m, n) and n / d = (t + ((n - t) >> min(l, 1))) >> max(l - 1, 0).
+struct DivMagic {
+  uint32_t m;
+  uint32_t shifts;  // min(l, 1) | max(l - 1, 0) << 8
+};
+inline DivMagic div_magic(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  DivMagic r;
+  r.m = (uint32_t)((((1ull << 32) * ((1ull << l) - d)) / d) + 1);
+  r.shifts = (l < 1 ? l : 1u) | ((l > 1 ? l - 1 : 0u) << 8);
+  return r;
+}
+__device__ __forceinline__ uint32_t div_by(uint32_t n, uint32_t m, uint32_t shifts) {
+  const uint32_t t = __umulhi(m, n);
+  return (t + ((n - t) >> (shifts & 0xffu))) >> (shifts >> 8);
+}
+
 // Device-side case descriptor. The host builds one per case, in launch
 // order (grouped by dtype), and the prologue kernel copies the table into
 // the workspace. Every case owns at least one chunk: a case that is not
@@ -38,8 +60,10 @@ struct DevCase {
   uint32_t orig;         // index of the case in the caller's arrays
   uint32_t dtype;
   uint32_t unit_elems;   // elements per wave range; a chunk is 4 of them
+  DivMagic cols_div;     // division by cols (when cols < 2^31)
+  uint32_t pad[2];
 };
-static_assert(sizeof(DevCase) == 160, "DevCase layout");
+static_assert(sizeof(DevCase) == 176, "DevCase layout");
 
 // Partial result of one chunk (one block of the main kernel; its four waves
 // interleave over the chunk), or of one group of up to kGroupChunks chunks.
@@ -84,6 +108,7 @@ struct Params {
   int32_t n_tols;              // 1 .. 8 (the kernel evaluates NT >= n_tols pairs)
   int32_t primary;
   int32_t tile_h, tile_w;
+  DivMagic th_div, tw_div;     // division by tile_h, tile_w
   int32_t k;                   // first-k length (0: none)
   int32_t do_tiles;            // 1: tile maps requested
   int32_t do_integ;

@@ -31,9 +31,11 @@
 //     fma(|r|, rlo, alo) <= atol + rtol |r| <= fma(|r|, rhi, ahi) (the host
 //     shrinks / grows the pair by 2^-20 and only enables this when the
 //     thresholds stay in the normal binary32 range); an element between the
-//     bounds sends the step to tier 2. Running-maximum tests are exact
-//     binary32 comparisons against thresholds rounded down to binary32, and
-//     fma(-M, |r|, d) > 0 (exact sign) for the quotient.
+//     bounds sends the step to tier 2. The running-maximum test of |c - r| is
+//     an exact binary32 comparison against the threshold rounded down to
+//     binary32; the quotient's test compares the binary32 estimate with the
+//     threshold lowered by 2^-20 (more than the estimate's error), so it
+//     never misses a larger quotient, and the update decides exactly.
 //  2. binary64 tier: the same evaluation in binary64 for steps with finite
 //     values and non-zero references.
 //  3. exact tier: element by element with the class tests (NaN, Inf, r = 0,
@@ -72,6 +74,16 @@ struct Tr<VC_BF16> {
 };
 
 constexpr uint32_t kNone = 0xffffffffu;
+constexpr int kDeferCap = 16;  // deferred steps listed per wave before they are evaluated
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt in
+// 6:4, lgkmcnt in 11:8): wait until at most 2 (or 0) vector memory
+// operations are outstanding, other counters unconstrained
+constexpr int kWaitVm2 = 0x0f72;
+constexpr int kWaitVm0 = 0x0f70;
+// outcome of a fast tier for one step
+constexpr int kDone = 0;      // evaluated and committed
+constexpr int kDefer = 1;     // to the exact tier, after streaming
+constexpr int kNotTaken = 2;  // not this tier (nothing changed)
 
 // 16 bytes of raw storage held by one lane.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -152,21 +164,42 @@ __device__ __forceinline__ u32x4 load_guarded(const uint8_t *base, uint64_t idx0
   return r;
 }
 
-// Row of element i in the (R, C) view, and the tile of element i. `narrow`
-// (every index of the case below 2^32) selects 32-bit divisions, which are
-// several times cheaper than 64-bit ones.
-__device__ __forceinline__ uint64_t row_of(uint64_t i, uint64_t cols, bool narrow) {
-  return narrow ? (uint64_t)((uint32_t)i / (uint32_t)cols) : i / cols;
-}
-__device__ __forceinline__ uint64_t tile_of(uint64_t i, uint64_t cols, uint32_t th, uint32_t tw,
-                                            uint64_t tiles_c, bool narrow) {
-  if (narrow) {
-    const uint32_t ii = (uint32_t)i, cc = (uint32_t)cols;
-    const uint32_t row = ii / cc, col = ii - row * cc;
-    return (uint64_t)(row / th) * tiles_c + col / tw;
+// Tile geometry of one chunk, for the localization path. The chunk's first
+// element is at row row0 = trow0 * tile_h + rrem0 and column col0 of the
+// (rows, cols) view.
+struct ChunkTiles {
+  uint64_t tiles_c;    // tiles per tile row
+  uint64_t trow0;      // tile row of row0
+  uint64_t tcol0;      // col0 / tile_w (rows of 2^31 or more elements)
+  uint64_t room;       // cols - col0: elements from the chunk start to the row end
+  uint64_t tile_off;   // offset of the case's map in the tile-map output
+  uint64_t win_base;   // first tile of the block's LDS window
+  uint32_t *tile_maps;
+  uint32_t col0;       // (rows shorter than 2^31 elements)
+  uint32_t cols32;
+  uint32_t rrem0;
+  uint32_t crem0;      // col0 % tile_w (rows of 2^31 or more elements)
+  DivMagic cdiv, hdiv, wdiv;
+  uint32_t win_len, kq, do_tiles, wide;
+};
+
+// Tile (row-major index within the case's map) of the element at chunk
+// offset o, with 32-bit divisions by the invariant divisors only (a chunk
+// holds fewer than 2^18 elements).
+__device__ __forceinline__ uint64_t tile_at(const ChunkTiles &g, uint32_t o) {
+  uint32_t dr;  // rows past row0
+  uint64_t tc;  // tile column
+  if (!g.wide) {
+    const uint32_t x = g.col0 + o;
+    dr = div_by(x, g.cdiv.m, g.cdiv.shifts);
+    tc = div_by(x - dr * g.cols32, g.wdiv.m, g.wdiv.shifts);
+  } else {
+    // rows of 2^31 elements or more: the chunk spans at most two rows
+    dr = (uint64_t)o >= g.room ? 1u : 0u;
+    tc = dr ? (uint64_t)div_by(o - (uint32_t)g.room, g.wdiv.m, g.wdiv.shifts)
+            : g.tcol0 + div_by(g.crem0 + o, g.wdiv.m, g.wdiv.shifts);
   }
-  const uint64_t row = i / cols, col = i - row * cols;
-  return (row / th) * tiles_c + col / tw;
+  return (g.trow0 + div_by(g.rrem0 + dr, g.hdiv.m, g.hdiv.shifts)) * g.tiles_c + tc;
 }
 
 // Member-wise copy of a case descriptor read through the constant address
@@ -191,6 +224,8 @@ __device__ __forceinline__ DevCase load_case(const VCK_CONST DevCase *t) {
   d.orig = t->orig;
   d.dtype = t->dtype;
   d.unit_elems = t->unit_elems;
+  d.cols_div.m = t->cols_div.m;
+  d.cols_div.shifts = t->cols_div.shifts;
   return d;
 }
 
@@ -239,6 +274,25 @@ __device__ __forceinline__ double wave_max_val(double v) {
 
 // Largest binary32 value <= x, for x = -1 or x >= 0 (the running-maximum
 // thresholds); values above the binary32 range give FLT_MAX.
+// c - r of element j of a step in binary32 (one rounding); binary16 pairs go
+// through the mixed-precision FMA, which converts both operands exactly.
+template <int DT>
+__device__ __forceinline__ float diff32(const u32x4 &cq, const u32x4 &rq, int j) {
+  if constexpr (DT == VC_F16) {
+    const int w = j >> 1;
+    const uint32_t cw = w == 0 ? cq[0] : w == 1 ? cq[1] : w == 2 ? cq[2] : cq[3];
+    const uint32_t rw = w == 0 ? rq[0] : w == 1 ? rq[1] : w == 2 ? rq[2] : rq[3];
+    float d;
+    if (j & 1)
+      asm("v_fma_mix_f32 %0, %1, 1.0, -%2 op_sel:[1,0,1] op_sel_hi:[1,0,1]" : "=v"(d) : "v"(cw), "v"(rw));
+    else
+      asm("v_fma_mix_f32 %0, %1, 1.0, -%2 op_sel_hi:[1,0,1]" : "=v"(d) : "v"(cw), "v"(rw));
+    return d;
+  } else {
+    return dec32<DT>(elem<DT>(cq, j)) - dec32<DT>(elem<DT>(rq, j));
+  }
+}
+
 __device__ __forceinline__ float f32_down(double x) {
   if (x < 0.0) return -1.0f;
   float f = (float)x;
@@ -562,6 +616,11 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     uint32_t win[kTileWindow];    // block tile-count window
   };
   __shared__ StreamLds sh_st;
+  // localization parameters, read from LDS by the (rare) localization path
+  // so that they do not occupy registers across the streaming loop
+  __shared__ ChunkTiles sh_loc;
+  // each wave's list of deferred steps (chunk offsets of the steps)
+  __shared__ uint32_t s_defer[kWavesPerBlock][kDeferCap];
   // dynamic LDS (launched with 5 * k words): each wave's ordered first-k
   // list, then the merged list of the block
   extern __shared__ uint32_t dyn_lds[];
@@ -626,6 +685,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   // their binary32 images rounded down
   double T_abs = -1.0, T_rel = -1.0;
   float thr_abs = -1.0f, b_rel = -1.0f;
+  bool rel_zero = false;  // the wave's best quotient is 0: any d > 0 beats it
   // wave-uniform counters
   uint32_t mism[NT];
 #pragma unroll
@@ -650,36 +710,62 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   }
 
   // Tile window: LDS counters for the tile-id range this chunk can touch.
-  const uint32_t th = (uint32_t)P.tile_h, tw = (uint32_t)P.tile_w;
-  bool win_ok = false;
-  uint64_t win_base = 0;
-  uint32_t win_len = 0;
-  const bool narrow = numel <= 0xffffffffull;
-  if (do_tiles && cend > cstart) {
-    const uint64_t row_lo = row_of(cstart, cols, narrow), row_hi = row_of(cend - 1, cols, narrow);
-    uint64_t t_min, t_max;
-    if (row_lo == row_hi) {
-      t_min = tile_of(cstart, cols, th, tw, tiles_c, narrow);
-      t_max = tile_of(cend - 1, cols, th, tw, tiles_c, narrow);
-    } else {
-      t_min = (row_lo / th) * tiles_c;
-      t_max = (row_hi / th) * tiles_c + tiles_c - 1;
+  const uint32_t kq = kk > 0 ? (uint32_t)kk : 0u;
+  if (threadIdx.x == 0) {
+    ChunkTiles g = {};
+    g.tile_maps = tile_maps;
+    g.kq = kq;
+    g.do_tiles = do_tiles ? 1u : 0u;
+    if (do_tiles && cend > cstart) {
+      const uint64_t th = (uint64_t)P.tile_h, tw = (uint64_t)P.tile_w;
+      const uint64_t row0 = cstart / cols, col0 = cstart - row0 * cols;
+      g.tiles_c = tiles_c;
+      g.trow0 = row0 / th;
+      g.rrem0 = (uint32_t)(row0 - g.trow0 * th);
+      g.wide = cols >= (1ull << 31) ? 1u : 0u;
+      g.col0 = (uint32_t)col0;
+      g.cols32 = (uint32_t)cols;
+      g.room = cols - col0;
+      g.tcol0 = col0 / tw;
+      g.crem0 = (uint32_t)(col0 - g.tcol0 * tw);
+      g.cdiv = dcs.cols_div;
+      g.hdiv = P.th_div;
+      g.wdiv = P.tw_div;
+      g.tile_off = tile_off;
+      // tiles of the first and last element; a chunk spanning several rows
+      // also covers the start (end) of its first (last) tile row when that
+      // tile row holds another of its rows
+      const uint32_t last = (uint32_t)(cend - cstart - 1);
+      const uint64_t t_first = tile_at(g, 0), t_last = tile_at(g, last);
+      const uint32_t dr_last =
+          g.wide ? ((uint64_t)last >= g.room ? 1u : 0u) : div_by(g.col0 + last, g.cdiv.m, g.cdiv.shifts);
+      const uint64_t rr_last = (uint64_t)g.rrem0 + dr_last;
+      const uint64_t tr_last = g.trow0 + rr_last / th;
+      const bool multi = dr_last > 0;
+      const uint64_t t_min = (multi && g.rrem0 + 1 < th) ? g.trow0 * tiles_c : t_first;
+      const uint64_t t_max = (multi && rr_last % th != 0) ? tr_last * tiles_c + tiles_c - 1 : t_last;
+      if (t_max - t_min < (uint64_t)kTileWindow) {
+        g.win_base = t_min;
+        g.win_len = (uint32_t)(t_max - t_min + 1);
+      }
     }
-    win_ok = (t_max - t_min) < (uint64_t)kTileWindow;
-    win_base = t_min;
-    win_len = win_ok ? (uint32_t)(t_max - t_min + 1) : 0u;
-    for (uint32_t e = threadIdx.x; e < win_len; e += kBlockThreads) sh_st.win[e] = 0;
+    sh_loc = g;
   }
   __syncthreads();
-  const uint32_t kq = kk > 0 ? (uint32_t)kk : 0u;
-  uint32_t *const lstage = dyn_lds + wave * kq;      // this wave's list
-  uint32_t *const lmerged = dyn_lds + kWavesPerBlock * kq;
+  {
+    const uint32_t wl = sh_loc.win_len;
+    for (uint32_t e = threadIdx.x; e < wl; e += kBlockThreads) sh_st.win[e] = 0;
+  }
+  __syncthreads();
 
   // Localization of the primary-pair mismatches given by per-lane bit mask
-  // pb (bit j = element i0 + j): ordered first-k staging and tile counts.
-  auto localize = [&](uint32_t pb, uint64_t i0) __attribute__((always_inline)) {
-    const uint32_t off0 = (uint32_t)(i0 - cstart);
-    if (kk > 0 && nfound < (uint32_t)kk) {
+  // pb (bit j = the element at chunk offset off0 + j): ordered first-k
+  // staging and tile counts.
+  auto localize = [&](uint32_t pb, uint32_t off0) __attribute__((always_inline)) {
+    asm volatile("" ::: "memory");  // read the block's parameters from LDS here
+    const ChunkTiles &g = sh_loc;
+    if (nfound < kq) {
+      uint32_t *const lstage = dyn_lds + wave * kq;  // this wave's list
       uint32_t before = 0, total = 0;
 #pragma unroll
       for (int j = 0; j < V; ++j) {
@@ -692,21 +778,21 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       while (bits != 0) {
         const int j = __builtin_ctz(bits);
         bits &= bits - 1;
-        if (pos < (uint32_t)kk) lstage[pos] = off0 + j;
+        if (pos < kq) lstage[pos] = off0 + j;
         ++pos;
       }
-      nfound = min(nfound + total, (uint32_t)kk);
+      nfound = min(nfound + total, kq);
     }
-    if (do_tiles) {
+    if (g.do_tiles != 0) {
       uint32_t bits = pb;
       while (bits != 0) {
         const int j = __builtin_ctz(bits);
         bits &= bits - 1;
-        const uint64_t t = tile_of(i0 + j, cols, th, tw, tiles_c, narrow);
-        if (win_ok && t >= win_base && t - win_base < (uint64_t)win_len)
-          atomicAdd(&sh_st.win[t - win_base], 1u);
+        const uint64_t t = tile_at(g, off0 + j);
+        if (t - g.win_base < (uint64_t)g.win_len)
+          atomicAdd(&sh_st.win[t - g.win_base], 1u);
         else
-          atomicAdd(&tile_maps[tile_off + t], 1u);
+          atomicAdd(&g.tile_maps[g.tile_off + t], 1u);
       }
     }
   };
@@ -731,7 +817,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
                                       : wave_max_val(lb_rel);
     if (v > T_rel) {
       T_rel = v;
-      b_rel = f32_down(v);
+      b_rel = v > 0.0 ? f32_down(v * (1.0 - 0x1p-20)) : 0.0f;
+      rel_zero = !(v > 0.0);
     }
   };
   // Tier-1 update of the lane bests for the lanes in absm | relm. Every
@@ -746,7 +833,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     if (la || lr) {
       double sd = 0.0, sa = 1.0;
       int sj = -1;
-#pragma unroll
+#pragma unroll 1
       for (int j = 0; j < V; ++j) {
         const float c = dec32<DT>(elem<DT>(cq, j));
         const float r = dec32<DT>(elem<DT>(rq, j));
@@ -812,9 +899,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   };
 
   // Exact binary64 evaluation of one step (element by element).
-  auto exact_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, uint64_t i0)
+  auto exact_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, uint32_t off0)
                         __attribute__((always_inline)) {
-    const uint32_t off0 = (uint32_t)(i0 - cstart);
     uint32_t pb = 0;
     uint32_t nan_c_step = 0, nan_r_step = 0, inf_c_step = 0, inf_r_step = 0;
     uint32_t fin_step = 0, rel_step = 0, undef_step = 0;
@@ -845,19 +931,22 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       fin_step += popc(ballot(fin));
       rel_step += popc(ballot(relok));
       undef_step += popc(ballot(fin && r == 0.0 && c != 0.0));
+      // deferred steps are evaluated after later steps of the stream: an
+      // equal value wins when it comes first
+      const uint32_t o = off0 + j;
       if (fin) {
         acc_abs += d;
-        if (d > lb_abs) {
+        if (d > lb_abs || (d == lb_abs && o < li_abs)) {
           lb_abs = d;
-          li_abs = off0 + j;
+          li_abs = o;
         }
       }
       if (relok) {
         const double q = d / a;
         acc_rel += q;
-        if (q > lb_rel) {
+        if (q > lb_rel || (q == lb_rel && o < li_rel)) {
           lb_rel = q;
-          li_rel = off0 + j;
+          li_rel = o;
         }
       }
     }
@@ -878,33 +967,44 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       hfc += nan_c_step;
       hfr += nan_r_step;
     }
-    if (loc_on() && ballot(pb != 0) != 0) localize(pb, i0);
+    if (loc_on() && ballot(pb != 0) != 0) localize(pb, off0);
   };
 
-  // Tier 1 (binary32) for a full step; returns false (and changes nothing)
-  // when some element is not finite, has r = 0, is outside the exactness
-  // bound, or (single pair) falls between the gate bounds. One pass computes
-  // the sums, the running-maximum tests and whether any element fails a
-  // gate; the common step (valid, nothing failing, no new maximum) then
-  // commits with one uniform branch, and the counts of failing elements are
-  // taken in a second pass over the step only when some element failed.
-  auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0)
-                     __attribute__((always_inline)) -> bool {
+  // Tier 1 (binary32) for a full step. Returns kNotTaken (and changes
+  // nothing) when some element is not finite, has r = 0, is outside the
+  // exactness bound, or (single pair) falls between the gate bounds, and
+  // kDefer (changing nothing) when some element fails the gate while
+  // mismatch positions are recorded. One pass computes the sums, the
+  // running-maximum tests and whether any element fails a gate; the common
+  // step (valid, nothing failing, no new maximum) then commits with one
+  // uniform branch, and the counts of failing elements are taken in a second
+  // pass over the step only when some element failed.
+  auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
+                     __attribute__((always_inline)) -> int {
     float sa0 = 0.f, sa1 = 0.f, sq0 = 0.f, sq1 = 0.f;
-    float md = 0.f, me = -__builtin_inff(), mq = 0.f, mr = 0.f;
-    uint64_t fany = 0;
+    float md = 0.f, mq = 0.f, mr = 0.f;
+    // single pair: whether some element fails; several pairs: the failures
+    // of each pair are counted in this pass (binary64 gate on the exact
+    // difference) and pany holds those of the primary pair
+    uint64_t fany = 0, pany = 0;
+    uint32_t fc1[NT];
+#pragma unroll
+    for (int p = 0; p < NT; ++p) fc1[p] = 0;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      const float c = dec32<DT>(elem<DT>(cq, j));
       const float r = dec32<DT>(elem<DT>(rq, j));
-      const float d = __builtin_fabsf(c - r);
+      const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
       const float a = __builtin_fabsf(r);
       if constexpr (NT == 1) {
         fany |= ballot(d > __builtin_fmaf(a, rlo, alo));
       } else {
         const double d64 = d, a64 = a;
 #pragma unroll
-        for (int p = 0; p < NT; ++p) fany |= ballot(d64 > atol[p] + rtol[p] * a64);
+        for (int p = 0; p < NT; ++p) {
+          const uint64_t f = ballot(d64 > atol[p] + rtol[p] * a64);
+          fc1[p] += popc(f);
+          if (p == prim) pany |= f;
+        }
       }
       const float ra = __builtin_amdgcn_rcpf(a);
       const float q = d * ra;
@@ -917,75 +1017,70 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       }
       md = __builtin_fmaxf(md, d);
       mq = __builtin_fmaxf(mq, q);
-      me = __builtin_fmaxf(me, __builtin_fmaf(-b_rel, a, d));
-      // |r| in [2^-60, 2^124]: the reciprocal, the quotient and the gate
-      // thresholds stay in the normal binary32 range
-      if constexpr (DT != VC_F16) mr = __builtin_fmaxf(mr, __builtin_fmaf(a, 0x1p-64f, ra));
+
+      // |r| in [2^-60, 2^30]: the reciprocal, every non-zero quotient and
+      // the gate thresholds stay in the normal binary32 range (a non-zero
+      // |c - r| <= 0.998 |r| is at least 2^-92 there)
+      if constexpr (DT != VC_F16) mr = __builtin_fmaxf(mr, __builtin_fmaf(a, 0x1p30f, ra));
     }
     const float sa = sa0 + sa1, sq = sq0 + sq1;
     bool ok = __builtin_isfinite(sa + sq) && mq <= QT;
     if constexpr (DT != VC_F16) ok = ok && mr <= 0x1p60f;
     const uint64_t bad = ballot(!ok);
     const uint64_t absm = ballot(md > thr_abs);
-    const uint64_t relm = ballot(me > 0.0f);
-    if ((bad | absm | relm | fany) == 0) {
+    const uint64_t relm = rel_zero ? ballot(md > 0.0f) : ballot(mq >= b_rel);
+    const bool defer_loc = (NT == 1 ? fany : pany) != 0 && loc_on();
+    if ((bad | absm | relm | fany) == 0 && !defer_loc) {
+#pragma unroll
+      for (int p = 0; p < NT; ++p) mism[p] += fc1[p];
       ++fast_steps;
       acc_abs += (double)sa;
       acc_rel += (double)sq;
-      return true;
+      return kDone;
     }
-    if (bad != 0) return false;
-    uint32_t pb = 0;
-    if (fany != 0) {
-      // exact counts, the primary pair's bits and (single pair) the elements
-      // between the bounds
+    if (bad != 0) return kNotTaken;
+    if (defer_loc) return kDefer;
+    const u32x4 &cs = cq, &rs = rq;
+#pragma unroll
+    for (int p = 0; p < NT; ++p) mism[p] += fc1[p];
+    if (NT == 1 && fany != 0) {
+      // exact counts and (single pair) the elements between the bounds
       uint32_t fcnt[NT];
 #pragma unroll
       for (int p = 0; p < NT; ++p) fcnt[p] = 0;
       uint64_t amb = 0;
-#pragma unroll
+#pragma unroll 1
       for (int j = 0; j < V; ++j) {
-        const float c = dec32<DT>(elem<DT>(cq, j));
-        const float r = dec32<DT>(elem<DT>(rq, j));
+        const float c = dec32<DT>(elem<DT>(cs, j));
+        const float r = dec32<DT>(elem<DT>(rs, j));
         const float d = __builtin_fabsf(c - r);
         const float a = __builtin_fabsf(r);
-        if constexpr (NT == 1) {
-          const bool f = d > __builtin_fmaf(a, rlo, alo);
-          fcnt[0] += popc(ballot(f));
-          amb |= ballot(f && !(d > __builtin_fmaf(a, rhi, ahi)));
-          pb |= (f ? 1u : 0u) << j;
-        } else {
-          const double d64 = d, a64 = a;
-#pragma unroll
-          for (int p = 0; p < NT; ++p) {
-            const bool f = d64 > atol[p] + rtol[p] * a64;
-            fcnt[p] += popc(ballot(f));
-            if (p == prim) pb |= (f ? 1u : 0u) << j;
-          }
-        }
+        const bool f = d > __builtin_fmaf(a, rlo, alo);
+        fcnt[0] += popc(ballot(f));
+        amb |= ballot(f && !(d > __builtin_fmaf(a, rhi, ahi)));
       }
-      if (amb != 0) return false;
+      if (amb != 0) return kNotTaken;
 #pragma unroll
       for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
     }
     ++fast_steps;
     acc_abs += (double)sa;
     acc_rel += (double)sq;
-    if ((absm | relm) != 0) t1_update(cq, rq, absm, relm, (uint32_t)(i0 - cstart));
-    if (loc_on() && ballot(pb != 0) != 0) localize(pb, i0);
-    return true;
+    if ((absm | relm) != 0) t1_update(cs, rs, absm, relm, off0);
+    return kDone;
   };
 
-  // Tier 2 (binary64) for a full step; returns false (and changes nothing)
-  // when the step holds a NaN, an infinity or a zero reference.
-  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0)
-                     __attribute__((always_inline)) -> bool {
+  // Tier 2 (binary64) for a full step. Returns kNotTaken (changing nothing)
+  // when the step holds a NaN, an infinity or a zero reference, and kDefer
+  // (changing nothing) when a primary-pair mismatch must be localized.
+  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
+                     __attribute__((always_inline)) -> int {
     double sa = 0.0, sq = 0.0;
     uint32_t fcnt[NT];
 #pragma unroll
     for (int p = 0; p < NT; ++p) fcnt[p] = 0;
     uint64_t pany = 0, absm = 0, relm = 0;
-#pragma unroll
+#pragma unroll 1
     for (int j = 0; j < V; ++j) {
       const double c = dec64<DT>(elem<DT>(cq, j));
       const double r = dec64<DT>(elem<DT>(rq, j));
@@ -1003,30 +1098,16 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       absm |= ballot(d > T_abs);
       relm |= ballot(__builtin_fma(-T_rel, a, d) > 0.0);
     }
-    if (ballot(!__builtin_isfinite(sa + sq)) != 0) return false;
+    if (ballot(!__builtin_isfinite(sa + sq)) != 0) return kNotTaken;
+    if (pany != 0 && loc_on()) return kDefer;
 #pragma unroll
     for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
     ++fast_steps;
     acc_abs += sa;
     acc_rel += sq;
-    const uint32_t off0 = (uint32_t)(i0 - cstart);
     if (absm != 0) abs_update(cq, rq, absm, off0);
     if (relm != 0) rel_update(cq, rq, relm, off0);
-    if (pany != 0 && loc_on()) {
-      uint32_t pb = 0;
-#pragma unroll 1
-      for (int j = 0; j < V; ++j) {
-        const double r = dec64<DT>(elem<DT>(rq, j));
-        const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
-        double t = 0.0;
-#pragma unroll
-        for (int p = 0; p < NT; ++p)
-          if (p == prim) t = atol[p] + rtol[p] * __builtin_fabs(r);
-        if (!(d <= t)) pb |= 1u << j;
-      }
-      localize(pb, i0);
-    }
-    return true;
+    return kDone;
   };
 
   // Degenerate-output detector counts of one side (cand or ref) of a step
@@ -1108,7 +1189,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
 
   // Detector counts and bit-equality evidence of one step.
   auto integ_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, bool full,
-                        uint64_t i0) __attribute__((always_inline)) {
+                        uint32_t off0) __attribute__((always_inline)) {
+    const uint64_t i0 = cstart + off0;
     integ_side(cq, first_c, zc, efc, bfc, hfc, vmask, full);
     integ_side(rq, first_r, zr, efr, bfr, hfr, vmask, full);
     // cand bit-equal to ref: tested only while no difference has been seen
@@ -1142,81 +1224,119 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     }
   };
 
+  // Steps that tiers 1 and 2 do not complete (non-finite values, zero
+  // references, ambiguous gate decisions, and mismatches whose positions are
+  // recorded) are deferred: the wave lists them (in stream order) and later
+  // evaluates them with the exact tier, reloading their data. The exact
+  // tier's code then never runs inside the streaming loop, which keeps the
+  // loop's register footprint, and with it the number of resident waves,
+  // set by tiers 1 and 2 alone.
+  uint32_t nd = 0;  // deferred steps of the wave (uniform)
+  auto defer = [&](uint32_t off0) __attribute__((always_inline)) {
+    if (lane == 0) s_defer[wave][nd] = off0;
+    ++nd;
+  };
+
   // Back-off of tier 1: after a step it cannot take, the wave skips it for
   // 1, then 3, then 7 steps while the failures go on (data that is not tame
   // tends to stay so); a step it takes resets the back-off.
   uint32_t t1_hold = 0, t1_next = 0;
-  auto step = [&](const u32x4 &cq, const u32x4 &rq, uint64_t i0) __attribute__((always_inline)) {
+  auto step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
+                  __attribute__((always_inline)) {
     const bool tried = t1ok && t1_hold == 0;
-    bool done = tried && t1_step(cq, rq, i0);
+    int res = tried ? t1_step(cq, rq, off0) : kNotTaken;
     if (tried) {
-      t1_next = done ? 0u : min(2u * t1_next + 1u, 7u);
-      t1_hold = done ? 0u : t1_next;
+      const bool tame = res != kNotTaken;
+      t1_next = tame ? 0u : min(2u * t1_next + 1u, 7u);
+      t1_hold = tame ? 0u : t1_next;
     } else if (t1_hold > 0) {
       --t1_hold;
     }
-    if (!done) done = t2_step(cq, rq, i0);
-    if (!done) exact_step(cq, rq, ALL, i0);
-    if constexpr (INTEG) integ_step(cq, rq, ALL, true, i0);
+    if (res == kNotTaken) res = t2_step(cq, rq, off0);
+    if (res != kDone) defer(off0);
+    if constexpr (INTEG) integ_step(cq, rq, ALL, true, off0);
   };
 
   // Steps of ITER elements; wave w takes steps w, w+4, w+8, ... of the chunk,
   // so the block streams its chunk front to back, one KiB per wave and tensor.
-  const uint64_t n_steps = (cend - cstart) / ITER;  // full steps in the chunk
-  const uint64_t n_full = n_steps > wave ? (n_steps - wave + 3) / 4 : 0;
-  const uint64_t lane_off = (uint64_t)lane * V;
-  auto step_i0 = [&](uint64_t st) __attribute__((always_inline)) {
-    return cstart + (wave + 4 * st) * ITER + lane_off;
+  // (32-bit counters: a chunk holds fewer than 2^18 elements, and uniform
+  // 32-bit compares stay on the scalar unit)
+  const uint32_t n_steps = (uint32_t)((cend - cstart) / ITER);  // full steps in the chunk
+  const uint32_t n_full = n_steps > wave ? (n_steps - wave + 3) / 4 : 0;
+  const uint32_t lane_off = lane * V;
+  // chunk offset of this lane's first element in the wave's step st
+  auto step_off = [&](uint32_t st) __attribute__((always_inline)) {
+    return (wave + 4 * st) * ITER + lane_off;
+  };
+  // exact evaluation of the deferred steps, in stream order
+  auto flush = [&]() __attribute__((always_inline)) {
+    for (uint32_t e = 0; e < nd; ++e) {
+      const uint32_t o0 = s_defer[wave][e] + lane_off;
+      const uint64_t i0 = cstart + o0;
+      const u32x4 cq = vec ? load16(cand + i0 * ES) : load_guarded<DT>(cand, i0, cend);
+      const u32x4 rq = vec ? load16(ref + i0 * ES) : load_guarded<DT>(ref, i0, cend);
+      exact_step(cq, rq, ALL, o0);
+    }
+    nd = 0;
   };
   if (vec) {
-    // Two steps per trip with the next step's loads in flight. The loads are
-    // unconditional (past the end they re-read the last step, a cache hit) and
-    // the trip has no exit between its two steps, so on every path into the
-    // loop head the only loads in flight are the next trip's first step: the
-    // wait counters stay exact and the loads overlap the evaluation.
+    // Two steps per trip: while a step is evaluated the loads of the next
+    // step are in flight. The loads are unconditional (past the end they
+    // re-read the last step, a cache hit) and a trip has no exit between its
+    // steps, so every step is preceded by an explicit wait for its own loads
+    // only and the evaluation never waits for the prefetch, whatever path it
+    // takes. The inner loop ends when the deferral list could overflow; the
+    // list is then evaluated and streaming resumes.
     const uint8_t *const cb = cand + cstart * ES;  // block-uniform bases
     const uint8_t *const rb = ref + cstart * ES;
     const uint32_t lane_b = lane * 16u;
-    const uint64_t last = n_full > 0 ? n_full - 1 : 0;
-    auto off = [&](uint64_t st) __attribute__((always_inline)) {
-      return (uint32_t)((wave + 4 * min(st, last)) * ITER * ES) + lane_b;
+    const uint32_t last = n_full > 0 ? n_full - 1 : 0;
+    auto off = [&](uint32_t st) __attribute__((always_inline)) {
+      return (wave + 4 * min(st, last)) * ITER * ES + lane_b;
     };
-    auto ld = [&](const uint8_t *base, uint64_t st) __attribute__((always_inline)) {
+    auto ld = [&](const uint8_t *base, uint32_t st) __attribute__((always_inline)) {
       return load16(base + off(st));
     };
-    u32x4 ca = {0, 0, 0, 0}, ra = ca, cn = ca, rn = ca;
-    if (n_full > 0) {
-      ca = ld(cb, 0);
-      ra = ld(rb, 0);
+    uint32_t st = 0;
+    while (st < n_full) {
+      u32x4 ca = ld(cb, st), ra = ld(rb, st);
+      while (st + 1 < n_full && nd + 2 <= (uint32_t)kDeferCap) {
+        const u32x4 cn = ld(cb, st + 1), rn = ld(rb, st + 1);
+        __builtin_amdgcn_s_waitcnt(kWaitVm2);
+        step(ca, ra, step_off(st));
+        ca = ld(cb, st + 2);
+        ra = ld(rb, st + 2);
+        __builtin_amdgcn_s_waitcnt(kWaitVm2);
+        step(cn, rn, step_off(st + 1));
+        st += 2;
+      }
+      if (st + 1 == n_full && nd < (uint32_t)kDeferCap) {
+        __builtin_amdgcn_s_waitcnt(kWaitVm0);
+        step(ca, ra, step_off(st));
+        st += 1;
+      }
+      if (nd != 0) flush();
     }
-    const uint64_t n_pairs = n_full / 2;
-    for (uint64_t pr = 0; pr < n_pairs; ++pr) {
-      const uint64_t st = 2 * pr;
-      cn = ld(cb, st + 1);
-      rn = ld(rb, st + 1);
-      step(ca, ra, step_i0(st));
-      ca = ld(cb, st + 2);
-      ra = ld(rb, st + 2);
-      step(cn, rn, step_i0(st + 1));
-    }
-    if (n_full & 1) step(ca, ra, step_i0(n_full - 1));
   } else {
-    for (uint64_t st = 0; st < n_full; ++st) {
-      const uint64_t i0 = step_i0(st);
-      const u32x4 cq = load_guarded<DT>(cand, i0, cend);
-      const u32x4 rq = load_guarded<DT>(ref, i0, cend);
-      step(cq, rq, i0);
+    for (uint32_t st = 0; st < n_full; ++st) {
+      const uint32_t o0 = step_off(st);
+      const u32x4 cq = load_guarded<DT>(cand, cstart + o0, cend);
+      const u32x4 rq = load_guarded<DT>(ref, cstart + o0, cend);
+      step(cq, rq, o0);
+      if (nd == (uint32_t)kDeferCap) flush();
     }
+    if (nd != 0) flush();
   }
   if ((cend - cstart) % ITER != 0 && n_steps % 4 == wave) {
-    const uint64_t i0 = cstart + n_steps * ITER + lane_off;
+    const uint32_t o0 = n_steps * ITER + lane_off;
+    const uint64_t i0 = cstart + o0;
     const u32x4 ct = load_guarded<DT>(cand, i0, cend);
     const u32x4 rt = load_guarded<DT>(ref, i0, cend);
     uint32_t vmask = 0;
 #pragma unroll
     for (int j = 0; j < V; ++j) vmask |= (i0 + j < cend ? 1u : 0u) << j;
-    exact_step(ct, rt, vmask, i0);
-    if constexpr (INTEG) integ_step(ct, rt, vmask, false, i0);
+    exact_step(ct, rt, vmask, o0);
+    if constexpr (INTEG) integ_step(ct, rt, vmask, false, o0);
   }
 
   // wave reductions (fixed butterfly order)
@@ -1260,15 +1380,17 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   }
   __syncthreads();
   // flush the tile window (all four waves are done with it)
-  for (uint32_t e = threadIdx.x; e < win_len; e += kBlockThreads) {
+  const uint32_t f_len = sh_loc.win_len;
+  for (uint32_t e = threadIdx.x; e < f_len; e += kBlockThreads) {
     const uint32_t v = sh_st.win[e];
-    if (v != 0) atomicAdd(&tile_maps[tile_off + win_base + e], v);
+    if (v != 0) atomicAdd(&tile_maps[tile_off + sh_loc.win_base + e], v);
   }
   // Merge the four waves' ascending first-k lists (disjoint index sets) into
   // the k smallest: an entry's rank is its position in its own list plus the
   // number of smaller entries in the other three.
   uint32_t merged = 0;
   const uint32_t *const stage0 = dyn_lds;
+  uint32_t *const lmerged = dyn_lds + kWavesPerBlock * kq;
   if (kk > 0) {
     const uint32_t k = (uint32_t)kk;
     const uint32_t total =
