@@ -25,8 +25,9 @@
 //  1. binary32 tier. When every element of the step has |c - r| <= 0.998 |r|
 //     (binary16/bfloat16 storage) or <= 0.49 |r| (binary32 storage), the
 //     binary32 difference c - r is exact (the exponents of c and r differ by
-//     at most 10; for binary32 by Sterbenz's lemma), so |c - r| equals its
-//     binary64 value. The gate then compares it with binary64 thresholds
+//     at most 10; for binary32 by Sterbenz's lemma; binary16 values are
+//     multiples of 2^-24, so their difference is also exact whenever it is
+//     below 1), so |c - r| equals its binary64 value. The gate then compares it with binary64 thresholds
 //     (several pairs) or, for a single pair, with binary32 bounds
 //     fma(|r|, rlo, alo) <= atol + rtol |r| <= fma(|r|, rhi, ahi) (the host
 //     shrinks / grows the pair by 2^-20 and only enables this when the
@@ -74,7 +75,7 @@ struct Tr<VC_BF16> {
 };
 
 constexpr uint32_t kNone = 0xffffffffu;
-constexpr int kDeferCap = 16;  // deferred steps listed per wave before they are evaluated
+constexpr int kDeferCap = 32;  // deferred steps listed per wave before they are evaluated
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt in
 // 6:4, lgkmcnt in 11:8): wait until at most 2 (or 0) vector memory
 // operations are outstanding, other counters unconstrained
@@ -265,15 +266,31 @@ __device__ __forceinline__ void wave_max(double &v, uint32_t &i) {
   i = __builtin_amdgcn_readfirstlane(i);
 }
 
-// Wave-wide maximum of v (values only), wave-uniform.
-__device__ __forceinline__ double wave_max_val(double v) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) v = __builtin_fmax(v, __shfl_xor(v, m));
-  return readfirstlane_f64(v);
+// One step of a wave maximum: v and the value CTRL moves in (DPP; lanes with
+// no source, or outside the rows ROWS enables, see -1).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_max(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)b, CTRL, ROWS, 0xf, false);
+  const uint32_t hi =
+      __builtin_amdgcn_update_dpp(0xbff00000u, (uint32_t)(b >> 32), CTRL, ROWS, 0xf, false);
+  return __builtin_fmax(v, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)));
 }
 
-// Largest binary32 value <= x, for x = -1 or x >= 0 (the running-maximum
-// thresholds); values above the binary32 range give FLT_MAX.
+// Wave-wide maximum of v (values -1 or >= 0), wave-uniform: row shifts by
+// 1, 2, 3, 4 and 8 leave each row's maximum in its last lane, two row
+// broadcasts carry them to lane 63.
+__device__ __forceinline__ double wave_max_val(double v) {
+  v = dpp_max<0x111, 0xf>(v);  // row_shr:1
+  v = dpp_max<0x112, 0xf>(v);  // row_shr:2
+  v = dpp_max<0x113, 0xf>(v);  // row_shr:3
+  v = dpp_max<0x114, 0xf>(v);  // row_shr:4
+  v = dpp_max<0x118, 0xf>(v);  // row_shr:8
+  v = dpp_max<0x142, 0xa>(v);  // row_bcast:15
+  v = dpp_max<0x143, 0xc>(v);  // row_bcast:31
+  return readlane_f64(v, kWaveSize - 1);
+}
+
 // c - r of element j of a step in binary32 (one rounding); binary16 pairs go
 // through the mixed-precision FMA, which converts both operands exactly.
 template <int DT>
@@ -293,6 +310,8 @@ __device__ __forceinline__ float diff32(const u32x4 &cq, const u32x4 &rq, int j)
   }
 }
 
+// Largest binary32 value <= x, for x = -1 or x >= 0 (the running-maximum
+// thresholds); values above the binary32 range give FLT_MAX.
 __device__ __forceinline__ float f32_down(double x) {
   if (x < 0.0) return -1.0f;
   float f = (float)x;
@@ -619,8 +638,11 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   // localization parameters, read from LDS by the (rare) localization path
   // so that they do not occupy registers across the streaming loop
   __shared__ ChunkTiles sh_loc;
-  // each wave's list of deferred steps (chunk offsets of the steps)
+  // each wave's list of deferred steps (chunk offsets of the steps), the
+  // lists' lengths and first-k counts, and their merged order
   __shared__ uint32_t s_defer[kWavesPerBlock][kDeferCap];
+  __shared__ uint32_t s_coop[kWavesPerBlock][2];
+  __shared__ uint32_t s_order[kWavesPerBlock * kDeferCap];
   // dynamic LDS (launched with 5 * k words): each wave's ordered first-k
   // list, then the merged list of the block
   extern __shared__ uint32_t dyn_lds[];
@@ -821,39 +843,35 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       rel_zero = !(v > 0.0);
     }
   };
-  // Tier-1 update of the lane bests for the lanes in absm | relm. Every
-  // |c - r| of the step is exact in binary32, so the quotients of two
-  // elements compare exactly through binary64 cross products (products of
-  // two binary32 values are exact), and distinct quotients differ by more
-  // than a binary64 rounding: the lane picks its best quotient of the step
-  // that way and divides once.
+  // Tier-1 update of the lane bests for the lanes in absm | relm, given each
+  // lane's largest |c - r| (md) and largest quotient estimate (mq) of the
+  // step. Every |c - r| of the step is exact in binary32: a lane whose md
+  // beats its best finds the first element holding md. For the quotient,
+  // only elements whose estimate lies within 2^-19 of mq can hold the step's
+  // largest quotient (the estimates are within 2^-21 of the quotients); each
+  // of them (usually one) is divided exactly in binary64 and compared.
   auto t1_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t absm, uint64_t relm,
-                       uint32_t off0) __attribute__((always_inline)) {
-    const bool la = (absm >> lane) & 1ull, lr = (relm >> lane) & 1ull;
-    if (la || lr) {
-      double sd = 0.0, sa = 1.0;
-      int sj = -1;
+                       uint32_t off0, float md, float mq) __attribute__((always_inline)) {
+    if (((absm >> lane) & 1ull) && (double)md > lb_abs) {
+      uint32_t jb = 0;
+#pragma unroll 1
+      for (int j = V - 1; j >= 0; --j)
+        if (__builtin_fabsf(diff32<DT>(cq, rq, j)) == md) jb = (uint32_t)j;
+      lb_abs = md;
+      li_abs = off0 + jb;
+    }
+    if ((relm >> lane) & 1ull) {
+      const float band = mq * (1.0f - 0x1p-19f);
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
-        const float c = dec32<DT>(elem<DT>(cq, j));
-        const float r = dec32<DT>(elem<DT>(rq, j));
-        const double d = (double)__builtin_fabsf(c - r);
-        const double a = (double)__builtin_fabsf(r);
-        if (la && d > lb_abs) {
-          lb_abs = d;
-          li_abs = off0 + j;
-        }
-        if (lr && (sj < 0 || d * sa > sd * a)) {
-          sd = d;
-          sa = a;
-          sj = j;
-        }
-      }
-      if (lr) {
-        const double q = sd / sa;
-        if (q > lb_rel) {
-          lb_rel = q;
-          li_rel = off0 + (uint32_t)sj;
+        const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+        const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+        if (d * __builtin_amdgcn_rcpf(a) >= band) {
+          const double q = (double)d / (double)a;
+          if (q > lb_rel) {
+            lb_rel = q;
+            li_rel = off0 + (uint32_t)j;
+          }
         }
       }
     }
@@ -862,35 +880,40 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   };
 
   // Exact updates of the lane bests for the lanes in `lanes` (every element
-  // of those lanes is finite with r != 0: tiers 1 and 2 only).
-  auto abs_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
-                        __attribute__((always_inline)) {
+  // of those lanes is finite with r != 0: tiers 1 and 2 only). A late
+  // (deferred) step comes after later steps of the stream, so an equal value
+  // replaces the best when its index is smaller.
+  auto abs_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0,
+                        bool late) __attribute__((always_inline)) {
     if ((lanes >> lane) & 1ull) {
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
         const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - dec64<DT>(elem<DT>(rq, j)));
-        if (d > lb_abs) {
+        const uint32_t o = off0 + j;
+        if (d > lb_abs || (late && d == lb_abs && o < li_abs)) {
           lb_abs = d;
-          li_abs = off0 + j;
+          li_abs = o;
         }
       }
     }
     raise_abs(lanes);
   };
-  auto rel_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
-                        __attribute__((always_inline)) {
+  auto rel_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0,
+                        bool late) __attribute__((always_inline)) {
     if ((lanes >> lane) & 1ull) {
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
         const double r = dec64<DT>(elem<DT>(rq, j));
         const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
         const double a = __builtin_fabs(r);
+        const uint32_t o = off0 + j;
         // exact sign test: d / a > lb  <=>  d - lb * a > 0
-        if (a != 0.0 && __builtin_fma(-lb_rel, a, d) > 0.0) {
+        const double e = __builtin_fma(-lb_rel, a, d);
+        if (a != 0.0 && (e > 0.0 || (late && e == 0.0))) {
           const double q = d / a;
-          if (q > lb_rel) {
+          if (q > lb_rel || (late && q == lb_rel && o < li_rel)) {
             lb_rel = q;
-            li_rel = off0 + j;
+            li_rel = o;
           }
         }
       }
@@ -1024,7 +1047,9 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       if constexpr (DT != VC_F16) mr = __builtin_fmaxf(mr, __builtin_fmaf(a, 0x1p30f, ra));
     }
     const float sa = sa0 + sa1, sq = sq0 + sq1;
-    bool ok = __builtin_isfinite(sa + sq) && mq <= QT;
+    // exactness: |c - r| <= QT |r| bounds the exponent gap; binary16
+    // values are multiples of 2^-24, so any |c - r| < 1 is exact as well
+    bool ok = __builtin_isfinite(sa + sq) && (mq <= QT || (DT == VC_F16 && md < 1.0f));
     if constexpr (DT != VC_F16) ok = ok && mr <= 0x1p60f;
     const uint64_t bad = ballot(!ok);
     const uint64_t absm = ballot(md > thr_abs);
@@ -1066,14 +1091,14 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     ++fast_steps;
     acc_abs += (double)sa;
     acc_rel += (double)sq;
-    if ((absm | relm) != 0) t1_update(cs, rs, absm, relm, off0);
+    if ((absm | relm) != 0) t1_update(cs, rs, absm, relm, off0, md, mq);
     return kDone;
   };
 
   // Tier 2 (binary64) for a full step. Returns kNotTaken (changing nothing)
   // when the step holds a NaN, an infinity or a zero reference, and kDefer
   // (changing nothing) when a primary-pair mismatch must be localized.
-  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
+  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, bool late)
                      __attribute__((always_inline)) -> int {
     double sa = 0.0, sq = 0.0;
     uint32_t fcnt[NT];
@@ -1095,18 +1120,34 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       }
       sa += d;
       sq += d * __builtin_amdgcn_rcp(a);
-      absm |= ballot(d > T_abs);
-      relm |= ballot(__builtin_fma(-T_rel, a, d) > 0.0);
+      // (a late step also visits the values equal to the wave's best)
+      absm |= ballot(late ? d >= T_abs : d > T_abs);
+      const double e = __builtin_fma(-T_rel, a, d);
+      relm |= ballot(late ? e >= 0.0 : e > 0.0);
     }
     if (ballot(!__builtin_isfinite(sa + sq)) != 0) return kNotTaken;
-    if (pany != 0 && loc_on()) return kDefer;
+    if (!late && pany != 0 && loc_on()) return kDefer;
 #pragma unroll
     for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
     ++fast_steps;
     acc_abs += sa;
     acc_rel += sq;
-    if (absm != 0) abs_update(cq, rq, absm, off0);
-    if (relm != 0) rel_update(cq, rq, relm, off0);
+    if (absm != 0) abs_update(cq, rq, absm, off0, late);
+    if (relm != 0) rel_update(cq, rq, relm, off0, late);
+    if (late && pany != 0 && loc_on()) {
+      uint32_t pb = 0;
+#pragma unroll 1
+      for (int j = 0; j < V; ++j) {
+        const double r = dec64<DT>(elem<DT>(rq, j));
+        const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
+        double t = 0.0;
+#pragma unroll
+        for (int p = 0; p < NT; ++p)
+          if (p == prim) t = atol[p] + rtol[p] * __builtin_fabs(r);
+        if (!(d <= t)) pb |= 1u << j;
+      }
+      localize(pb, off0);
+    }
     return kDone;
   };
 
@@ -1252,7 +1293,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     } else if (t1_hold > 0) {
       --t1_hold;
     }
-    if (res == kNotTaken) res = t2_step(cq, rq, off0);
+    if (res == kNotTaken) res = t2_step(cq, rq, off0, false);
     if (res != kDone) defer(off0);
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, off0);
   };
@@ -1268,15 +1309,17 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   auto step_off = [&](uint32_t st) __attribute__((always_inline)) {
     return (wave + 4 * st) * ITER + lane_off;
   };
-  // exact evaluation of the deferred steps, in stream order
+  // Exact evaluation of one deferred step given its chunk offset.
+  auto deferred_step = [&](uint32_t soff) __attribute__((always_inline)) {
+    const uint32_t o0 = soff + lane_off;
+    const uint64_t i0 = cstart + o0;
+    const u32x4 cq = vec ? load16(cand + i0 * ES) : load_guarded<DT>(cand, i0, cend);
+    const u32x4 rq = vec ? load16(ref + i0 * ES) : load_guarded<DT>(ref, i0, cend);
+    exact_step(cq, rq, ALL, o0);
+  };
+  // the wave's deferred steps, in stream order
   auto flush = [&]() __attribute__((always_inline)) {
-    for (uint32_t e = 0; e < nd; ++e) {
-      const uint32_t o0 = s_defer[wave][e] + lane_off;
-      const uint64_t i0 = cstart + o0;
-      const u32x4 cq = vec ? load16(cand + i0 * ES) : load_guarded<DT>(cand, i0, cend);
-      const u32x4 rq = vec ? load16(ref + i0 * ES) : load_guarded<DT>(ref, i0, cend);
-      exact_step(cq, rq, ALL, o0);
-    }
+    for (uint32_t e = 0; e < nd; ++e) deferred_step(s_defer[wave][e]);
     nd = 0;
   };
   if (vec) {
@@ -1315,7 +1358,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
         step(ca, ra, step_off(st));
         st += 1;
       }
-      if (nd != 0) flush();
+      if (st < n_full) flush();  // the list is full and steps remain
     }
   } else {
     for (uint32_t st = 0; st < n_full; ++st) {
@@ -1323,9 +1366,46 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       const u32x4 cq = load_guarded<DT>(cand, cstart + o0, cend);
       const u32x4 rq = load_guarded<DT>(ref, cstart + o0, cend);
       step(cq, rq, o0);
-      if (nd == (uint32_t)kDeferCap) flush();
+      if (nd == (uint32_t)kDeferCap && st + 1 < n_full) flush();
     }
-    if (nd != 0) flush();
+  }
+  // The steps still listed are evaluated by the four waves together, in the
+  // chunk's stream order (wave w takes every fourth), when no wave has
+  // recorded a mismatch position yet: each wave then records positions in
+  // increasing order, as the final merge of the four lists requires. A
+  // concentrated failure (many listed steps in one wave) is thus spread over
+  // the block. Otherwise each wave evaluates its own list.
+  if (lane == 0) {
+    s_coop[wave][0] = nd;
+    s_coop[wave][1] = nfound;
+  }
+  __syncthreads();
+  const uint32_t nd0 = s_coop[0][0], nd1 = s_coop[1][0], nd2 = s_coop[2][0], nd3 = s_coop[3][0];
+  const uint32_t n_listed = nd0 + nd1 + nd2 + nd3;
+  if ((s_coop[0][1] | s_coop[1][1] | s_coop[2][1] | s_coop[3][1]) == 0 && n_listed != 0) {
+    // rank of every listed step among all listed steps (the lists ascend)
+    for (uint32_t e = threadIdx.x; e < kWavesPerBlock * kDeferCap; e += kBlockThreads) {
+      const uint32_t w = e / kDeferCap, i = e % kDeferCap;
+      if (i >= s_coop[w][0]) continue;
+      const uint32_t x = s_defer[w][i];
+      uint32_t rank = i;
+      for (uint32_t v = 0; v < (uint32_t)kWavesPerBlock; ++v) {
+        if (v == w) continue;
+        uint32_t lo = 0, hi = s_coop[v][0];
+        while (lo < hi) {
+          const uint32_t mid = (lo + hi) / 2;
+          if (s_defer[v][mid] < x) lo = mid + 1;
+          else hi = mid;
+        }
+        rank += lo;
+      }
+      s_order[rank] = x;
+    }
+    __syncthreads();
+    for (uint32_t r = wave; r < n_listed; r += kWavesPerBlock) deferred_step(s_order[r]);
+    nd = 0;
+  } else {
+    flush();
   }
   if ((cend - cstart) % ITER != 0 && n_steps % 4 == wave) {
     const uint32_t o0 = n_steps * ITER + lane_off;
