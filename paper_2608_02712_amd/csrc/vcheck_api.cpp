@@ -125,13 +125,13 @@ struct Plan {
   size_t bytes = 0;
 };
 
-// Elements per wave (a chunk is four of them): about 32K waves over the
+// Elements per wave (a chunk is four of them): about 16K waves over the
 // group, between 1 Ki elements and 64 KiB of each tensor per wave, a power of
 // two (so every step is 16-byte aligned). Many short chunks keep every CU
 // streaming until the end of the launch; longer ones amortize the per-block
 // setup and the running-maximum records.
 #ifndef VCK_WAVE_TARGET
-#define VCK_WAVE_TARGET 32768
+#define VCK_WAVE_TARGET 16384
 #endif
 uint32_t unit_for(uint64_t group_elems, int32_t dtype) {
   const uint64_t lo = 1024, hi = 65536 / elem_size(dtype);

@@ -187,9 +187,8 @@ struct ChunkTiles {
 // Tile (row-major index within the case's map) of the element at chunk
 // offset o, with 32-bit divisions by the invariant divisors only (a chunk
 // holds fewer than 2^18 elements).
-__device__ __forceinline__ uint64_t tile_at(const ChunkTiles &g, uint32_t o) {
-  uint32_t dr;  // rows past row0
-  uint64_t tc;  // tile column
+__device__ __forceinline__ uint64_t tile_at(const ChunkTiles &g, uint32_t o, uint32_t &dr) {
+  uint64_t tc;  // tile column (dr: rows past row0)
   if (!g.wide) {
     const uint32_t x = g.col0 + o;
     dr = div_by(x, g.cdiv.m, g.cdiv.shifts);
@@ -758,7 +757,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       // also covers the start (end) of its first (last) tile row when that
       // tile row holds another of its rows
       const uint32_t last = (uint32_t)(cend - cstart - 1);
-      const uint64_t t_first = tile_at(g, 0), t_last = tile_at(g, last);
+      uint32_t dr_first;
+      const uint64_t t_first = tile_at(g, 0, dr_first), t_last = tile_at(g, last, dr_first);
       const uint32_t dr_last =
           g.wide ? ((uint64_t)last >= g.room ? 1u : 0u) : div_by(g.col0 + last, g.cdiv.m, g.cdiv.shifts);
       const uint64_t rr_last = (uint64_t)g.rrem0 + dr_last;
@@ -805,16 +805,25 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       }
       nfound = min(nfound + total, kq);
     }
-    if (g.do_tiles != 0) {
-      uint32_t bits = pb;
+    if (g.do_tiles != 0 && pb != 0) {
+      // a lane's elements are consecutive: when its first and last
+      // mismatches lie in one row and one tile, so do all of them (one
+      // addition)
+      uint32_t dr_lo, dr_hi;
+      const uint64_t t_lo = tile_at(g, off0 + __builtin_ctz(pb), dr_lo);
+      const uint64_t t_hi = tile_at(g, off0 + 31 - __builtin_clz(pb), dr_hi);
+      const bool one = t_lo == t_hi && dr_lo == dr_hi;
+      uint32_t bits = one ? 1u : pb;
+      const uint32_t add = one ? popc(pb) : 1u;
       while (bits != 0) {
         const int j = __builtin_ctz(bits);
         bits &= bits - 1;
-        const uint64_t t = tile_at(g, off0 + j);
+        uint32_t dr;
+        const uint64_t t = one ? t_lo : tile_at(g, off0 + j, dr);
         if (t - g.win_base < (uint64_t)g.win_len)
-          atomicAdd(&sh_st.win[t - g.win_base], 1u);
+          atomicAdd(&sh_st.win[t - g.win_base], add);
         else
-          atomicAdd(&g.tile_maps[g.tile_off + t], 1u);
+          atomicAdd(&g.tile_maps[g.tile_off + t], add);
       }
     }
   };
