@@ -1005,8 +1005,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   // Tier 1 (binary32) for a full step. Returns kNotTaken (and changes
   // nothing) when some element is not finite, has r = 0, is outside the
   // exactness bound, or (single pair) falls between the gate bounds, and
-  // kDefer (changing nothing) when some element fails the gate while
-  // mismatch positions are recorded. One pass computes the sums, the
+  // (single pair) kDefer, changing nothing, when some element fails the gate
+  // while mismatch positions are recorded. One pass computes the sums, the
   // running-maximum tests and whether any element fails a gate; the common
   // step (valid, nothing failing, no new maximum) then commits with one
   // uniform branch, and the counts of failing elements are taken in a second
@@ -1017,8 +1017,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     float md = 0.f, mq = 0.f, mr = 0.f;
     // single pair: whether some element fails; several pairs: the failures
     // of each pair are counted in this pass (binary64 gate on the exact
-    // difference) and pany holds those of the primary pair
-    uint64_t fany = 0, pany = 0;
+    // difference)
+    uint64_t fany = 0;
     uint32_t fc1[NT];
 #pragma unroll
     for (int p = 0; p < NT; ++p) fc1[p] = 0;
@@ -1033,9 +1033,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
         const double d64 = d, a64 = a;
 #pragma unroll
         for (int p = 0; p < NT; ++p) {
-          const uint64_t f = ballot(d64 > atol[p] + rtol[p] * a64);
-          fc1[p] += popc(f);
-          if (p == prim) pany |= f;
+          fc1[p] += popc(ballot(d64 > atol[p] + rtol[p] * a64));
         }
       }
       const float ra = __builtin_amdgcn_rcpf(a);
@@ -1063,7 +1061,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     const uint64_t bad = ballot(!ok);
     const uint64_t absm = ballot(md > thr_abs);
     const uint64_t relm = rel_zero ? ballot(md > 0.0f) : ballot(mq >= b_rel);
-    const bool defer_loc = (NT == 1 ? fany : pany) != 0 && loc_on();
+    const bool defer_loc = NT == 1 && fany != 0 && loc_on();
     if ((bad | absm | relm | fany) == 0 && !defer_loc) {
 #pragma unroll
       for (int p = 0; p < NT; ++p) mism[p] += fc1[p];
@@ -1105,8 +1103,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   };
 
   // Tier 2 (binary64) for a full step. Returns kNotTaken (changing nothing)
-  // when the step holds a NaN, an infinity or a zero reference, and kDefer
-  // (changing nothing) when a primary-pair mismatch must be localized.
+  // when the step holds a NaN, an infinity or a zero reference, and (single
+  // pair) kDefer, changing nothing, when a mismatch must be localized.
   auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, bool late)
                      __attribute__((always_inline)) -> int {
     double sa = 0.0, sq = 0.0;
@@ -1135,7 +1133,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       relm |= ballot(late ? e >= 0.0 : e > 0.0);
     }
     if (ballot(!__builtin_isfinite(sa + sq)) != 0) return kNotTaken;
-    if (!late && pany != 0 && loc_on()) return kDefer;
+    if (NT == 1 && !late && pany != 0 && loc_on()) return kDefer;
 #pragma unroll
     for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
     ++fast_steps;
@@ -1158,6 +1156,27 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       localize(pb, off0);
     }
     return kDone;
+  };
+
+  // Primary-pair mismatch positions of a step that tier 1 or 2 committed
+  // (every element finite): the gate in binary64, then the localization.
+  auto locate_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
+                         __attribute__((always_inline)) {
+    double at = 0.0, rt = 0.0;
+#pragma unroll
+    for (int p = 0; p < NT; ++p)
+      if (p == prim) {
+        at = atol[p];
+        rt = rtol[p];
+      }
+    uint32_t pb = 0;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const double c = dec64<DT>(elem<DT>(cq, j));
+      const double r = dec64<DT>(elem<DT>(rq, j));
+      if (!(__builtin_fabs(c - r) <= at + rt * __builtin_fabs(r))) pb |= 1u << j;
+    }
+    if (loc_on() && ballot(pb != 0) != 0) localize(pb, off0);
   };
 
   // Degenerate-output detector counts of one side (cand or ref) of a step
@@ -1275,12 +1294,16 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   };
 
   // Steps that tiers 1 and 2 do not complete (non-finite values, zero
-  // references, ambiguous gate decisions, and mismatches whose positions are
-  // recorded) are deferred: the wave lists them (in stream order) and later
-  // evaluates them with the exact tier, reloading their data. The exact
-  // tier's code then never runs inside the streaming loop, which keeps the
-  // loop's register footprint, and with it the number of resident waves,
-  // set by tiers 1 and 2 alone.
+  // references, ambiguous gate decisions and, with one tolerance pair,
+  // mismatches whose positions are recorded) are deferred: the wave lists
+  // them (in stream order) and later evaluates them with the exact tier,
+  // reloading their data. With several pairs, a step the fast tiers
+  // committed with primary-pair mismatches is listed for its positions only
+  // (bit 0 of its listed offset set; offsets of steps are multiples of 256):
+  // there the exact tier would evaluate every pair again. Neither the exact
+  // tier's code nor the localization then runs inside the streaming loop,
+  // which keeps the loop's register footprint, and with it the number of
+  // resident waves, set by tiers 1 and 2 alone.
   uint32_t nd = 0;  // deferred steps of the wave (uniform)
   auto defer = [&](uint32_t off0) __attribute__((always_inline)) {
     if (lane == 0) s_defer[wave][nd] = off0;
@@ -1291,8 +1314,17 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   // 1, then 3, then 7 steps while the failures go on (data that is not tame
   // tends to stay so); a step it takes resets the back-off.
   uint32_t t1_hold = 0, t1_next = 0;
+  // primary-pair mismatch count of the wave (uniform)
+  auto prim_count = [&]() __attribute__((always_inline)) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int p = 0; p < NT; ++p)
+      if (p == prim) m = mism[p];
+    return m;
+  };
   auto step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
                   __attribute__((always_inline)) {
+    const uint32_t m0 = prim_count();
     const bool tried = t1ok && t1_hold == 0;
     int res = tried ? t1_step(cq, rq, off0) : kNotTaken;
     if (tried) {
@@ -1303,7 +1335,10 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       --t1_hold;
     }
     if (res == kNotTaken) res = t2_step(cq, rq, off0, false);
-    if (res != kDone) defer(off0);
+    if (res != kDone)
+      defer(off0);
+    else if (NT > 1 && prim_count() != m0 && loc_on())
+      defer(off0 | 1u);
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, off0);
   };
 
@@ -1318,13 +1353,17 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   auto step_off = [&](uint32_t st) __attribute__((always_inline)) {
     return (wave + 4 * st) * ITER + lane_off;
   };
-  // Exact evaluation of one deferred step given its chunk offset.
+  // Evaluation of one listed step given its list entry: the mismatch
+  // positions only (several pairs, bit 0 set), else the exact tier.
   auto deferred_step = [&](uint32_t soff) __attribute__((always_inline)) {
-    const uint32_t o0 = soff + lane_off;
+    const uint32_t o0 = (NT > 1 ? (soff & ~1u) : soff) + lane_off;
     const uint64_t i0 = cstart + o0;
     const u32x4 cq = vec ? load16(cand + i0 * ES) : load_guarded<DT>(cand, i0, cend);
     const u32x4 rq = vec ? load16(ref + i0 * ES) : load_guarded<DT>(ref, i0, cend);
-    exact_step(cq, rq, ALL, o0);
+    if (NT > 1 && (__builtin_amdgcn_readfirstlane(soff) & 1u))
+      locate_step(cq, rq, o0);
+    else
+      exact_step(cq, rq, ALL, o0);
   };
   // the wave's deferred steps, in stream order
   auto flush = [&]() __attribute__((always_inline)) {

@@ -1,8 +1,10 @@
 """GPU parity on large cases whose steps are mostly deferred to the exact tier.
 
 Steps holding a NaN, or a mismatch while mismatch positions are recorded,
-are evaluated after the streaming loop; when more of them pile up than a
-wave lists, the list is evaluated mid-stream. These cases are large enough
+are evaluated after the streaming loop (with several tolerance pairs a
+mismatching step is committed in the loop and only its positions are found
+afterwards); when more of them pile up than a wave lists, the list is
+evaluated mid-stream. These cases are large enough
 (2^29 binary32 elements in the batch) for the planner to give each wave 64
 steps, so both the list overflow and the final evaluation run, on an aligned
 case (vector loads) and on a misaligned one (element loads). Equal maxima are
@@ -35,7 +37,15 @@ def _case(rng, n):
     return c, r
 
 
-def test_deferred_steps_large():
+@pytest.mark.parametrize(
+    "tols,primary",
+    [
+        ([(1e-3, 1e-3, 0)], 0),
+        ([(1e-5, 1e-5, 0), (1e-3, 1e-3, 0), (0.5, 0.5, 1)], 1),
+    ],
+    ids=["one-pair", "three-pairs"],
+)
+def test_deferred_steps_large(tols, primary):
     import torch
 
     rng = np.random.default_rng(2608_77)
@@ -53,12 +63,11 @@ def test_deferred_steps_large():
     assert cand1.data_ptr() % 16 == 4
     del c0, r0, c1, r1
     cases = [(cand0, ref0), (cand1, ref1)]
-    tols = [(1e-3, 1e-3, 0)]
-    print("deferral: sweep of 2 x %d fp32 elements" % n, flush=True)
-    res = vc.vcheck_sweep(cases, tols, primary=0, tile=(64, 64), k=64)
+    print("deferral: sweep of 2 x %d fp32 elements, %d pairs" % (n, len(tols)), flush=True)
+    res = vc.vcheck_sweep(cases, tols, primary=primary, tile=(64, 64), k=64)
     for i, (c, r) in enumerate(cases):
         tag = "case %d" % i
-        o = oracle_case(c, r, tols, primary=0, tile=(64, 64), k=64)
+        o = oracle_case(c, r, tols, primary=primary, tile=(64, 64), k=64)
         assert_stats(res["stats"][i], o.stats, tag)
         assert [int(x) for x in res["mismatches"][i]] == o.mismatches, tag
         assert np.array_equal(res["tile_maps"][i], o.tile_map), tag + " tiles"
