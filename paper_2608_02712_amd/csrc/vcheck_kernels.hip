@@ -76,6 +76,9 @@ struct Tr<VC_BF16> {
 
 constexpr uint32_t kNone = 0xffffffffu;
 constexpr int kDeferCap = 32;  // deferred steps listed per wave before they are evaluated
+// a list entry keeps its list position and wave in bits 1..7 of the step's
+// chunk offset (a multiple of 256)
+static_assert(kDeferCap <= 32, "list entry layout");
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt in
 // 6:4, lgkmcnt in 11:8): wait until at most 2 (or 0) vector memory
 // operations are outstanding, other counters unconstrained
@@ -85,6 +88,7 @@ constexpr int kWaitVm0 = 0x0f70;
 constexpr int kDone = 0;      // evaluated and committed
 constexpr int kDefer = 1;     // to the exact tier, after streaming
 constexpr int kNotTaken = 2;  // not this tier (nothing changed)
+constexpr int kLocate = 3;    // committed; mismatch positions are recorded after streaming
 
 // 16 bytes of raw storage held by one lane.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -620,11 +624,22 @@ __device__ __forceinline__ uint64_t find_entry(const uint64_t *first, uint64_t l
 
 // ------------------------------------------------------------ main kernel
 
+// The register budget of 72 VGPRs (seven waves per SIMD) steers the
+// scheduler toward that occupancy; a variant that needs more registers still
+// gets them (none spills).
 template <int DT, int NT, bool INTEG>
-__global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_num_vgpr(72)))
+void main_kernel(const Params P) {
   constexpr int V = Tr<DT>::V;
   constexpr int ES = Tr<DT>::ES;
   constexpr uint32_t ITER = kWaveSize * V;  // elements per wave step
+  static_assert(ITER % 256 == 0, "list entry layout");
+  // Single pair, 16-bit storage: a step the fast tiers find mismatching
+  // while positions are recorded is committed, and its mismatch bits wait in
+  // LDS for the localization after streaming. Binary32 storage defers such
+  // a step whole to the exact tier instead: there the committing path costs
+  // registers (and resident waves) across the streaming loop.
+  constexpr bool kBitsInLds = NT == 1 && DT != VC_F32;
   constexpr uint32_t ALL = (1u << V) - 1u;
   // binary32 tier: bound on the estimate of |c - r| / |r| under which c - r
   // is exact in binary32 (with a margin for the estimate's error)
@@ -642,6 +657,9 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   __shared__ uint32_t s_defer[kWavesPerBlock][kDeferCap];
   __shared__ uint32_t s_coop[kWavesPerBlock][2];
   __shared__ uint32_t s_order[kWavesPerBlock * kDeferCap];
+  // single pair: each lane's primary-pair mismatch bits of the listed steps
+  // that the fast tiers committed (indexed by wave and list position)
+  __shared__ uint8_t s_pb[kWavesPerBlock][kDeferCap][kWaveSize];
   // dynamic LDS (launched with 5 * k words): each wave's ordered first-k
   // list, then the merged list of the block
   extern __shared__ uint32_t dyn_lds[];
@@ -889,17 +907,16 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   };
 
   // Exact updates of the lane bests for the lanes in `lanes` (every element
-  // of those lanes is finite with r != 0: tiers 1 and 2 only). A late
-  // (deferred) step comes after later steps of the stream, so an equal value
-  // replaces the best when its index is smaller.
-  auto abs_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0,
-                        bool late) __attribute__((always_inline)) {
+  // of those lanes is finite with r != 0: tiers 1 and 2 only, in stream
+  // order, so an equal value never replaces the best).
+  auto abs_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
+                        __attribute__((always_inline)) {
     if ((lanes >> lane) & 1ull) {
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
         const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - dec64<DT>(elem<DT>(rq, j)));
         const uint32_t o = off0 + j;
-        if (d > lb_abs || (late && d == lb_abs && o < li_abs)) {
+        if (d > lb_abs) {
           lb_abs = d;
           li_abs = o;
         }
@@ -907,8 +924,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     }
     raise_abs(lanes);
   };
-  auto rel_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0,
-                        bool late) __attribute__((always_inline)) {
+  auto rel_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
+                        __attribute__((always_inline)) {
     if ((lanes >> lane) & 1ull) {
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
@@ -918,9 +935,9 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
         const uint32_t o = off0 + j;
         // exact sign test: d / a > lb  <=>  d - lb * a > 0
         const double e = __builtin_fma(-lb_rel, a, d);
-        if (a != 0.0 && (e > 0.0 || (late && e == 0.0))) {
+        if (a != 0.0 && e > 0.0) {
           const double q = d / a;
-          if (q > lb_rel || (late && q == lb_rel && o < li_rel)) {
+          if (q > lb_rel) {
             lb_rel = q;
             li_rel = o;
           }
@@ -930,9 +947,11 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     raise_rel(lanes);
   };
 
-  // Exact binary64 evaluation of one step (element by element).
+  // Exact binary64 evaluation of one step (element by element). Returns the
+  // lane's primary-pair mismatch bits (bit j: element j) for the caller's
+  // localization.
   auto exact_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t vmask, uint32_t off0)
-                        __attribute__((always_inline)) {
+                        __attribute__((always_inline)) -> uint32_t {
     uint32_t pb = 0;
     uint32_t nan_c_step = 0, nan_r_step = 0, inf_c_step = 0, inf_r_step = 0;
     uint32_t fin_step = 0, rel_step = 0, undef_step = 0;
@@ -999,7 +1018,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       hfc += nan_c_step;
       hfr += nan_r_step;
     }
-    if (loc_on() && ballot(pb != 0) != 0) localize(pb, off0);
+    return pb;
   };
 
   // Tier 1 (binary32) for a full step. Returns kNotTaken (and changes
@@ -1011,7 +1030,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   // step (valid, nothing failing, no new maximum) then commits with one
   // uniform branch, and the counts of failing elements are taken in a second
   // pass over the step only when some element failed.
-  auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
+  auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, uint32_t &pbm)
                      __attribute__((always_inline)) -> int {
     float sa0 = 0.f, sa1 = 0.f, sq0 = 0.f, sq1 = 0.f;
     float md = 0.f, mq = 0.f, mr = 0.f;
@@ -1061,7 +1080,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     const uint64_t bad = ballot(!ok);
     const uint64_t absm = ballot(md > thr_abs);
     const uint64_t relm = rel_zero ? ballot(md > 0.0f) : ballot(mq >= b_rel);
-    const bool defer_loc = NT == 1 && fany != 0 && loc_on();
+    // (binary32 storage, single pair: such a step is deferred whole)
+    const bool defer_loc = !kBitsInLds && NT == 1 && fany != 0 && loc_on();
     if ((bad | absm | relm | fany) == 0 && !defer_loc) {
 #pragma unroll
       for (int p = 0; p < NT; ++p) mism[p] += fc1[p];
@@ -1075,11 +1095,11 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     const u32x4 &cs = cq, &rs = rq;
 #pragma unroll
     for (int p = 0; p < NT; ++p) mism[p] += fc1[p];
+    int res = kDone;
     if (NT == 1 && fany != 0) {
-      // exact counts and (single pair) the elements between the bounds
-      uint32_t fcnt[NT];
-#pragma unroll
-      for (int p = 0; p < NT; ++p) fcnt[p] = 0;
+      // exact counts, the lane's mismatch bits and the elements between
+      // the bounds
+      uint32_t fcnt = 0, bits = 0;
       uint64_t amb = 0;
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
@@ -1088,30 +1108,36 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
         const float d = __builtin_fabsf(c - r);
         const float a = __builtin_fabsf(r);
         const bool f = d > __builtin_fmaf(a, rlo, alo);
-        fcnt[0] += popc(ballot(f));
+        fcnt += popc(ballot(f));
         amb |= ballot(f && !(d > __builtin_fmaf(a, rhi, ahi)));
+        bits |= (f ? 1u : 0u) << j;
       }
       if (amb != 0) return kNotTaken;
-#pragma unroll
-      for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
+      mism[0] += fcnt;
+      if (kBitsInLds && loc_on()) {
+        pbm = bits;
+        res = kLocate;
+      }
     }
     ++fast_steps;
     acc_abs += (double)sa;
     acc_rel += (double)sq;
     if ((absm | relm) != 0) t1_update(cs, rs, absm, relm, off0, md, mq);
-    return kDone;
+    return res;
   };
 
   // Tier 2 (binary64) for a full step. Returns kNotTaken (changing nothing)
   // when the step holds a NaN, an infinity or a zero reference, and (single
-  // pair) kDefer, changing nothing, when a mismatch must be localized.
-  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, bool late)
+  // pair) kLocate, with the lane's mismatch bits in pbm, when a mismatch
+  // position must be recorded.
+  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, uint32_t &pbm)
                      __attribute__((always_inline)) -> int {
     double sa = 0.0, sq = 0.0;
     uint32_t fcnt[NT];
 #pragma unroll
     for (int p = 0; p < NT; ++p) fcnt[p] = 0;
-    uint64_t pany = 0, absm = 0, relm = 0;
+    uint64_t absm = 0, relm = 0;
+    uint32_t bits = 0;
 #pragma unroll 1
     for (int j = 0; j < V; ++j) {
       const double c = dec64<DT>(elem<DT>(cq, j));
@@ -1121,47 +1147,34 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
 #pragma unroll
       for (int p = 0; p < NT; ++p) {
         const double t = atol[p] + rtol[p] * a;
-        const uint64_t f = ballot(!(d <= t));
-        fcnt[p] += popc(f);
-        if (p == prim) pany |= f;
+        const bool f = !(d <= t);
+        fcnt[p] += popc(ballot(f));
+        if (kBitsInLds) bits |= (f ? 1u : 0u) << j;
       }
       sa += d;
       sq += d * __builtin_amdgcn_rcp(a);
-      // (a late step also visits the values equal to the wave's best)
-      absm |= ballot(late ? d >= T_abs : d > T_abs);
-      const double e = __builtin_fma(-T_rel, a, d);
-      relm |= ballot(late ? e >= 0.0 : e > 0.0);
+      absm |= ballot(d > T_abs);
+      relm |= ballot(__builtin_fma(-T_rel, a, d) > 0.0);
     }
     if (ballot(!__builtin_isfinite(sa + sq)) != 0) return kNotTaken;
-    if (NT == 1 && !late && pany != 0 && loc_on()) return kDefer;
+    if (!kBitsInLds && NT == 1 && fcnt[0] != 0 && loc_on()) return kDefer;
 #pragma unroll
     for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
     ++fast_steps;
     acc_abs += sa;
     acc_rel += sq;
-    if (absm != 0) abs_update(cq, rq, absm, off0, late);
-    if (relm != 0) rel_update(cq, rq, relm, off0, late);
-    if (late && pany != 0 && loc_on()) {
-      uint32_t pb = 0;
-#pragma unroll 1
-      for (int j = 0; j < V; ++j) {
-        const double r = dec64<DT>(elem<DT>(rq, j));
-        const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - r);
-        double t = 0.0;
-#pragma unroll
-        for (int p = 0; p < NT; ++p)
-          if (p == prim) t = atol[p] + rtol[p] * __builtin_fabs(r);
-        if (!(d <= t)) pb |= 1u << j;
-      }
-      localize(pb, off0);
+    if (absm != 0) abs_update(cq, rq, absm, off0);
+    if (relm != 0) rel_update(cq, rq, relm, off0);
+    if (kBitsInLds && fcnt[0] != 0 && loc_on()) {
+      pbm = bits;
+      return kLocate;
     }
     return kDone;
   };
 
-  // Primary-pair mismatch positions of a step that tier 1 or 2 committed
-  // (every element finite): the gate in binary64, then the localization.
-  auto locate_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0)
-                         __attribute__((always_inline)) {
+  // Primary-pair mismatch bits of a step that tier 1 or 2 committed (every
+  // element finite): the gate in binary64.
+  auto locate_step = [&](const u32x4 &cq, const u32x4 &rq) __attribute__((always_inline)) {
     double at = 0.0, rt = 0.0;
 #pragma unroll
     for (int p = 0; p < NT; ++p)
@@ -1176,7 +1189,7 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
       const double r = dec64<DT>(elem<DT>(rq, j));
       if (!(__builtin_fabs(c - r) <= at + rt * __builtin_fabs(r))) pb |= 1u << j;
     }
-    if (loc_on() && ballot(pb != 0) != 0) localize(pb, off0);
+    return pb;
   };
 
   // Degenerate-output detector counts of one side (cand or ref) of a step
@@ -1326,7 +1339,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
                   __attribute__((always_inline)) {
     const uint32_t m0 = prim_count();
     const bool tried = t1ok && t1_hold == 0;
-    int res = tried ? t1_step(cq, rq, off0) : kNotTaken;
+    uint32_t pbm = 0;
+    int res = tried ? t1_step(cq, rq, off0, pbm) : kNotTaken;
     if (tried) {
       const bool tame = res != kNotTaken;
       t1_next = tame ? 0u : min(2u * t1_next + 1u, 7u);
@@ -1334,11 +1348,17 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     } else if (t1_hold > 0) {
       --t1_hold;
     }
-    if (res == kNotTaken) res = t2_step(cq, rq, off0, false);
-    if (res != kDone)
+    if (res == kNotTaken) res = t2_step(cq, rq, off0, pbm);
+    if (res == kLocate) {
+      // single pair: the lane's mismatch bits wait in LDS; the entry holds
+      // the offset, bit 0, the list position and the wave
+      s_pb[wave][nd][lane] = (uint8_t)pbm;
+      defer(off0 | 1u | (nd << 1) | (wave << 6));
+    } else if (res != kDone) {
       defer(off0);
-    else if (NT > 1 && prim_count() != m0 && loc_on())
+    } else if (NT > 1 && prim_count() != m0 && loc_on()) {
       defer(off0 | 1u);
+    }
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, off0);
   };
 
@@ -1355,15 +1375,19 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
   };
   // Evaluation of one listed step given its list entry: the mismatch
   // positions only (several pairs, bit 0 set), else the exact tier.
-  auto deferred_step = [&](uint32_t soff) __attribute__((always_inline)) {
-    const uint32_t o0 = (NT > 1 ? (soff & ~1u) : soff) + lane_off;
-    const uint64_t i0 = cstart + o0;
-    const u32x4 cq = vec ? load16(cand + i0 * ES) : load_guarded<DT>(cand, i0, cend);
-    const u32x4 rq = vec ? load16(ref + i0 * ES) : load_guarded<DT>(ref, i0, cend);
-    if (NT > 1 && (__builtin_amdgcn_readfirstlane(soff) & 1u))
-      locate_step(cq, rq, o0);
-    else
-      exact_step(cq, rq, ALL, o0);
+  auto deferred_step = [&](uint32_t entry) __attribute__((always_inline)) {
+    const uint32_t e = __builtin_amdgcn_readfirstlane(entry);
+    const uint32_t o0 = (e & ~0xffu) + lane_off;
+    uint32_t pb;
+    if (kBitsInLds && (e & 1u)) {
+      pb = s_pb[(e >> 6) & 3u][(e >> 1) & 31u][lane];
+    } else {
+      const uint64_t i0 = cstart + o0;
+      const u32x4 cq = vec ? load16(cand + i0 * ES) : load_guarded<DT>(cand, i0, cend);
+      const u32x4 rq = vec ? load16(ref + i0 * ES) : load_guarded<DT>(ref, i0, cend);
+      pb = (NT > 1 && (e & 1u)) ? locate_step(cq, rq) : exact_step(cq, rq, ALL, o0);
+    }
+    if (loc_on() && ballot(pb != 0) != 0) localize(pb, o0);
   };
   // the wave's deferred steps, in stream order
   auto flush = [&]() __attribute__((always_inline)) {
@@ -1463,7 +1487,8 @@ __global__ __launch_bounds__(kBlockThreads) void main_kernel(const Params P) {
     uint32_t vmask = 0;
 #pragma unroll
     for (int j = 0; j < V; ++j) vmask |= (i0 + j < cend ? 1u : 0u) << j;
-    exact_step(ct, rt, vmask, o0);
+    const uint32_t pb = exact_step(ct, rt, vmask, o0);
+    if (loc_on() && ballot(pb != 0) != 0) localize(pb, o0);
     if constexpr (INTEG) integ_step(ct, rt, vmask, false, o0);
   }
 
