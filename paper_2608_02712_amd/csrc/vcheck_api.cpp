@@ -133,6 +133,19 @@ struct Plan {
 #ifndef VCK_WAVE_TARGET
 #define VCK_WAVE_TARGET 16384
 #endif
+// How the four waves of a block share its chunk: with 16-bit storage each
+// wave streams one contiguous quarter, so that the steps of a faulty tile
+// (the same columns of consecutive rows) spread over the four waves; with
+// binary32 storage (rows of 4 KiB and more, where a tile's rows already fall
+// on several waves) they take steps round robin, which streams a little
+// faster there.
+#ifndef VCK_SPLIT
+#define VCK_SPLIT 2
+#endif
+uint32_t split_for(int32_t dtype) {
+  return VCK_SPLIT == 2 ? (dtype == VC_F32 ? 0u : 1u) : (uint32_t)VCK_SPLIT;
+}
+
 uint32_t unit_for(uint64_t group_elems, int32_t dtype) {
   const uint64_t lo = 1024, hi = 65536 / elem_size(dtype);
   uint64_t u = lo;
@@ -505,39 +518,48 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
     Q.blob_dst = base + plan.off_table;
     Q.blob_bytes = plan.blob_bytes;
   }
-  vc_status st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
-  if (st == VC_OK && slot != nullptr) {
-    st = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
-    if (st == VC_OK) slot->pending = true;
-  }
-  if (lock.owns_lock()) lock.unlock();
-  if (st != VC_OK) return st;
-
-  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
-  g_prof_begin = g_prof_end = nullptr;
-  if (prof_begin != nullptr) {
-    st = hip_check(hipEventRecord(prof_begin, stream), "profile begin event");
+  // The launches of the call, back to back: no host work or event sits
+  // between them, so the GPU never waits for the host inside a call.
+  auto launch_all = [&]() -> vc_status {
+    vc_status st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
     if (st != VC_OK) return st;
+    hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
+    g_prof_begin = g_prof_end = nullptr;
+    if (prof_begin != nullptr) {
+      st = hip_check(hipEventRecord(prof_begin, stream), "profile begin event");
+      if (st != VC_OK) return st;
+    }
+    for (const Group &g : plan.groups) {
+      vck::Params G = P;
+      G.chunk_lo = g.chunk_lo;
+      G.case_lo = g.case_lo;
+      G.case_hi = g.case_hi;
+      G.unit_elems = g.unit;
+      G.split = split_for(g.dtype);
+      st = hip_check(vck::launch_main(g.dtype, plan.nt_class, plan.do_integ ? 1 : 0, G,
+                                      g.n_chunks, stream),
+                     "main kernel launch");
+      if (st != VC_OK) return st;
+    }
+    if (prof_end != nullptr) {
+      st = hip_check(hipEventRecord(prof_end, stream), "profile end event");
+      if (st != VC_OK) return st;
+    }
+    const uint64_t n_multi = single ? (plan.table[0].n_groups > 1 ? 1 : 0) : plan.multi.size();
+    return hip_check(vck::launch_finalize(P, plan.total_groups, n_multi, stream),
+                     "finalize launch");
+  };
+  vc_status st = launch_all();
+  if (slot != nullptr) {
+    // The staging slot may be refilled once the prologue has read it; an
+    // event behind the call's last kernel (recorded also after a failed
+    // launch, in case the prologue was enqueued) guards that. The slot's
+    // lock is held until then.
+    const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
+    if (se == VC_OK) slot->pending = true;
+    if (st == VC_OK) st = se;
   }
-  for (const Group &g : plan.groups) {
-    vck::Params G = P;
-    G.chunk_lo = g.chunk_lo;
-    G.case_lo = g.case_lo;
-    G.case_hi = g.case_hi;
-    G.unit_elems = g.unit;
-    st = hip_check(vck::launch_main(g.dtype, plan.nt_class, plan.do_integ ? 1 : 0, G, g.n_chunks,
-                                    stream),
-                   "main kernel launch");
-    if (st != VC_OK) return st;
-  }
-  if (prof_end != nullptr) {
-    st = hip_check(hipEventRecord(prof_end, stream), "profile end event");
-    if (st != VC_OK) return st;
-  }
-  const bool rates = out.match_rate != nullptr || out.numeric_rate != nullptr;
-  const uint64_t n_multi = single ? (plan.table[0].n_groups > 1 ? 1 : 0) : plan.multi.size();
-  return hip_check(vck::launch_finalize(P, plan.total_groups, n_multi, rates, stream),
-                   "finalize launch");
+  return st;
 }
 
 vc_case one_case(const vc_tensor *cand, const vc_tensor *ref, const vc_tensor *inputs,

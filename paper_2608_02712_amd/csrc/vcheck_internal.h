@@ -90,11 +90,12 @@ constexpr int kEqCandInpShift = 8;         // bits 8..15: cand bit-equal to inpu
 constexpr int kEqRefInpShift = 16;         // bits 16..23: ref bit-equal to input j
 
 // Suite counters in the workspace (cleared by the prologue, incremented by
-// the finalize launches, read by the rates kernel).
+// the finalize launches; the block that completes the last case reads them).
 struct Counters {
   uint32_t pass[VC_MAX_TOLS];       // cases passing pair p numerically
   uint32_t cert[VC_MAX_TOLS];       // ... and with no integrity flag
-  uint32_t pad[16];
+  uint32_t done;                    // cases whose results are written
+  uint32_t pad[15];
 };
 static_assert(sizeof(Counters) == 128, "Counters layout");
 
@@ -115,7 +116,7 @@ struct Params {
   int32_t tier1;               // 1: the binary32 fast path is valid for these pairs
   uint32_t unit_elems;         // elements per wave range (one quarter of a chunk)
   uint32_t eqnan_mask;         // bit p: equal_nan of pair p
-  uint32_t pad0;
+  uint32_t split;              // 1: each wave streams one contiguous quarter of a chunk
   uint64_t chunk_lo;           // first global chunk of this launch
   uint64_t case_lo;            // first table index of this launch's cases
   uint64_t case_hi;
@@ -162,7 +163,7 @@ struct Prologue {
 hipError_t launch_prologue(const Prologue &p, hipStream_t s);
 hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint64_t n_chunks,
                        hipStream_t s);
-hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi, bool rates,
+hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi,
                            hipStream_t s);
 
 }  // namespace vck

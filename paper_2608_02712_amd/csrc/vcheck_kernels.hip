@@ -9,10 +9,11 @@
 // degenerate-output detector counts. Each block of the main kernel writes
 // one chunk record; separate launches then merge the records in a fixed
 // order: a finalize kernel per group of up to 256 chunks (writing the case's
-// results directly when the case has one group), a second one for cases with
-// several groups, and a rates kernel for the suite match rates. Kernel
-// boundaries order the launches, so no device-scope fences or completion
-// counters are needed.
+// results directly when the case has one group) and a second one for cases
+// with several groups. Kernel boundaries order the launches, so the streaming
+// kernel needs no device-scope fences; the block that writes the last case's
+// results also writes the suite match rates, after one acquire-release
+// increment of a completion count per case.
 //
 // Work decomposition: a case is cut into chunks of 4 * U elements; one block
 // (4 waves) owns one chunk and streams it front to back: a step is 64 lanes x
@@ -593,12 +594,28 @@ __device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P,
     g.reserved = 0;
     if (P.integ != nullptr) P.integ[oi] = g;
   }
-  // suite counters (the rates kernel reads them after this launch)
+  // suite counters
   for (int p = 0; p < nt; ++p) {
     if (ok && cnt(p) == 0) {
       atomicAdd(&P.ctr->pass[p], 1u);
       if (flags == 0) atomicAdd(&P.ctr->cert[p], 1u);
     }
+  }
+  if (P.match_rate == nullptr && P.numeric_rate == nullptr) return;
+  // The case written last writes the suite rates. Its increment of the
+  // completion count acquires what every earlier case released with its
+  // own increment (the counter updates above), so it reads final counters.
+  const uint32_t done =
+      __hip_atomic_fetch_add(&P.ctr->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+  if (done + 1 != (uint32_t)P.n_cases) return;
+  const double nc = (double)P.n_cases;
+  for (int p = 0; p < nt; ++p) {
+    const uint32_t num = __hip_atomic_load(&P.ctr->pass[p], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t cert = __hip_atomic_load(&P.ctr->cert[p], __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    if (P.match_rate != nullptr) P.match_rate[p] = (double)cert / nc;
+    if (P.numeric_rate != nullptr) P.numeric_rate[p] = (double)num / nc;
   }
 }
 
@@ -1362,16 +1379,24 @@ void main_kernel(const Params P) {
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, off0);
   };
 
-  // Steps of ITER elements; wave w takes steps w, w+4, w+8, ... of the chunk,
-  // so the block streams its chunk front to back, one KiB per wave and tensor.
-  // (32-bit counters: a chunk holds fewer than 2^18 elements, and uniform
-  // 32-bit compares stay on the scalar unit)
+  // Steps of ITER elements (one KiB per wave and tensor). Either wave w
+  // streams the contiguous quarter [w q, (w + 1) q) of the chunk's steps
+  // (split), or it takes steps w, w+4, w+8, ... (round robin, the block
+  // streaming its chunk front to back); the partial tail step goes to the
+  // wave whose range it continues. (32-bit counters: a chunk holds fewer than
+  // 2^18 elements, and uniform 32-bit arithmetic stays on the scalar unit.)
   const uint32_t n_steps = (uint32_t)((cend - cstart) / ITER);  // full steps in the chunk
-  const uint32_t n_full = n_steps > wave ? (n_steps - wave + 3) / 4 : 0;
+  const bool split = P.split != 0;
+  const uint32_t q_steps = (n_steps + 3) / 4;
+  const uint32_t w_first = split ? min(wave * q_steps, n_steps) : wave;
+  const uint32_t w_stride = split ? 1u : 4u;
+  const uint32_t n_full = split ? min(w_first + q_steps, n_steps) - w_first
+                                : (n_steps > wave ? (n_steps - wave + 3) / 4 : 0u);
+  const bool tail_here = split ? wave == 3 : n_steps % 4 == wave;
   const uint32_t lane_off = lane * V;
   // chunk offset of this lane's first element in the wave's step st
   auto step_off = [&](uint32_t st) __attribute__((always_inline)) {
-    return (wave + 4 * st) * ITER + lane_off;
+    return (w_first + w_stride * st) * ITER + lane_off;
   };
   // Evaluation of one listed step given its list entry: the mismatch
   // positions only (several pairs, bit 0 set), else the exact tier.
@@ -1407,7 +1432,7 @@ void main_kernel(const Params P) {
     const uint32_t lane_b = lane * 16u;
     const uint32_t last = n_full > 0 ? n_full - 1 : 0;
     auto off = [&](uint32_t st) __attribute__((always_inline)) {
-      return (wave + 4 * min(st, last)) * ITER * ES + lane_b;
+      return (w_first + w_stride * min(st, last)) * ITER * ES + lane_b;
     };
     auto ld = [&](const uint8_t *base, uint32_t st) __attribute__((always_inline)) {
       return load16(base + off(st));
@@ -1479,7 +1504,7 @@ void main_kernel(const Params P) {
   } else {
     flush();
   }
-  if ((cend - cstart) % ITER != 0 && n_steps % 4 == wave) {
+  if ((cend - cstart) % ITER != 0 && tail_here) {
     const uint32_t o0 = n_steps * ITER + lane_off;
     const uint64_t i0 = cstart + o0;
     const u32x4 ct = load_guarded<DT>(cand, i0, cend);
@@ -1703,16 +1728,6 @@ __global__ __launch_bounds__(kBlockThreads) void finalize_multi_kernel(const Par
                 P.gstage + cs.group_begin * k, k);
 }
 
-// Suite match rates from the pass counters of the finalize launches.
-__global__ void rates_kernel(const Params P) {
-  const int p = threadIdx.x;
-  if (p >= P.n_tols) return;
-  const double nc = (double)P.n_cases;
-  const uint32_t num = P.ctr->pass[p], cert = P.ctr->cert[p];
-  if (P.match_rate != nullptr) P.match_rate[p] = P.n_cases > 0 ? (double)cert / nc : 0.0;
-  if (P.numeric_rate != nullptr) P.numeric_rate[p] = P.n_cases > 0 ? (double)num / nc : 0.0;
-}
-
 // Copies the descriptor blob from pinned host memory, clears the counter
 // area and the tile maps; writes zero rates for a sweep without cases.
 __global__ __launch_bounds__(256) void prologue_kernel(const Prologue Q) {
@@ -1769,7 +1784,7 @@ hipError_t launch_prologue(const Prologue &p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi, bool rates,
+hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi,
                            hipStream_t s) {
   if (n_groups > 0) {
     hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)n_groups), dim3(kBlockThreads), 0, s, p);
@@ -1781,10 +1796,6 @@ hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi,
                        p);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-  }
-  if (rates && n_groups > 0) {
-    hipLaunchKernelGGL(rates_kernel, dim3(1), dim3(64), 0, s, p);
-    return hipGetLastError();
   }
   return hipSuccess;
 }
