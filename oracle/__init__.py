@@ -64,6 +64,21 @@ class Integrity(ctypes.Structure):
     ]
 
 
+HIST_BINS = 64
+HIST_EMIN = -40
+
+
+class TStats(ctypes.Structure):
+    _fields_ = [
+        ("numel", ctypes.c_uint64), ("nan", ctypes.c_uint64), ("inf", ctypes.c_uint64),
+        ("zero", ctypes.c_uint64), ("n_finite", ctypes.c_uint64),
+        ("min", ctypes.c_double), ("max", ctypes.c_double),
+        ("argmin", ctypes.c_int64), ("argmax", ctypes.c_int64),
+        ("sum", ctypes.c_double), ("sum_sq", ctypes.c_double), ("sum_abs", ctypes.c_double),
+        ("hist", ctypes.c_uint64 * HIST_BINS),
+    ]
+
+
 def _struct_dict(s) -> dict:
     return {name: getattr(s, name) for name, _ in s._fields_ if name != "reserved"}
 
@@ -87,6 +102,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.orc_decode.argtypes = [ctypes.c_int32, _P, ctypes.c_int64, _P]
     lib.orc_suite.restype = None
     lib.orc_suite.argtypes = [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, _P]
+    lib.orc_tensor_stats.restype = None
+    lib.orc_tensor_stats.argtypes = [ctypes.c_int32, _P, ctypes.c_int64, ctypes.POINTER(TStats)]
     return lib
 
 
@@ -211,3 +228,16 @@ def suite(mismatches: np.ndarray, status, flags=None, lib=None):
     lib.orc_suite(n_cases, n_tols, _ptr(m), _ptr(st), _ptr(fl) if fl is not None else None,
                   _ptr(pas), _ptr(rate))
     return pas, rate
+
+
+def tensor_stats(raw: np.ndarray, dtype: int, lib=None) -> dict:
+    """Tensor-statistics probe of one tensor (raw storage: float32 or 16-bit
+    patterns): counts, first-index min/max over finite values, binary64 sums
+    in index order and the binary-exponent histogram (see the C header)."""
+    lib = lib or default_lib()
+    raw = _raw(raw, dtype).reshape(-1)
+    st = TStats()
+    lib.orc_tensor_stats(dtype, _ptr(raw) if raw.size else None, raw.size, ctypes.byref(st))
+    d = _struct_dict(st)
+    d["hist"] = [int(v) for v in st.hist]
+    return d

@@ -265,3 +265,45 @@ void orc_suite(int32_t n_cases, int32_t n_tols, const uint64_t *mismatches,
     rate[p] = n_cases > 0 ? (double)certified / (double)n_cases : 0.0;
   }
 }
+
+/* ---- tensor-statistics probe ---------------------------------------------- */
+
+/* Histogram bin of a finite non-zero value: frexp gives x = m * 2^p with
+ * 0.5 <= |m| < 1, so floor(log2 |x|) = p - 1 exactly. */
+static int hist_bin(double x) {
+  int p = 0;
+  (void)frexp(x, &p);
+  const int b = (p - 1) - ORC_HIST_EMIN + 1;
+  return b < 0 ? 0 : (b > ORC_HIST_BINS - 1 ? ORC_HIST_BINS - 1 : b);
+}
+
+void orc_tensor_stats(int32_t dtype, const void *x, int64_t n, orc_tstats *out) {
+  memset(out, 0, sizeof *out);
+  out->numel = (uint64_t)n;
+  out->argmin = out->argmax = -1;
+  for (int64_t i = 0; i < n; ++i) {
+    const double v = decode_one(dtype, x, i);
+    if (isnan(v)) {
+      out->nan++;
+      continue;
+    }
+    if (isinf(v)) {
+      out->inf++;
+      continue;
+    }
+    out->n_finite++;
+    if (v == 0.0) out->zero++;
+    if (out->argmin < 0 || v < out->min) {
+      out->min = v;
+      out->argmin = i;
+    }
+    if (out->argmax < 0 || v > out->max) {
+      out->max = v;
+      out->argmax = i;
+    }
+    out->sum += v;
+    out->sum_sq += v * v;
+    out->sum_abs += fabs(v);
+    if (v != 0.0) out->hist[hist_bin(v)]++;
+  }
+}

@@ -83,6 +83,30 @@ int32_t orc_validate(int32_t dtype, const void *cand, const void *ref, int64_t r
                      const void *const *inputs, const int32_t *input_dtype,
                      const int64_t *input_numel, orc_integrity *integ);
 
+/* Tensor-statistics probe of one tensor (the multi-level tensor statistics
+ * that the engine's diagnostic instrumentation records at pipeline
+ * boundaries, Sec. 4.2, and the tensor-statistic probes of the mechanism
+ * figure's instrumentation panel). Over the n elements in flat order:
+ * counts of NaN, of infinities, of zeros (+0 and -0) and of finite values;
+ * the smallest and largest finite value with the first index holding each
+ * (0 and -1 when no value is finite; +0 and -0 compare equal, and the value
+ * reported is the element's own); binary64 sums of x, x*x and |x| over the
+ * finite values, accumulated in index order; and a histogram of the finite
+ * non-zero values by binary exponent e = floor(log2 |x|): bin
+ * e - ORC_HIST_EMIN + 1 clamped to [0, ORC_HIST_BINS - 1], so bin 0 gathers
+ * e < ORC_HIST_EMIN and the last bin e >= ORC_HIST_EMIN + ORC_HIST_BINS - 2. */
+enum { ORC_HIST_BINS = 64, ORC_HIST_EMIN = -40 };
+
+typedef struct orc_tstats {
+  uint64_t numel, nan, inf, zero, n_finite;
+  double min, max;
+  int64_t argmin, argmax;
+  double sum, sum_sq, sum_abs;
+  uint64_t hist[ORC_HIST_BINS];
+} orc_tstats;
+
+void orc_tensor_stats(int32_t dtype, const void *x, int64_t n, orc_tstats *out);
+
 /* Suite verdict over n_cases x n_tols mismatch counts (case-major).
  * status[c] < 0 marks a case that could not be evaluated (it fails).
  * flags[c] (nullable) are the detector flags; certification requires 0.

@@ -13,7 +13,8 @@ Pinned outputs: decode (fp32/fp16/bf16), the gate at every tolerance pair,
 NaN/Inf counts, n_finite, n_rel, n_rel_undef, max/argmax abs and rel, sum
 abs/rel, tile map, first-k, all integrity counts, input/ref bit-equality
 masks, the five detector flags, copy_input, per-case pass and the suite match
-rate.
+rate; and the tensor-statistics probe (counts, first-index min/max, sums,
+exponent histogram).
 """
 from __future__ import annotations
 
@@ -548,7 +549,96 @@ def pin_suite_handbuilt(lib):
     assert rate.tolist() == [0.5, 1.0]
 
 
+def _tstats_expected(raw: np.ndarray, dtype: int) -> dict:
+    """Tensor statistics from numpy / torch conversions, numpy reductions,
+    frexp and math.fsum (an independent route to every field)."""
+    v = lib_decode(raw, dtype).reshape(-1)
+    fin = np.isfinite(v)
+    fv = v[fin]
+    idx = np.flatnonzero(fin)
+    e = {"numel": v.size, "nan": int(np.isnan(v).sum()), "inf": int(np.isinf(v).sum()),
+         "zero": int((fv == 0).sum()), "n_finite": int(fin.sum())}
+    if fv.size:
+        e["argmin"] = int(idx[np.argmin(fv)])  # first occurrence
+        e["argmax"] = int(idx[np.argmax(fv)])
+        e["min"], e["max"] = v[e["argmin"]], v[e["argmax"]]
+    else:
+        e["argmin"] = e["argmax"] = -1
+        e["min"] = e["max"] = 0.0
+    nz = fv[fv != 0]
+    ex = np.frexp(nz)[1].astype(np.int64) - 1
+    bins = np.clip(ex - oracle.HIST_EMIN + 1, 0, oracle.HIST_BINS - 1)
+    e["hist"] = np.bincount(bins, minlength=oracle.HIST_BINS).tolist()
+    e["fsum"] = (math.fsum(fv.tolist()), math.fsum((fv * fv).tolist()),
+                 math.fsum(np.abs(fv).tolist()))
+    e["abs_total"] = (math.fsum(np.abs(fv).tolist()), math.fsum((fv * fv).tolist()))
+    return e
+
+
+def _check_tstats(got: dict, e: dict) -> None:
+    for k in ("numel", "nan", "inf", "zero", "n_finite", "argmin", "argmax", "hist"):
+        assert got[k] == e[k], (k, got[k], e[k])
+    for k in ("min", "max"):
+        # the value of the element itself, sign of zero included
+        assert np.float64(got[k]).tobytes() == np.float64(e[k]).tobytes(), (k, got[k], e[k])
+    # a sum in index order is within n * 2^-53 * sum|terms| of the exact sum
+    n = max(e["n_finite"], 1)
+    bound = n * 2.0 ** -53
+    for k, exact, mag in (("sum", e["fsum"][0], e["abs_total"][0]),
+                          ("sum_sq", e["fsum"][1], e["abs_total"][1]),
+                          ("sum_abs", e["fsum"][2], e["abs_total"][0])):
+        assert abs(got[k] - exact) <= bound * mag, (k, got[k], exact)
+
+
+def pin_tstats_numpy(lib):
+    """Tensor statistics of random bit patterns of every dtype (NaN, +-Inf,
+    +-0, subnormals, huge values) and of normal data, against numpy."""
+    rng = np.random.default_rng(26081)
+    for dt in (F32, F16, BF16):
+        for n in (0, 1, 7, 1000, 4099):
+            cand, ref = random_pairs(rng, n, dt)
+            for raw in (cand, ref):
+                got = oracle.tensor_stats(as_storage(raw, dt), dt, lib=lib)
+                _check_tstats(got, _tstats_expected(raw, dt))
+
+
+def pin_tstats_handbuilt(lib):
+    """Literal tensor statistics of hand-built tensors."""
+    x = np.array([1.0, -0.0, 0.0, np.nan, np.inf, 0.75, -3.0, 65504, 2.0 ** -24, 1e-30, 1e30,
+                  -3.0], dtype=np.float32)
+    d = oracle.tensor_stats(x, F32, lib=lib)
+    assert (d["nan"], d["inf"], d["zero"], d["n_finite"]) == (1, 1, 2, 10)
+    assert (d["min"], d["argmin"]) == (-3.0, 6)  # the first of the two -3
+    assert (d["max"], d["argmax"]) == (float(np.float32(1e30)), 10)
+    # exponents: 1 -> 0, 0.75 -> -1, -3 -> 1 (twice), 65504 -> 15, 2^-24 -> -24,
+    # 1e-30 -> -100 (first bin), 1e30 -> 99 (last bin)
+    want = {41: 1, 40: 1, 42: 2, 56: 1, 17: 1, 0: 1, 63: 1}
+    assert {i: c for i, c in enumerate(d["hist"]) if c} == want
+    # zeros only: the first zero is both extremes, with its own sign
+    z = np.array([-0.0, 0.0, 0.0], dtype=np.float32)
+    d = oracle.tensor_stats(z, F32, lib=lib)
+    assert d["argmin"] == d["argmax"] == 0 and math.copysign(1.0, d["min"]) == -1.0
+    assert d["zero"] == 3 and sum(d["hist"]) == 0
+    # nothing finite
+    d = oracle.tensor_stats(np.array([np.nan, -np.inf], dtype=np.float32), F32, lib=lib)
+    assert (d["n_finite"], d["argmin"], d["argmax"], d["min"], d["sum"]) == (0, -1, -1, 0.0, 0.0)
+    # binary16: the smallest subnormal, the largest finite value, 1.5
+    h = np.array([2.0 ** -24, 65504.0, 1.5], dtype=np.float16).view(np.uint16)
+    d = oracle.tensor_stats(h, F16, lib=lib)
+    assert {i: c for i, c in enumerate(d["hist"]) if c} == {17: 1, 56: 1, 41: 1}
+    assert d["sum"] == 2.0 ** -24 + 65504.0 + 1.5
+    # bfloat16: a subnormal (exponent -133) and -2
+    b = np.array([0x0001, 0xC000], dtype=np.uint16)
+    d = oracle.tensor_stats(b, BF16, lib=lib)
+    assert {i: c for i, c in enumerate(d["hist"]) if c} == {0: 1, 42: 1}
+    assert (d["min"], d["argmin"], d["max"], d["argmax"]) == (-2.0, 1, 2.0 ** -133, 0)
+    assert d["sum_sq"] == 4.0 + 2.0 ** -266 and d["sum_abs"] == 2.0 + 2.0 ** -133
+    d = oracle.tensor_stats(np.zeros(0, dtype=np.uint16), F16, lib=lib)
+    assert d["numel"] == 0 and d["argmin"] == -1
+
+
 PINS = [
+    pin_tstats_handbuilt, pin_tstats_numpy,
     pin_gate_ties, pin_suite_handbuilt, pin_flags_handbuilt, pin_decode, pin_no_fma,
     pin_metrics_numpy, pin_gate_isclose, pin_localize_numpy, pin_invariants, pin_integrity_counts,
     pin_config5, pin_config4, pin_config2, pin_config3, pin_config1,

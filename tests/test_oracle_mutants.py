@@ -62,6 +62,13 @@ MUTANTS = [
     ("suite_ignores_flags", "if (ok && (!flags || flags[c] == 0)) certified += 1;",
      "if (ok) certified += 1;"),
     ("suite_ignores_status", "const int ok = status[c] >= 0 &&", "const int ok ="),
+    ("tstats_argmin_last_tie", "v < out->min", "v <= out->min"),
+    ("tstats_zero_in_hist", "if (v != 0.0) out->hist[hist_bin(v)]++;", "out->hist[hist_bin(v)]++;"),
+    ("tstats_bin_off_by_one", "const int b = (p - 1) - ORC_HIST_EMIN + 1;",
+     "const int b = p - ORC_HIST_EMIN + 1;"),
+    ("tstats_inf_in_sums", "    if (isinf(v)) {\n      out->inf++;\n      continue;\n    }",
+     "    if (isinf(v)) {\n      out->inf++;\n    }"),
+    ("tstats_sum_sq_abs", "out->sum_sq += v * v;", "out->sum_sq += fabs(v);"),
 ]
 
 
