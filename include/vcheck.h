@@ -237,6 +237,56 @@ vc_status vcheck_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols
                        const vc_sweep_opts *opts, const vc_sweep_out *out, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* ---- tensor-statistics probe ---------------------------------------------
+ *
+ * The multi-level tensor statistics that the engine's diagnostic
+ * instrumentation records at pipeline boundaries when a repair attempt has
+ * failed (Sec. 4.2, diagnostic instrumentation; the instrumentation panel of
+ * the mechanisms figure: tensor-statistic probes). One call probes a batch of
+ * tensors in one pass over HBM. Per tensor, over its elements in flat order:
+ *   nan, inf, zero      counts of NaN, of +-Inf and of +-0 elements;
+ *   n_finite            finite elements (zeros included);
+ *   min, max            smallest / largest finite value, the value of the
+ *                       element itself (+0 and -0 compare equal);
+ *   argmin, argmax      first flat index holding it (-1, and min = max = 0,
+ *                       when no element is finite);
+ *   sum, sum_sq, sum_abs binary64 sums of x, x*x and |x| over finite values
+ *                       (summation order unspecified: each differs from the
+ *                       exact sum by at most 1e-6 times the sum of its terms'
+ *                       magnitudes);
+ *   hist[b]             finite non-zero values with binary exponent
+ *                       e = floor(log2 |x|) in bin b = e - VC_HIST_EMIN + 1,
+ *                       clamped to [0, VC_HIST_BINS - 1] (bin 0 gathers
+ *                       e < VC_HIST_EMIN, the last bin e >= VC_HIST_EMIN + 62).
+ * mean = sum / n_finite, the standard deviation and the mean magnitude
+ * follow from these. */
+#define VC_HIST_BINS 64
+#define VC_HIST_EMIN (-40)
+
+typedef struct vc_tstats {
+  uint64_t numel, nan, inf, zero, n_finite;
+  double min, max;
+  int64_t argmin, argmax;
+  double sum, sum_sq, sum_abs;
+  uint64_t hist[VC_HIST_BINS];
+} vc_tstats;
+
+/* Statistics of tensors[0 .. n_tensors) (device data, any storage type, any
+ * element-aligned pointer; 16-byte alignment takes the vectorised path) into
+ * out[0 .. n_tensors) (device vc_tstats, one per tensor, in order).
+ * Workspace: vcheck_tensor_stats_workspace for the same tensors.
+ * Errors: VC_ERR_NULL (tensors, out or a data pointer of a non-empty tensor
+ * NULL), VC_ERR_DTYPE, VC_ERR_SHAPE, VC_ERR_ALIGN (pointer not aligned to the
+ * element size), VC_ERR_LIMIT (n_tensors outside 0 .. 2^20, or a tensor of
+ * 2^34 elements or more), VC_ERR_WORKSPACE, VC_ERR_HIP. n_tensors = 0 enqueues
+ * nothing. */
+vc_status vcheck_tensor_stats(const vc_tensor *tensors, int32_t n_tensors, vc_tstats *out,
+                              void *workspace, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for vcheck_tensor_stats over the same tensors. */
+vc_status vcheck_tensor_stats_workspace(const vc_tensor *tensors, int32_t n_tensors,
+                                        size_t *bytes);
+
 /* Profiling hook (tracing): the next vcheck_compare / _localize / _integrity /
  * _sweep call made on this thread records `begin_event` on its stream just
  * before its first streaming-kernel launch and `end_event` just after its

@@ -12,7 +12,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libvcheck.so")
-SOURCES = [os.path.join(CSRC, "vcheck_kernels.hip"), os.path.join(CSRC, "vcheck_api.cpp")]
+SOURCES = [os.path.join(CSRC, "vcheck_kernels.hip"), os.path.join(CSRC, "vcheck_probe.hip"),
+           os.path.join(CSRC, "vcheck_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # -ffp-contract=off: the tolerance gate and the metrics are specified with

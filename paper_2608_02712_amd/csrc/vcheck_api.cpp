@@ -583,6 +583,69 @@ vc_status check_pair(const vc_tensor *cand, const vc_tensor *ref) {
   return VC_OK;
 }
 
+// ---- tensor-statistics probe ---------------------------------------------
+
+struct ProbePlan {
+  std::vector<vck::ProbeTensor> tensors;
+  std::vector<uint64_t> chunk_first, group_first;
+  uint32_t unit = 1024;
+  uint64_t total_chunks = 0, total_groups = 0;
+  size_t off_recs = 0, off_grecs = 0, blob_bytes = 0, bytes = 0;
+};
+
+// Elements per wave of the probe: a power of two between 1 Ki and 8 Ki
+// (8-bit histogram counters per lane), about 16K waves over the batch, and
+// at least what keeps every tensor within 256 groups of 256 chunks.
+uint32_t probe_unit(uint64_t total, uint64_t largest) {
+  uint64_t u = 1024;
+  while (u < 8192 && u * 2 * VCK_WAVE_TARGET <= total) u *= 2;
+  while (u < 8192 && 4 * u * vck::kProbeGroupChunks * vck::kProbeGroupChunks < largest) u *= 2;
+  return (uint32_t)u;
+}
+
+vc_status make_probe_plan(const vc_tensor *tensors, int32_t n, ProbePlan &plan) {
+  if (n < 0 || n > (1 << 20)) return fail(VC_ERR_LIMIT, "n_tensors %d outside 0..2^20", n);
+  if (n > 0 && tensors == nullptr) return fail(VC_ERR_NULL, "tensors is NULL");
+  uint64_t total = 0, largest = 0;
+  char what[48];
+  for (int32_t i = 0; i < n; ++i) {
+    if (tensor_status(&tensors[i]) != VC_OK) {
+      snprintf(what, sizeof what, "tensor %d", i);
+      return check_tensor(&tensors[i], what);
+    }
+    const uint64_t m = (uint64_t)numel_of(tensors[i]);
+    if (m >= (1ull << 31)) return fail(VC_ERR_LIMIT, "tensor %d has 2^31 elements or more", i);
+    total += m;
+    largest = std::max(largest, m);
+  }
+  plan.unit = probe_unit(total, largest);
+  const uint64_t ch = 4ull * plan.unit;
+  plan.tensors.resize(n);
+  plan.chunk_first.resize(n);
+  plan.group_first.resize(n);
+  for (int32_t i = 0; i < n; ++i) {
+    vck::ProbeTensor &t = plan.tensors[i];
+    t.data = (const uint8_t *)tensors[i].data;
+    t.numel = (uint64_t)numel_of(tensors[i]);
+    t.dtype = tensors[i].dtype;
+    t.chunk_begin = plan.total_chunks;
+    const uint64_t nc = std::max<uint64_t>(1, (t.numel + ch - 1) / ch);
+    t.n_chunks = (uint32_t)nc;
+    plan.chunk_first[i] = plan.total_chunks;
+    plan.group_first[i] = plan.total_groups;
+    plan.total_chunks += nc;
+    plan.total_groups += (nc + vck::kProbeGroupChunks - 1) / vck::kProbeGroupChunks;
+  }
+  plan.blob_bytes = (sizeof(vck::ProbeTensor) + 2 * sizeof(uint64_t)) * (size_t)n;
+  size_t off = align_up(plan.blob_bytes);
+  plan.off_recs = off;
+  off += align_up(sizeof(vck::ProbeRec) * (size_t)plan.total_chunks);
+  plan.off_grecs = off;
+  off += align_up(sizeof(vck::ProbeRec) * (size_t)plan.total_groups);
+  plan.bytes = off + kAlign;  // room to align the caller's pointer
+  return VC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -746,3 +809,62 @@ vc_status vcheck_profile_events(void *begin_event, void *end_event) {
 }
 
 }  // extern "C"
+
+vc_status vcheck_tensor_stats_workspace(const vc_tensor *tensors, int32_t n_tensors,
+                                        size_t *bytes) {
+  g_last_error.clear();
+  if (bytes == nullptr) return fail(VC_ERR_NULL, "bytes is NULL");
+  ProbePlan plan;
+  const vc_status st = make_probe_plan(tensors, n_tensors, plan);
+  if (st != VC_OK) return st;
+  *bytes = plan.bytes;
+  return VC_OK;
+}
+
+vc_status vcheck_tensor_stats(const vc_tensor *tensors, int32_t n_tensors, vc_tstats *out,
+                              void *ws, size_t ws_bytes, void *stream_) {
+  g_last_error.clear();
+  ProbePlan plan;
+  vc_status st = make_probe_plan(tensors, n_tensors, plan);
+  if (st != VC_OK) return st;
+  if (n_tensors == 0) return VC_OK;
+  if (out == nullptr) return fail(VC_ERR_NULL, "out is NULL");
+  if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < plan.bytes)
+    return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
+  const hipStream_t stream = (hipStream_t)stream_;
+  uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
+  const size_t n = (size_t)n_tensors;
+  std::vector<uint8_t> blob(plan.blob_bytes);
+  memcpy(blob.data(), plan.tensors.data(), sizeof(vck::ProbeTensor) * n);
+  memcpy(blob.data() + sizeof(vck::ProbeTensor) * n, plan.chunk_first.data(), 8 * n);
+  memcpy(blob.data() + (sizeof(vck::ProbeTensor) + 8) * n, plan.group_first.data(), 8 * n);
+  std::unique_lock<std::mutex> lock;
+  Slot *slot = nullptr;
+  st = stage_blob(blob.data(), blob.size(), lock, slot);
+  if (st != VC_OK) return st;
+  vck::Prologue Q;
+  memset(&Q, 0, sizeof Q);
+  Q.blob_src = (const uint8_t *)slot->dev;
+  Q.blob_dst = base;
+  Q.blob_bytes = plan.blob_bytes;
+  Q.n_cases = 1;  // (no suite rates to clear)
+  vck::ProbeParams P;
+  memset(&P, 0, sizeof P);
+  P.tensors = (const vck::ProbeTensor *)base;
+  P.chunk_first = (const uint64_t *)(base + sizeof(vck::ProbeTensor) * n);
+  P.group_first = (const uint64_t *)(base + (sizeof(vck::ProbeTensor) + 8) * n);
+  P.n_tensors = n_tensors;
+  P.unit = plan.unit;
+  P.recs = (vck::ProbeRec *)(base + plan.off_recs);
+  P.grecs = (vck::ProbeRec *)(base + plan.off_grecs);
+  P.out = out;
+  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  if (st == VC_OK)
+    st = hip_check(vck::launch_probe(P, plan.total_chunks, plan.total_groups, stream),
+                   "probe launch");
+  // the staging slot is reused once the prologue has read it
+  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
+  if (se == VC_OK) slot->pending = true;
+  return st != VC_OK ? st : se;
+}

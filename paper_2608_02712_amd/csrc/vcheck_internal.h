@@ -159,6 +159,50 @@ struct Prologue {
   int32_t n_tols;
 };
 
+// ---- tensor-statistics probe (vcheck_probe.hip) ---------------------------
+
+constexpr int kHistBins = 64;
+constexpr int kHistEmin = -40;
+constexpr uint32_t kProbeGroupChunks = 256;  // chunk records merged per group block
+
+// One probed tensor (32 bytes). Its chunks are [chunk_begin, chunk_begin +
+// n_chunks) (an empty tensor owns one empty chunk), its groups of up to
+// kProbeGroupChunks chunks start at group_begin.
+struct ProbeTensor {
+  const uint8_t *data;
+  uint64_t numel;
+  uint64_t chunk_begin;
+  uint32_t n_chunks;
+  int32_t dtype;
+};
+static_assert(sizeof(ProbeTensor) == 32, "ProbeTensor layout");
+
+// Partial statistics of one chunk or group (element indices within the
+// tensor; -1 when no finite value).
+struct ProbeRec {
+  uint64_t nan, inf, zero, fin;
+  int64_t argmin, argmax;
+  double min, max, sum, sum_sq, sum_abs;
+  uint32_t hist[kHistBins];
+  uint64_t pad[1];
+};
+static_assert(sizeof(ProbeRec) == 352, "ProbeRec layout");
+static_assert(sizeof(vc_tstats) == 608, "vc_tstats layout");
+
+struct ProbeParams {
+  const ProbeTensor *tensors;    // [n] in the workspace
+  const uint64_t *chunk_first;   // [n] first chunk of each tensor (ascending)
+  const uint64_t *group_first;   // [n] first group of each tensor (ascending)
+  int32_t n_tensors;
+  uint32_t unit;                 // elements per wave (a chunk is four)
+  ProbeRec *recs;                // [total chunks]
+  ProbeRec *grecs;               // [total groups]
+  vc_tstats *out;                // [n]
+};
+
+hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_groups,
+                        hipStream_t s);
+
 // Launchers (vcheck_kernels.hip). Each returns the HIP error of its launch.
 hipError_t launch_prologue(const Prologue &p, hipStream_t s);
 hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint64_t n_chunks,

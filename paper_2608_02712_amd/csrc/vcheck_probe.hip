@@ -1,0 +1,399 @@
+// vcheck_probe.hip -- gfx950 kernels of the tensor-statistics probe.
+//
+// The diagnostic instrumentation of the repair loop records multi-level
+// tensor statistics at pipeline boundaries (Sec. 4.2; the instrumentation
+// panel of the mechanisms figure). One call probes a batch of tensors in one
+// streaming pass: counts of NaN, Inf, zero and finite elements, the first
+// smallest and largest finite value, binary64 sums of x, x^2 and |x|, and a
+// histogram of binary exponents.
+//
+// Work decomposition: a tensor is cut into chunks of 4 * U elements; one
+// block (4 waves) owns one chunk and each wave streams one contiguous
+// quarter, one 16-byte load per lane and step. Each block writes one chunk
+// record; a merge launch combines up to 256 chunk records per group in a
+// fixed order (writing the tensor's statistics when it has one group), and a
+// last launch combines the group records of larger tensors. Kernel
+// boundaries order the launches; no floating-point atomics are used, so the
+// results are bit-reproducible.
+//
+// Histogram: each lane owns a private row of 8-bit counters in LDS (four
+// bins per word, rows padded to 17 words so that lanes incrementing the same
+// bin hit different banks); a lane counts at most U / 64 <= 128 elements
+// (U <= 8192), so no counter overflows. The rows are summed when the chunk
+// is done.
+#pragma clang fp contract(off)
+
+#include "vcheck_internal.h"
+
+namespace vck {
+namespace {
+
+constexpr int kPWaves = 4;
+constexpr int kPThreads = kPWaves * 64;
+constexpr int kRowWords = kHistBins / 4 + 1;  // 8-bit counters plus one pad word
+
+#define PRB_GLOBAL __attribute__((address_space(1)))
+
+typedef uint32_t p32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ p32x4 pload16(const uint8_t *p) {
+  return __builtin_nontemporal_load((const PRB_GLOBAL p32x4 *)(p));
+}
+
+// Exact binary32 value of element j (of V) of a 16-byte vector.
+template <int DT>
+__device__ __forceinline__ float pdec(const p32x4 &q, int j) {
+  if constexpr (DT == VC_F32) {
+    return __uint_as_float(q[j]);
+  } else {
+    const uint32_t w = q[j >> 1];
+    const uint32_t h = (j & 1) ? (w >> 16) : (w & 0xffffu);
+    if constexpr (DT == VC_BF16) return __uint_as_float(h << 16);
+    else return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+  }
+}
+
+// Element loads of indices i0 .. i0 + V - 1 below n (others read as 0).
+template <int DT>
+__device__ __forceinline__ p32x4 pload_guarded(const uint8_t *base, uint64_t i0, uint64_t n) {
+  constexpr int V = DT == VC_F32 ? 4 : 8;
+  uint32_t v[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const uint64_t i = i0 + j;
+    uint32_t x = 0;
+    if (i < n) {
+      if constexpr (DT == VC_F32) x = *(const PRB_GLOBAL uint32_t *)(base + i * 4);
+      else x = *(const PRB_GLOBAL uint16_t *)(base + i * 2);
+    }
+    v[j] = x;
+  }
+  p32x4 r;
+  if constexpr (DT == VC_F32) {
+    r[0] = v[0];
+    r[1] = v[1];
+    r[2] = v[2];
+    r[3] = v[3];
+  } else {
+    r[0] = v[0] | (v[1] << 16);
+    r[1] = v[2] | (v[3] << 16);
+    r[2] = v[4] | (v[5] << 16);
+    r[3] = v[6] | (v[7] << 16);
+  }
+  return r;
+}
+
+// Last entry in [0, n) whose value in `first` is <= x (first ascends and
+// first[0] <= x), found by one wave: each lane tests one of 64 evenly spaced
+// probes and the ballot counts those at or below x, narrowing the range
+// 64-fold per round. Uniform result.
+__device__ __forceinline__ uint32_t find_first(const uint64_t *first, uint32_t n, uint64_t x) {
+  const PRB_GLOBAL uint64_t *f = (const PRB_GLOBAL uint64_t *)first;
+  const uint32_t lane = threadIdx.x & 63u;
+  uint32_t lo = 0;
+  while (n > 64) {
+    const uint32_t stride = (n + 63) / 64;
+    const uint32_t idx = lo + lane * stride;
+    const bool le = lane * stride < n ? f[idx] <= x : false;
+    const uint32_t k = (uint32_t)__popcll(__ballot(le)) - 1u;
+    lo += k * stride;
+    n = min(stride, n - k * stride);
+  }
+  const bool le = lane < n ? f[lo + lane] <= x : false;
+  return lo + (uint32_t)__popcll(__ballot(le)) - 1u;
+}
+
+// (value, index) of the smaller / larger of two candidates; equal values
+// keep the smaller index; index -1 marks no candidate.
+__device__ __forceinline__ void pick_min(double &v, int64_t &i, double v2, int64_t i2) {
+  if (i2 < 0) return;
+  if (i < 0 || v2 < v || (v2 == v && i2 < i)) {
+    v = v2;
+    i = i2;
+  }
+}
+__device__ __forceinline__ void pick_max(double &v, int64_t &i, double v2, int64_t i2) {
+  if (i2 < 0) return;
+  if (i < 0 || v2 > v || (v2 == v && i2 < i)) {
+    v = v2;
+    i = i2;
+  }
+}
+
+struct ProbeLds {
+  union {
+    uint32_t hist[kPWaves * 64 * kRowWords];  // while streaming
+    struct {                                  // per-thread partials afterwards
+      double d[3][kPThreads];
+      double mv[2][kPThreads];
+      int64_t mi[2][kPThreads];
+      uint64_t c[4][kPThreads];
+    };
+  };
+  uint32_t tensor;
+};
+
+// Fixed-order reduction of the per-thread partials in s (256 threads) into
+// a record (valid in thread 0).
+__device__ void block_reduce(ProbeLds &s, ProbeRec &r) {
+  const uint32_t t = threadIdx.x;
+  for (uint32_t w = kPThreads / 2; w >= 1; w >>= 1) {
+    __syncthreads();
+    if (t < w) {
+#pragma unroll
+      for (int f = 0; f < 3; ++f) s.d[f][t] += s.d[f][t + w];
+#pragma unroll
+      for (int f = 0; f < 4; ++f) s.c[f][t] += s.c[f][t + w];
+      pick_min(s.mv[0][t], s.mi[0][t], s.mv[0][t + w], s.mi[0][t + w]);
+      pick_max(s.mv[1][t], s.mi[1][t], s.mv[1][t + w], s.mi[1][t + w]);
+    }
+  }
+  __syncthreads();
+  if (t == 0) {
+    r.nan = s.c[0][0];
+    r.inf = s.c[1][0];
+    r.zero = s.c[2][0];
+    r.fin = s.c[3][0];
+    r.sum = s.d[0][0];
+    r.sum_sq = s.d[1][0];
+    r.sum_abs = s.d[2][0];
+    r.argmin = s.mi[0][0];
+    r.argmax = s.mi[1][0];
+    r.min = s.mi[0][0] < 0 ? 0.0 : s.mv[0][0];
+    r.max = s.mi[1][0] < 0 ? 0.0 : s.mv[1][0];
+  }
+}
+
+// Stream one chunk: per-lane partials, then the chunk record.
+template <int DT>
+__device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint64_t c1,
+                            uint32_t U, ProbeRec *rec) {
+  constexpr int V = DT == VC_F32 ? 4 : 8;
+  constexpr int ES = DT == VC_F32 ? 4 : 2;
+  constexpr uint32_t ITER = 64 * V;
+  const uint32_t t = threadIdx.x, lane = t & 63u;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  uint32_t *const row = s.hist + t * kRowWords;
+  for (int w = 0; w < kRowWords; ++w) row[w] = 0;
+  const uint64_t w0 = min(c0 + (uint64_t)wave * U, c1), w1 = min(w0 + U, c1);
+  const bool vec = ((uintptr_t)T.data % 16) == 0;
+  uint32_t n_nan = 0, n_inf = 0, n_zero = 0, n_fin = 0;
+  float mn = __builtin_inff(), mx = -__builtin_inff();
+  uint32_t imn = 0xffffffffu, imx = 0xffffffffu;  // offsets from c0
+  double sm = 0.0, sq = 0.0, sa = 0.0;
+  for (uint64_t b = w0; b < w1; b += ITER) {
+    const uint64_t i0 = b + (uint64_t)lane * V;
+    const p32x4 q = (vec && b + ITER <= w1) ? pload16(T.data + i0 * ES)
+                                            : pload_guarded<DT>(T.data, i0, w1);
+    const uint32_t o0 = (uint32_t)(i0 - c0);
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      if (i0 + j >= w1) break;
+      const float x = pdec<DT>(q, j);
+      const bool isn = x != x;
+      const bool isi = __builtin_fabsf(x) == __builtin_inff();
+      n_nan += isn ? 1u : 0u;
+      n_inf += isi ? 1u : 0u;
+      if (isn || isi) continue;
+      ++n_fin;
+      const uint32_t o = o0 + (uint32_t)j;
+      if (x < mn || imn == 0xffffffffu) {
+        mn = x;
+        imn = o;
+      }
+      if (x > mx || imx == 0xffffffffu) {
+        mx = x;
+        imx = o;
+      }
+      const double xd = (double)x;
+      sm += xd;
+      sq = __builtin_fma(xd, xd, sq);  // x*x is exact in binary64
+      sa += __builtin_fabs(xd);
+      if (x == 0.0f) {
+        ++n_zero;
+      } else {
+        const uint32_t e = (__float_as_uint(x) >> 23) & 0xffu;
+        const int bin = e == 0 ? 0 : min(max((int)e - 127 - kHistEmin + 1, 0), kHistBins - 1);
+        atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+      }
+    }
+  }
+  // histogram: thread t sums bin t % 64 over the rows of lanes
+  // (t / 64) * 64 .. + 63, then the four partial sums are added in order
+  __syncthreads();
+  const uint32_t bin = t & 63u, part = t >> 6;
+  uint32_t h = 0;
+  for (uint32_t l = part * 64; l < part * 64 + 64; ++l)
+    h += (s.hist[l * kRowWords + (bin >> 2)] >> ((bin & 3) * 8)) & 0xffu;
+  __syncthreads();  // the rows are dead from here: the partials reuse them
+  s.c[0][t] = h;
+  __syncthreads();
+  if (t < (uint32_t)kHistBins)
+    rec->hist[t] = (uint32_t)(s.c[0][t] + s.c[0][t + 64] + s.c[0][t + 128] + s.c[0][t + 192]);
+  __syncthreads();
+  s.c[0][t] = n_nan;
+  s.c[1][t] = n_inf;
+  s.c[2][t] = n_zero;
+  s.c[3][t] = n_fin;
+  s.d[0][t] = sm;
+  s.d[1][t] = sq;
+  s.d[2][t] = sa;
+  s.mv[0][t] = mn;
+  s.mi[0][t] = imn == 0xffffffffu ? -1 : (int64_t)(c0 + imn);
+  s.mv[1][t] = mx;
+  s.mi[1][t] = imx == 0xffffffffu ? -1 : (int64_t)(c0 + imx);
+  ProbeRec r;
+  block_reduce(s, r);
+  if (t == 0) {
+    rec->nan = r.nan;
+    rec->inf = r.inf;
+    rec->zero = r.zero;
+    rec->fin = r.fin;
+    rec->argmin = r.argmin;
+    rec->argmax = r.argmax;
+    rec->min = r.min;
+    rec->max = r.max;
+    rec->sum = r.sum;
+    rec->sum_sq = r.sum_sq;
+    rec->sum_abs = r.sum_abs;
+    rec->pad[0] = 0;
+  }
+}
+
+__global__ __launch_bounds__(kPThreads) void probe_kernel(const ProbeParams P) {
+  __shared__ ProbeLds s;
+  const uint64_t chunk = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const uint32_t ti = find_first(P.chunk_first, (uint32_t)P.n_tensors, chunk);
+    if (threadIdx.x == 0) s.tensor = ti;
+  }
+  __syncthreads();
+  const ProbeTensor T = P.tensors[s.tensor];
+  const uint64_t CH = 4ull * P.unit;
+  const uint64_t c0 = (chunk - T.chunk_begin) * CH;
+  const uint64_t c1 = min(c0 + CH, T.numel);
+  ProbeRec *const rec = P.recs + chunk;
+  switch (T.dtype) {
+    case VC_F32: probe_chunk<VC_F32>(s, T, c0, max(c0, c1), P.unit, rec); break;
+    case VC_F16: probe_chunk<VC_F16>(s, T, c0, max(c0, c1), P.unit, rec); break;
+    default: probe_chunk<VC_BF16>(s, T, c0, max(c0, c1), P.unit, rec); break;
+  }
+}
+
+// Merges records recs[0 .. n) (n <= 256) in a fixed order; thread 0 gets the
+// totals in r, threads 0..63 the histogram bins in hist.
+__device__ void merge_recs(ProbeLds &s, const ProbeRec *recs, uint32_t n, ProbeRec &r,
+                           uint64_t &hist) {
+  const uint32_t t = threadIdx.x;
+  const bool has = t < n;
+  const ProbeRec *const x = recs + (has ? t : 0);
+  s.c[0][t] = has ? x->nan : 0;
+  s.c[1][t] = has ? x->inf : 0;
+  s.c[2][t] = has ? x->zero : 0;
+  s.c[3][t] = has ? x->fin : 0;
+  s.d[0][t] = has ? x->sum : 0.0;
+  s.d[1][t] = has ? x->sum_sq : 0.0;
+  s.d[2][t] = has ? x->sum_abs : 0.0;
+  s.mv[0][t] = has ? x->min : 0.0;
+  s.mi[0][t] = has ? x->argmin : -1;
+  s.mv[1][t] = has ? x->max : 0.0;
+  s.mi[1][t] = has ? x->argmax : -1;
+  block_reduce(s, r);
+  // histogram: thread t sums bin t % 64 over records t / 64, t / 64 + 4, ...
+  const uint32_t bin = t & 63u, part = t >> 6;
+  uint64_t h = 0;
+  for (uint32_t i = part; i < n; i += 4) h += recs[i].hist[bin];
+  __syncthreads();
+  s.c[0][t] = h;
+  __syncthreads();
+  hist = t < 64 ? s.c[0][t] + s.c[0][t + 64] + s.c[0][t + 128] + s.c[0][t + 192] : 0;
+}
+
+__device__ void write_out(vc_tstats *o, const ProbeTensor &T, const ProbeRec &r, uint64_t h) {
+  const uint32_t t = threadIdx.x;
+  if (t < (uint32_t)kHistBins) o->hist[t] = h;
+  if (t == 0) {
+    o->numel = T.numel;
+    o->nan = r.nan;
+    o->inf = r.inf;
+    o->zero = r.zero;
+    o->n_finite = r.fin;
+    o->min = r.min;
+    o->max = r.max;
+    o->argmin = r.argmin;
+    o->argmax = r.argmax;
+    o->sum = r.sum;
+    o->sum_sq = r.sum_sq;
+    o->sum_abs = r.sum_abs;
+  }
+}
+
+// One block per group: the group's chunk records; a tensor with one group
+// gets its statistics here, a larger one a group record.
+__global__ __launch_bounds__(kPThreads) void probe_merge_kernel(const ProbeParams P) {
+  __shared__ ProbeLds s;
+  const uint64_t g = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const uint32_t ti = find_first(P.group_first, (uint32_t)P.n_tensors, g);
+    if (threadIdx.x == 0) s.tensor = ti;
+  }
+  __syncthreads();
+  const uint32_t ti = s.tensor;
+  const ProbeTensor T = P.tensors[ti];
+  const uint64_t gl = g - P.group_first[ti];
+  const uint64_t first = T.chunk_begin + gl * kProbeGroupChunks;
+  const uint32_t n = (uint32_t)min((uint64_t)kProbeGroupChunks,
+                                   T.chunk_begin + T.n_chunks - first);
+  ProbeRec r;
+  uint64_t h;
+  merge_recs(s, P.recs + first, n, r, h);
+  if (T.n_chunks <= kProbeGroupChunks) {
+    write_out(P.out + ti, T, r, h);
+    return;
+  }
+  ProbeRec *const gr = P.grecs + g;
+  if (threadIdx.x < (uint32_t)kHistBins) gr->hist[threadIdx.x] = (uint32_t)h;
+  if (threadIdx.x == 0) {
+    gr->nan = r.nan;
+    gr->inf = r.inf;
+    gr->zero = r.zero;
+    gr->fin = r.fin;
+    gr->argmin = r.argmin;
+    gr->argmax = r.argmax;
+    gr->min = r.min;
+    gr->max = r.max;
+    gr->sum = r.sum;
+    gr->sum_sq = r.sum_sq;
+    gr->sum_abs = r.sum_abs;
+    gr->pad[0] = 0;
+  }
+}
+
+// One block per tensor: the group records of a tensor with several groups.
+__global__ __launch_bounds__(kPThreads) void probe_final_kernel(const ProbeParams P) {
+  __shared__ ProbeLds s;
+  const uint32_t ti = blockIdx.x;
+  const ProbeTensor T = P.tensors[ti];
+  if (T.n_chunks <= kProbeGroupChunks) return;
+  const uint32_t n_groups = (T.n_chunks + kProbeGroupChunks - 1) / kProbeGroupChunks;
+  ProbeRec r;
+  uint64_t h;
+  merge_recs(s, P.grecs + P.group_first[ti], n_groups, r, h);
+  write_out(P.out + ti, T, r, h);
+}
+
+}  // namespace
+
+hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_groups,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(probe_kernel, dim3((uint32_t)n_chunks), dim3(kPThreads), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(probe_merge_kernel, dim3((uint32_t)n_groups), dim3(kPThreads), 0, s, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(probe_final_kernel, dim3((uint32_t)p.n_tensors), dim3(kPThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace vck

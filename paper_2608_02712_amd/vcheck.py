@@ -86,6 +86,15 @@ INTEG_DTYPE = np.dtype([
     ("reserved", "<u4")])
 assert STATS_DTYPE.itemsize == 128 and INTEG_DTYPE.itemsize == 88
 
+HIST_BINS = 64
+HIST_EMIN = -40
+TSTATS_DTYPE = np.dtype([
+    ("numel", "<u8"), ("nan", "<u8"), ("inf", "<u8"), ("zero", "<u8"), ("n_finite", "<u8"),
+    ("min", "<f8"), ("max", "<f8"), ("argmin", "<i8"), ("argmax", "<i8"),
+    ("sum", "<f8"), ("sum_sq", "<f8"), ("sum_abs", "<f8"), ("hist", "<u8", (HIST_BINS,)),
+])
+assert TSTATS_DTYPE.itemsize == 608
+
 _LIB = None
 
 
@@ -122,8 +131,13 @@ def lib() -> ctypes.CDLL:
     L.vcheck_profile_events.restype = ctypes.c_int32
     L.vcheck_abi_version.argtypes = []
     L.vcheck_abi_version.restype = ctypes.c_int32
+    L.vcheck_tensor_stats.argtypes = [ctypes.POINTER(VcTensor), ctypes.c_int32, P, P,
+                                      ctypes.c_size_t, P]
+    L.vcheck_tensor_stats_workspace.argtypes = [ctypes.POINTER(VcTensor), ctypes.c_int32,
+                                                ctypes.POINTER(ctypes.c_size_t)]
     for name in ("vcheck_compare", "vcheck_localize", "vcheck_integrity", "vcheck_sweep",
-                 "vcheck_workspace_bytes"):
+                 "vcheck_workspace_bytes", "vcheck_tensor_stats",
+                 "vcheck_tensor_stats_workspace"):
         getattr(L, name).restype = ctypes.c_int32
     if L.vcheck_abi_version() != 1:
         raise RuntimeError("libvcheck.so ABI version mismatch")
@@ -381,3 +395,50 @@ compare = vcheck_compare
 localize = vcheck_localize
 integrity = vcheck_integrity
 sweep = vcheck_sweep
+
+
+class TensorStats:
+    """A prepared tensor-statistics probe over a fixed batch of device tensors
+    (descriptors, output and workspace allocated once); launch() enqueues
+    vcheck_tensor_stats, results() reads the statistics back."""
+
+    def __init__(self, tensors):
+        self.tensors = list(tensors)
+        n = len(self.tensors)
+        self.desc = (VcTensor * max(n, 1))(*[tensor_desc(t) for t in self.tensors])
+        size = ctypes.c_size_t(0)
+        _check(lib().vcheck_tensor_stats_workspace(self.desc, n, ctypes.byref(size)))
+        dev = self.tensors[0].device if n else torch.device("cuda")
+        self.ws = _ws(size.value, dev)
+        self.out = torch.zeros(max(n, 1) * TSTATS_DTYPE.itemsize, dtype=torch.uint8, device=dev)
+
+    def launch(self, stream=None) -> None:
+        _check(lib().vcheck_tensor_stats(self.desc, len(self.tensors), self.out.data_ptr(),
+                                         self.ws.data_ptr(), self.ws.numel(),
+                                         _stream_ptr(stream)))
+
+    def results(self) -> list[dict]:
+        torch.cuda.synchronize(self.out.device)
+        arr = np.frombuffer(self.out.cpu().numpy().tobytes(), dtype=TSTATS_DTYPE)
+        res = []
+        for i in range(len(self.tensors)):
+            d = {k: arr[k][i].item() for k in TSTATS_DTYPE.names if k != "hist"}
+            d["hist"] = [int(v) for v in arr["hist"][i]]
+            # derived: mean, population standard deviation, mean magnitude
+            nf = d["n_finite"]
+            d["mean"] = d["sum"] / nf if nf else 0.0
+            d["std"] = (max(d["sum_sq"] / nf - d["mean"] ** 2, 0.0) ** 0.5) if nf else 0.0
+            d["abs_mean"] = d["sum_abs"] / nf if nf else 0.0
+            res.append(d)
+        return res
+
+
+def vcheck_tensor_stats(tensors, stream=None) -> list[dict]:
+    """Tensor-statistics probe of a batch of device tensors (one pass); one
+    dict per tensor: counts, min/max with first index, binary64 sums, the
+    binary-exponent histogram and the derived mean / std / abs_mean."""
+    ts = TensorStats(tensors)
+    if ts.tensors:
+        ts.launch(stream)
+    return ts.results()
+

@@ -175,3 +175,40 @@ def test_workspace_bytes(L):
     # a case with differing shapes is a per-case outcome in a sweep, not an error
     mixed = _cases((desc(shape=(4, 4)), desc(shape=(4, 5))))
     assert L.vcheck_workspace_bytes(mixed, 1, 1, None, ctypes.byref(n)) == 0
+
+
+ERR_CODES = {v: k for k, v in vc.STATUS_NAMES.items()}
+VC_ERR_NULL, VC_ERR_DTYPE = ERR_CODES["VC_ERR_NULL"], ERR_CODES["VC_ERR_DTYPE"]
+VC_ERR_WORKSPACE, VC_ERR_LIMIT = ERR_CODES["VC_ERR_WORKSPACE"], ERR_CODES["VC_ERR_LIMIT"]
+VC_ERR_ALIGN = ERR_CODES["VC_ERR_ALIGN"]
+
+
+def test_tensor_stats_host_checks(L):
+    """The tensor-statistics probe rejects malformed arguments on the host."""
+    size = ctypes.c_size_t(0)
+    arr = (vc.VcTensor * 3)(desc(), desc(vc.VC_F16, (7,)), desc(vc.VC_BF16, ()))
+    assert L.vcheck_tensor_stats_workspace(arr, 3, ctypes.byref(size)) == 0
+    assert size.value > 0
+    # workspace grows with the batch
+    one = ctypes.c_size_t(0)
+    assert L.vcheck_tensor_stats_workspace(arr, 1, ctypes.byref(one)) == 0
+    assert one.value <= size.value
+    assert L.vcheck_tensor_stats_workspace(arr, -1, ctypes.byref(size)) == VC_ERR_LIMIT
+    assert L.vcheck_tensor_stats_workspace(None, 2, ctypes.byref(size)) == VC_ERR_NULL
+    assert L.vcheck_tensor_stats_workspace(arr, 3, None) == VC_ERR_NULL
+    bad = (vc.VcTensor * 2)(desc(), desc(dtype=7))
+    assert L.vcheck_tensor_stats_workspace(bad, 2, ctypes.byref(size)) == VC_ERR_DTYPE
+    bad = (vc.VcTensor * 1)(desc(vc.VC_F32, (5,), data=FAKE + 2))
+    assert L.vcheck_tensor_stats_workspace(bad, 1, ctypes.byref(size)) == VC_ERR_ALIGN
+    bad = (vc.VcTensor * 1)(desc(vc.VC_F32, (5,), data=0))
+    assert L.vcheck_tensor_stats_workspace(bad, 1, ctypes.byref(size)) == VC_ERR_NULL
+    bad = (vc.VcTensor * 1)(desc(vc.VC_F16, (1 << 16, 1 << 15)))
+    assert L.vcheck_tensor_stats_workspace(bad, 1, ctypes.byref(size)) == VC_ERR_LIMIT
+    # the entry point itself: argument errors before anything is enqueued
+    assert L.vcheck_tensor_stats(arr, 3, None, FAKE, 1 << 30, None) == VC_ERR_NULL
+    assert L.vcheck_tensor_stats(arr, 3, FAKE, None, 1 << 30, None) == VC_ERR_WORKSPACE
+    assert L.vcheck_tensor_stats(arr, 3, FAKE, FAKE, 16, None) == VC_ERR_WORKSPACE
+    assert L.vcheck_tensor_stats(arr, 1 << 21, FAKE, FAKE, 1 << 30, None) == VC_ERR_LIMIT
+    # an empty batch enqueues nothing
+    assert L.vcheck_tensor_stats(None, 0, None, None, 0, None) == 0
+    assert vc.TSTATS_DTYPE.itemsize == 608
