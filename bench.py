@@ -10,7 +10,8 @@ The streaming kernels are timed in a second pass with events the library
 records around them.
 
 Headline line: the fp16 batch of 64 cases of 2048x2048 (the configuration the
-metric is quoted on). ``workloads`` holds the same figures for all five
+metric is quoted on). ``probe`` reports the tensor-statistics probe over the
+128 cand and ref tensors of that batch in one call. ``workloads`` holds the same figures for all five
 workloads, measured in the same run. ``roofline`` reports the main streaming
 kernel's achieved HBM bandwidth (algorithmic bytes / its event-timed average
 duration) against the 8 TB/s peak; ``cpu_baseline`` times the CPU oracle on a
@@ -142,6 +143,69 @@ def measure(cfg, steps, warmup, flush):
     return w, out
 
 
+def measure_probe(w, steps, warmup, flush):
+    """The tensor-statistics probe over every cand and ref tensor of workload
+    w in one call (the tensors of a batch of pipeline-boundary probes): call
+    time per step (events around the call, cache flushed before it) and the
+    streaming kernel's time (events the library records around it)."""
+    import torch
+
+    import oracle
+    import workloads as wl
+    from paper_2608_02712_amd import vcheck as vc
+
+    tensors = [t for c in w.cases for t in (c.cand, c.ref)]
+    ts = vc.TensorStats(tensors)
+    for _ in range(warmup):
+        ts.launch()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for quad in evs:  # (torch only times events it has seen recorded)
+        for e in quad:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        flush.fill_(i & 0xFF)
+        evs[i][0].record(stream)
+        ts.launch(stream)
+        evs[i][1].record(stream)
+    for i in range(steps):
+        flush.fill_((i + 1) & 0xFF)
+        vc.vcheck_profile_events(evs[i][2], evs[i][3])
+        ts.launch(stream)
+    torch.cuda.synchronize()
+    call = sorted(a.elapsed_time(b) for a, b, _, _ in evs)[steps // 2]
+    kern = sum(c.elapsed_time(d) for _, _, c, d in evs) / steps
+    nbytes = sum(t.numel() * t.element_size() for t in tensors)
+    # the oracle on a few tensors, one thread
+    spent, done = 0.0, 0
+    for t in tensors:
+        raw = wl.raw_numpy(t).reshape(-1)
+        t0 = time.perf_counter()
+        oracle.tensor_stats(raw, wl.dtype_code(t.dtype))
+        spent += time.perf_counter() - t0
+        done += raw.nbytes
+        if spent >= 2.0:
+            break
+    out = {
+        "workload": "tensor statistics of the %d cand and ref tensors of %s" % (
+            len(tensors), w.name),
+        "n_tensors": len(tensors),
+        "bytes": nbytes,
+        "ms_per_call": round(call, 5),
+        "gbps": round(nbytes / (call * 1e-3) / 1e9, 2),
+        "pct_hbm_peak": round(100.0 * nbytes / (call * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "tensors_per_s": round(len(tensors) / (call * 1e-3), 1),
+        "stream_kernel_ms": round(kern, 5),
+        "stream_kernel_gbps": round(nbytes / (kern * 1e-3) / 1e9, 2),
+        "oracle_one_thread_gbps": round(done / spent / 1e9, 4),
+    }
+    log("probe: %.3f ms/call, %.1f GB/s (%.1f%% of peak), streaming kernel %.3f ms" % (
+        call, out["gbps"], out["pct_hbm_peak"], kern))
+    return out
+
+
 def cpu_baseline(w, seconds):
     """The CPU oracle on whole cases of the workload: first one thread until
     the time budget is used (at least one case), then the same cases spread
@@ -241,6 +305,9 @@ def main():
     w, head = measure(first, args.steps, args.warmup, flush)
     results[first] = head
     cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds)
+    probe = None
+    if not args.only:
+        probe = measure_probe(w, args.steps, args.warmup, flush)
     del w
     torch.cuda.empty_cache()
     if not args.headline_only and not args.only:
@@ -278,6 +345,7 @@ def main():
                      "avg_launch_ms": head["main_kernel_ms"]},
         "cpu_baseline": cpu,
         "workloads": {str(k): v for k, v in sorted(results.items())},
+        "probe": probe,
     }
     print(json.dumps(line), flush=True)
 

@@ -288,10 +288,10 @@ vc_status vcheck_tensor_stats_workspace(const vc_tensor *tensors, int32_t n_tens
                                         size_t *bytes);
 
 /* Profiling hook (tracing): the next vcheck_compare / _localize / _integrity /
- * _sweep call made on this thread records `begin_event` on its stream just
- * before its first streaming-kernel launch and `end_event` just after its
- * last one, so hipEventElapsedTime gives the duration of the main kernels
- * alone (without the tile-map fill, finalize and rate kernels). Both are
+ * _sweep / _tensor_stats call made on this thread records `begin_event` on
+ * its stream just before its first streaming-kernel launch and `end_event`
+ * just after its last one, so hipEventElapsedTime gives the duration of the
+ * streaming kernels alone (without the prologue and the merge kernels). Both are
  * hipEvent_t handles created by the caller; the hook is consumed by that one
  * call. Pass NULL, NULL to clear it. Returns VC_OK, or VC_ERR_NULL when only
  * one of the two is NULL. */

@@ -859,9 +859,12 @@ vc_status vcheck_tensor_stats(const vc_tensor *tensors, int32_t n_tensors, vc_ts
   P.recs = (vck::ProbeRec *)(base + plan.off_recs);
   P.grecs = (vck::ProbeRec *)(base + plan.off_grecs);
   P.out = out;
+  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
+  g_prof_begin = g_prof_end = nullptr;
   st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
   if (st == VC_OK)
-    st = hip_check(vck::launch_probe(P, plan.total_chunks, plan.total_groups, stream),
+    st = hip_check(vck::launch_probe(P, plan.total_chunks, plan.total_groups, stream,
+                                     prof_begin, prof_end),
                    "probe launch");
   // the staging slot is reused once the prologue has read it
   const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");

@@ -200,8 +200,10 @@ struct ProbeParams {
   vc_tstats *out;                // [n]
 };
 
+// Launches the probe's streaming and merge kernels; `begin` / `end`
+// (nullable) are recorded around the streaming kernel.
 hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_groups,
-                        hipStream_t s);
+                        hipStream_t s, hipEvent_t begin, hipEvent_t end);
 
 // Launchers (vcheck_kernels.hip). Each returns the HIP error of its launch.
 hipError_t launch_prologue(const Prologue &p, hipStream_t s);

@@ -385,10 +385,13 @@ __global__ __launch_bounds__(kPThreads) void probe_final_kernel(const ProbeParam
 }  // namespace
 
 hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_groups,
-                        hipStream_t s) {
+                        hipStream_t s, hipEvent_t begin, hipEvent_t end) {
+  hipError_t e;
+  if (begin != nullptr && (e = hipEventRecord(begin, s)) != hipSuccess) return e;
   hipLaunchKernelGGL(probe_kernel, dim3((uint32_t)n_chunks), dim3(kPThreads), 0, s, p);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (end != nullptr && (e = hipEventRecord(end, s)) != hipSuccess) return e;
   hipLaunchKernelGGL(probe_merge_kernel, dim3((uint32_t)n_groups), dim3(kPThreads), 0, s, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

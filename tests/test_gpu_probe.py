@@ -93,3 +93,22 @@ def test_probe_repeat_is_bitwise_identical():
     ts.launch()
     b = ts.results()
     assert a == b
+
+
+def test_probe_extreme_magnitudes():
+    """Values far outside [2^-60, 2^60) (binary32 and bfloat16 subnormals,
+    huge values) next to ordinary ones: the sums keep them."""
+    import torch
+
+    x = np.array([1e-30, 3e-38, 1e-45, 1.5, -2.5e30, 3e38, -3e38, 0.0, 1e-20, 7.0] * 301,
+                 dtype=np.float32)
+    tiny = np.full(1001, 1e-30, dtype=np.float32)
+    batch = [(x.view(np.uint32), oracle.F32), (tiny.view(np.uint32), oracle.F32),
+             (oracle_pins.to_raw16(x, oracle.BF16), oracle.BF16),
+             (oracle_pins.to_raw16(tiny, oracle.BF16), oracle.BF16)]
+    tensors = [_raw_to_tensor(torch, raw, dt).cuda() for raw, dt in batch]
+    res = vc.vcheck_tensor_stats(tensors)
+    for i, ((raw, dt), got) in enumerate(zip(batch, res)):
+        want = oracle.tensor_stats(raw.view(np.float32) if dt == oracle.F32 else raw, dt)
+        _check(got, want, "extreme %d" % i)
+        assert got["sum_sq"] > 0.0
