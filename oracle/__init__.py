@@ -79,6 +79,20 @@ class TStats(ctypes.Structure):
     ]
 
 
+RATIO_BINS = 32
+ULP_BINS = 18
+
+
+class NearPass(ctypes.Structure):
+    _fields_ = [
+        ("numel", ctypes.c_uint64), ("n_pairs", ctypes.c_uint64), ("n_fail", ctypes.c_uint64),
+        ("n_zero_tol", ctypes.c_uint64), ("max_ratio", ctypes.c_double),
+        ("argmax_ratio", ctypes.c_int64), ("max_ulp_fail", ctypes.c_uint32),
+        ("reserved", ctypes.c_uint32),
+        ("ratio_hist", ctypes.c_uint64 * RATIO_BINS), ("ulp_hist", ctypes.c_uint64 * ULP_BINS),
+    ]
+
+
 def _struct_dict(s) -> dict:
     return {name: getattr(s, name) for name, _ in s._fields_ if name != "reserved"}
 
@@ -102,6 +116,11 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.orc_decode.argtypes = [ctypes.c_int32, _P, ctypes.c_int64, _P]
     lib.orc_suite.restype = None
     lib.orc_suite.argtypes = [ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, _P]
+    lib.orc_nearpass.restype = None
+    lib.orc_nearpass.argtypes = [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_double,
+                                 ctypes.c_double, ctypes.POINTER(NearPass)]
+    lib.orc_round_binary16.restype = ctypes.c_uint16
+    lib.orc_round_binary16.argtypes = [ctypes.c_double]
     lib.orc_tensor_stats.restype = None
     lib.orc_tensor_stats.argtypes = [ctypes.c_int32, _P, ctypes.c_int64, ctypes.POINTER(TStats)]
     return lib
@@ -240,4 +259,23 @@ def tensor_stats(raw: np.ndarray, dtype: int, lib=None) -> dict:
     lib.orc_tensor_stats(dtype, _ptr(raw) if raw.size else None, raw.size, ctypes.byref(st))
     d = _struct_dict(st)
     d["hist"] = [int(v) for v in st.hist]
+    return d
+
+
+def nearpass(cand: np.ndarray, ref: np.ndarray, dtype: int, atol: float, rtol: float,
+             lib=None) -> dict:
+    """Near-pass statistics of one case at one tolerance pair (raw storage
+    arrays; see the C header): violation-ratio maximum and histogram, and
+    the distance histogram on the binary16 / bfloat16 grid."""
+    lib = lib or default_lib()
+    cand = _raw(cand, dtype).reshape(-1)
+    ref = _raw(ref, dtype).reshape(-1)
+    if cand.size != ref.size:
+        raise ValueError("cand and ref sizes differ")
+    st = NearPass()
+    lib.orc_nearpass(dtype, _ptr(cand) if cand.size else None, _ptr(ref) if ref.size else None,
+                     cand.size, float(atol), float(rtol), ctypes.byref(st))
+    d = _struct_dict(st)
+    d["ratio_hist"] = [int(v) for v in st.ratio_hist]
+    d["ulp_hist"] = [int(v) for v in st.ulp_hist]
     return d

@@ -307,3 +307,98 @@ void orc_tensor_stats(int32_t dtype, const void *x, int64_t n, orc_tstats *out) 
     if (v != 0.0) out->hist[hist_bin(v)]++;
   }
 }
+
+/* ---- near-pass statistics -------------------------------------------------- */
+
+/* Nearest binary16 (ties to even) of a finite binary64 value, written from
+ * the format's definition: 1 sign, 5 exponent (bias 15), 10 fraction bits;
+ * the grid spacing is 2^(e-10) for |v| in [2^e, 2^(e+1)), e >= -14, and
+ * 2^-24 below 2^-14; magnitudes that round beyond 65504 become Inf. */
+uint16_t orc_round_binary16(double v) {
+  const uint16_t sign = signbit(v) ? 0x8000u : 0u;
+  double a = fabs(v);
+  if (a == 0.0) return sign;
+  int p = 0;
+  (void)frexp(a, &p); /* a = m * 2^p, 0.5 <= m < 1: exponent e = p - 1 */
+  int e = p - 1;
+  if (e < -14) e = -14; /* subnormal range: spacing 2^-24 */
+  const double spacing = ldexp(1.0, e - 10);
+  double k = a / spacing; /* exact: a power-of-two scaling */
+  double kr = floor(k);
+  const double frac = k - kr;
+  if (frac > 0.5 || (frac == 0.5 && fmod(kr, 2.0) != 0.0)) kr += 1.0;
+  const double r = kr * spacing;
+  if (r > 65504.0) return (uint16_t)(sign | 0x7c00u);
+  /* encode r exactly */
+  if (r < ldexp(1.0, -14)) return (uint16_t)(sign | (uint16_t)(r / ldexp(1.0, -24)));
+  int q = 0;
+  const double m = frexp(r, &q); /* r = m * 2^q */
+  const uint16_t expo = (uint16_t)(q - 1 + 15);
+  const uint16_t fracb = (uint16_t)((m * 2.0 - 1.0) * 1024.0);
+  return (uint16_t)(sign | (uint16_t)(expo << 10) | fracb);
+}
+
+/* Position on the ordered grid: -0 and +0 coincide. */
+static int64_t grid_key(uint16_t h) {
+  const int64_t mag = h & 0x7fff;
+  return (h & 0x8000u) ? -mag : mag;
+}
+
+/* Grid pattern of a finite storage value: binary16 for binary32 values
+ * (rounded), the stored pattern for 16-bit storage. Returns 0 when the
+ * rounded value is beyond the grid's finite range. */
+static int grid_of(int32_t dtype, const void *base, int64_t i, uint16_t *h) {
+  if (dtype == ORC_F32) {
+    *h = orc_round_binary16(decode_one(dtype, base, i));
+  } else {
+    *h = (uint16_t)bits_of(dtype, base, i);
+  }
+  const uint16_t expo_mask = dtype == ORC_BF16 ? 0x7f80u : 0x7c00u;
+  return (*h & expo_mask) != expo_mask;
+}
+
+void orc_nearpass(int32_t dtype, const void *cand, const void *ref, int64_t n, double atol,
+                  double rtol, orc_np *out) {
+  memset(out, 0, sizeof *out);
+  out->numel = (uint64_t)n;
+  out->argmax_ratio = -1;
+  for (int64_t i = 0; i < n; ++i) {
+    const double c = decode_one(dtype, cand, i);
+    const double r = decode_one(dtype, ref, i);
+    if (!isfinite(c) || !isfinite(r)) continue;
+    out->n_pairs++;
+    const double d = fabs(c - r);
+    const double t = atol + rtol * fabs(r);
+    const int fail = d > t;
+    if (fail) out->n_fail++;
+    if (t == 0.0) {
+      if (d > 0.0) out->n_zero_tol++;
+    } else {
+      const double q = d / t;
+      if (out->argmax_ratio < 0 || q > out->max_ratio) {
+        out->max_ratio = q;
+        out->argmax_ratio = i;
+      }
+      if (fail) {
+        int p = 0;
+        (void)frexp(q, &p); /* q >= 1: floor(log2 q) = p - 1 */
+        const int b = p - 1 > ORC_RATIO_BINS - 1 ? ORC_RATIO_BINS - 1 : p - 1;
+        out->ratio_hist[b]++;
+      }
+    }
+    uint16_t hc = 0, hr = 0;
+    const int in_c = grid_of(dtype, cand, i, &hc), in_r = grid_of(dtype, ref, i, &hr);
+    uint32_t dist;
+    if (in_c && in_r) {
+      const int64_t g = grid_key(hc) - grid_key(hr);
+      dist = (uint32_t)(g < 0 ? -g : g);
+      int bin = 0;
+      while (bin < 16 && (dist >> bin) != 0) bin++; /* bin = bit length of dist */
+      out->ulp_hist[bin]++;
+    } else {
+      dist = 0xffffffffu;
+      out->ulp_hist[ORC_ULP_BINS - 1]++;
+    }
+    if (fail && dist > out->max_ulp_fail) out->max_ulp_fail = dist;
+  }
+}

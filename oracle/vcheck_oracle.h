@@ -107,6 +107,44 @@ typedef struct orc_tstats {
 
 void orc_tensor_stats(int32_t dtype, const void *x, int64_t n, orc_tstats *out);
 
+/* Near-pass statistics of one case at one tolerance pair, for the near-pass
+ * and fp16-ceiling detection of the adaptive scheduling rules (Sec. 4.4) and
+ * the precision failures of Sec. 3.2 (Table 1: a cumsum whose binary32
+ * accumulation misses a binary16-rounding reference). Over the pairs where
+ * c and r are both finite, with d = |c - r| and t = atol + rtol*|r| in
+ * binary64 (each operation rounded):
+ *   n_pairs      such pairs; n_fail those with d > t;
+ *   n_zero_tol   pairs with t == 0 and d > 0 (violation ratio unbounded);
+ *   max_ratio    largest d / t over pairs with t > 0, argmax_ratio its first
+ *                index (0 and -1 when there is none);
+ *   ratio_hist   failing pairs with t > 0 by floor(log2(d / t)), the last
+ *                bin gathering 31 and more;
+ *   ulp_hist     pairs by their distance on the grid (binary16 for binary32
+ *                and binary16 storage, bfloat16 for bfloat16 storage): both
+ *                values rounded to the grid (nearest, ties to even), then the
+ *                number of grid values between them; bin 0 distance 0, bin
+ *                k in 1..16 distances [2^(k-1), 2^k), bin 17 pairs with a
+ *                value beyond the grid's finite range;
+ *   max_ulp_fail largest grid distance among failing pairs (0 if none,
+ *                0xffffffff when one lies beyond the grid's range). */
+enum { ORC_RATIO_BINS = 32, ORC_ULP_BINS = 18 };
+
+typedef struct orc_np {
+  uint64_t numel, n_pairs, n_fail, n_zero_tol;
+  double max_ratio;
+  int64_t argmax_ratio;
+  uint32_t max_ulp_fail, reserved;
+  uint64_t ratio_hist[ORC_RATIO_BINS];
+  uint64_t ulp_hist[ORC_ULP_BINS];
+} orc_np;
+
+/* Rounds a finite binary64 value to binary16 (nearest, ties to even) and
+ * returns the bit pattern; values beyond the range give +-Inf. */
+uint16_t orc_round_binary16(double v);
+
+void orc_nearpass(int32_t dtype, const void *cand, const void *ref, int64_t n, double atol,
+                  double rtol, orc_np *out);
+
 /* Suite verdict over n_cases x n_tols mismatch counts (case-major).
  * status[c] < 0 marks a case that could not be evaluated (it fails).
  * flags[c] (nullable) are the detector flags; certification requires 0.

@@ -637,7 +637,102 @@ def pin_tstats_handbuilt(lib):
     assert d["numel"] == 0 and d["argmin"] == -1
 
 
+def _nearpass_expected(cand, ref, dt, atol, rtol) -> dict:
+    """Near-pass statistics from numpy: binary64 arithmetic on numpy / torch
+    decoded values, numpy's float32 -> float16 rounding for the grid, frexp
+    for the bins."""
+    c = lib_decode(cand, dt).reshape(-1)
+    r = lib_decode(ref, dt).reshape(-1)
+    fin = np.isfinite(c) & np.isfinite(r)
+    idx = np.flatnonzero(fin)
+    c, r = c[fin], r[fin]
+    d = np.abs(c - r)
+    t = atol + rtol * np.abs(r)
+    fail = d > t
+    e = {"numel": cand.size, "n_pairs": int(fin.sum()), "n_fail": int(fail.sum()),
+         "n_zero_tol": int(((t == 0) & (d > 0)).sum())}
+    pos = t > 0
+    if pos.any():
+        q = np.zeros_like(d)
+        q[pos] = d[pos] / t[pos]
+        k = int(np.argmax(np.where(pos, q, -1.0)))  # first occurrence
+        e["max_ratio"], e["argmax_ratio"] = float(q[k]), int(idx[k])
+    else:
+        e["max_ratio"], e["argmax_ratio"] = 0.0, -1
+    qf = d[fail & pos] / t[fail & pos]
+    rb = np.minimum(np.frexp(qf)[1] - 1, oracle.RATIO_BINS - 1)
+    e["ratio_hist"] = np.bincount(rb, minlength=oracle.RATIO_BINS).tolist()
+    if dt == F32:
+        with np.errstate(over="ignore"):
+            gc = c.astype(np.float32).astype(np.float16).view(np.uint16).astype(np.int64)
+            gr = r.astype(np.float32).astype(np.float16).view(np.uint16).astype(np.int64)
+        mask = 0x7C00
+    else:
+        gc = cand.reshape(-1)[fin].astype(np.int64)
+        gr = ref.reshape(-1)[fin].astype(np.int64)
+        mask = 0x7C00 if dt == F16 else 0x7F80
+    inside = ((gc & mask) != mask) & ((gr & mask) != mask)
+    key = lambda h: np.where(h & 0x8000, -(h & 0x7FFF), h & 0x7FFF)
+    dist = np.abs(key(gc) - key(gr))
+    bins = np.where(dist == 0, 0, np.frexp(dist.astype(np.float64))[1])
+    bins = np.where(inside, bins, oracle.ULP_BINS - 1)
+    e["ulp_hist"] = np.bincount(bins, minlength=oracle.ULP_BINS).tolist()
+    df = np.where(inside, dist, 0xFFFFFFFF)[fail]
+    e["max_ulp_fail"] = int(df.max()) if df.size else 0
+    return e
+
+
+def _check_nearpass(got, e):
+    for k in ("numel", "n_pairs", "n_fail", "n_zero_tol", "argmax_ratio", "ratio_hist",
+              "ulp_hist", "max_ulp_fail"):
+        assert got[k] == e[k], (k, got[k], e[k])
+    assert np.float64(got["max_ratio"]).tobytes() == np.float64(e["max_ratio"]).tobytes()
+
+
+def pin_nearpass_numpy(lib):
+    """Near-pass statistics of random pairs of every class and storage type,
+    at several tolerances, against numpy."""
+    rng = np.random.default_rng(26082)
+    for dt in (F32, F16, BF16):
+        for n in (0, 1, 5, 3000):
+            cand, ref = random_pairs(rng, n, dt)
+            for atol, rtol in ((1e-3, 1e-3), (0.0, 1e-2), (0.0, 0.0), (1e-5, 0.0)):
+                got = oracle.nearpass(as_storage(cand, dt), as_storage(ref, dt), dt, atol, rtol,
+                                      lib=lib)
+                _check_nearpass(got, _nearpass_expected(cand, ref, dt, atol, rtol))
+
+
+def pin_nearpass_handbuilt(lib):
+    """Literal near-pass statistics: one binary16 step apart (the fp16
+    ceiling), a zero tolerance, values beyond the binary16 range, and the
+    binary16 rounding routine at its boundaries."""
+    one_up = np.array([1.0 + 2.0 ** -10, 1.0], dtype=np.float16).view(np.uint16)
+    d = oracle.nearpass(one_up[:1], one_up[1:], F16, 1e-4, 1e-4, lib=lib)
+    # d = 2^-10, t = 2e-4: ratio 4.8828125 (bin 2), one grid step
+    assert (d["n_fail"], d["max_ulp_fail"], d["argmax_ratio"]) == (1, 1, 0)
+    assert d["max_ratio"] == 2.0 ** -10 / (1e-4 + 1e-4 * 1.0)
+    assert d["ratio_hist"][2] == 1 and sum(d["ratio_hist"]) == 1 and d["ulp_hist"][1] == 1
+    x = np.array([1e5, 1.0, 3.0], dtype=np.float32)
+    y = np.array([1e5 + 8, 1.0, 3.0], dtype=np.float32)
+    d = oracle.nearpass(x, y, F32, 0.0, 0.0, lib=lib)
+    assert (d["n_fail"], d["n_zero_tol"], d["max_ulp_fail"]) == (1, 1, 0xFFFFFFFF)
+    # t == 0 everywhere: no finite violation ratio
+    assert d["ulp_hist"][0] == 2 and d["ulp_hist"][17] == 1
+    assert (d["argmax_ratio"], d["max_ratio"]) == (-1, 0.0)
+    # -0 and +0 are the same grid value; NaN / Inf pairs are left out
+    z = np.array([-0.0, np.nan, np.inf], dtype=np.float32)
+    w = np.array([0.0, 1.0, np.inf], dtype=np.float32)
+    d = oracle.nearpass(z, w, F32, 1e-3, 1e-3, lib=lib)
+    assert (d["n_pairs"], d["n_fail"], d["ulp_hist"][0]) == (1, 0, 1)
+    # binary16 rounding: ties to even, the last finite value, the overflow threshold
+    for v, h in ((1.0 + 2.0 ** -11, 0x3C00), (1.0 + 3 * 2.0 ** -11, 0x3C02), (65504.0, 0x7BFF),
+                 (65519.99, 0x7BFF), (65520.0, 0x7C00), (2.0 ** -25, 0x0000),
+                 (3 * 2.0 ** -25, 0x0002), (-2.0 ** -24, 0x8001)):
+        assert lib.orc_round_binary16(v) == h, (v, hex(lib.orc_round_binary16(v)))
+
+
 PINS = [
+    pin_nearpass_handbuilt, pin_nearpass_numpy,
     pin_tstats_handbuilt, pin_tstats_numpy,
     pin_gate_ties, pin_suite_handbuilt, pin_flags_handbuilt, pin_decode, pin_no_fma,
     pin_metrics_numpy, pin_gate_isclose, pin_localize_numpy, pin_invariants, pin_integrity_counts,

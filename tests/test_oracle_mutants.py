@@ -63,6 +63,12 @@ MUTANTS = [
      "if (ok) certified += 1;"),
     ("suite_ignores_status", "const int ok = status[c] >= 0 &&", "const int ok ="),
     ("tstats_argmin_last_tie", "v < out->min", "v <= out->min"),
+    ("np_ratio_last_tie", "q > out->max_ratio", "q >= out->max_ratio"),
+    ("np_fail_ge", "const int fail = d > t;", "const int fail = d >= t;"),
+    ("np_round_ties_up", "(frac == 0.5 && fmod(kr, 2.0) != 0.0)", "(frac == 0.5)"),
+    ("np_key_unsigned", "return (h & 0x8000u) ? -mag : mag;", "return h;"),
+    ("np_ratio_bin_off", "const int b = p - 1 > ORC_RATIO_BINS - 1 ? ORC_RATIO_BINS - 1 : p - 1;",
+     "const int b = p > ORC_RATIO_BINS - 1 ? ORC_RATIO_BINS - 1 : p;"),
     ("tstats_zero_in_hist", "if (v != 0.0) out->hist[hist_bin(v)]++;", "out->hist[hist_bin(v)]++;"),
     ("tstats_bin_off_by_one", "const int b = (p - 1) - ORC_HIST_EMIN + 1;",
      "const int b = p - ORC_HIST_EMIN + 1;"),
