@@ -287,11 +287,63 @@ vc_status vcheck_tensor_stats(const vc_tensor *tensors, int32_t n_tensors, vc_ts
 vc_status vcheck_tensor_stats_workspace(const vc_tensor *tensors, int32_t n_tensors,
                                         size_t *bytes);
 
+/* ---- near-pass statistics -------------------------------------------------
+ *
+ * Evidence for the near-pass and fp16-ceiling rules of the adaptive
+ * scheduling (Sec. 4.4) and for precision failures such as Table 1's (a
+ * binary32 accumulation against a reference that rounds to binary16 at every
+ * step): how far the failing elements are from the tolerance, and how many
+ * grid steps apart the two outputs are. Per case, at one tolerance pair,
+ * over the elements where cand and ref are both finite, with d = |c - r|
+ * and t = atol + rtol*|r| in binary64 (each operation rounded):
+ *   n_pairs       such elements; n_fail those with d > t;
+ *   n_zero_tol    elements with t == 0 and d > 0 (unbounded ratio);
+ *   max_ratio     largest binary64 d / t over elements with t > 0, at the
+ *                 first flat index argmax_ratio (0 and -1 when none);
+ *   ratio_hist[b] failing elements with t > 0 and floor(log2(d / t)) = b
+ *                 (the last bin: b >= 31);
+ *   ulp_hist[b]   elements by their distance on the grid: binary16 for
+ *                 binary32 and binary16 storage, bfloat16 for bfloat16
+ *                 storage (both values rounded to the grid, nearest, ties to
+ *                 even; -0 and +0 are one grid value); bin 0 distance 0, bin
+ *                 b in 1..16 distances in [2^(b-1), 2^b), bin 17 elements
+ *                 with a value beyond the grid's finite range;
+ *   max_ulp_fail  largest grid distance among failing elements (0 if none,
+ *                 0xffffffff when one lies beyond the grid's range).
+ * A case fails only within one grid step (the fp16 ceiling) when
+ * n_fail > 0 and max_ulp_fail <= 1 and no non-finite element mismatches. */
+#define VC_RATIO_BINS 32
+#define VC_ULP_BINS 18
+
+typedef struct vc_nearpass {
+  uint64_t numel, n_pairs, n_fail, n_zero_tol;
+  double max_ratio;
+  int64_t argmax_ratio;
+  uint32_t max_ulp_fail, reserved;
+  uint64_t ratio_hist[VC_RATIO_BINS];
+  uint64_t ulp_hist[VC_ULP_BINS];
+} vc_nearpass;
+
+/* Near-pass statistics of cases[0 .. n_cases) at tolerance `tol` (its
+ * equal_nan is ignored: only finite pairs count) into out[0 .. n_cases)
+ * (device vc_nearpass, in case order); inputs are not read. Workspace:
+ * vcheck_nearpass_workspace. Errors: VC_ERR_NULL, VC_ERR_DTYPE and
+ * VC_ERR_SHAPE (also for a case whose cand and ref differ in dtype or
+ * shape), VC_ERR_ALIGN, VC_ERR_TOL, VC_ERR_LIMIT (n_cases outside
+ * 0 .. 2^20, or a case of 2^31 elements or more), VC_ERR_WORKSPACE,
+ * VC_ERR_HIP. n_cases = 0 enqueues nothing. */
+vc_status vcheck_nearpass(const vc_case *cases, int32_t n_cases, const vc_tol *tol,
+                          vc_nearpass *out, void *workspace, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for vcheck_nearpass over the same cases. */
+vc_status vcheck_nearpass_workspace(const vc_case *cases, int32_t n_cases, size_t *bytes);
+
 /* Profiling hook (tracing): the next vcheck_compare / _localize / _integrity /
- * _sweep / _tensor_stats call made on this thread records `begin_event` on
- * its stream just before its first streaming-kernel launch and `end_event`
- * just after its last one, so hipEventElapsedTime gives the duration of the
- * streaming kernels alone (without the prologue and the merge kernels). Both are
+ * _sweep / _tensor_stats / _nearpass call made on this thread records
+ * `begin_event` on its stream just before its first streaming-kernel launch
+ * and `end_event` just after its last one, so hipEventElapsedTime gives the
+ * duration of the streaming kernels alone (without the prologue and the
+ * merge kernels). Both are
  * hipEvent_t handles created by the caller; the hook is consumed by that one
  * call. Pass NULL, NULL to clear it. Returns VC_OK, or VC_ERR_NULL when only
  * one of the two is NULL. */

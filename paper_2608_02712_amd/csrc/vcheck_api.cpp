@@ -646,6 +646,70 @@ vc_status make_probe_plan(const vc_tensor *tensors, int32_t n, ProbePlan &plan) 
   return VC_OK;
 }
 
+// ---- near-pass statistics -------------------------------------------------
+
+struct NpPlan {
+  std::vector<vck::NpCase> cases;
+  std::vector<uint64_t> chunk_first, group_first;
+  uint32_t unit = 1024;
+  uint64_t total_chunks = 0, total_groups = 0;
+  size_t off_recs = 0, off_grecs = 0, blob_bytes = 0, bytes = 0;
+};
+
+vc_status make_np_plan(const vc_case *cases, int32_t n, NpPlan &plan) {
+  if (n < 0 || n > (1 << 20)) return fail(VC_ERR_LIMIT, "n_cases %d outside 0..2^20", n);
+  if (n > 0 && cases == nullptr) return fail(VC_ERR_NULL, "cases is NULL");
+  uint64_t total = 0, largest = 0;
+  char what[48];
+  for (int32_t i = 0; i < n; ++i) {
+    const vc_case &c = cases[i];
+    if (tensor_status(&c.cand) != VC_OK) {
+      snprintf(what, sizeof what, "case %d cand", i);
+      return check_tensor(&c.cand, what);
+    }
+    if (tensor_status(&c.ref) != VC_OK) {
+      snprintf(what, sizeof what, "case %d ref", i);
+      return check_tensor(&c.ref, what);
+    }
+    if (c.cand.dtype != c.ref.dtype)
+      return fail(VC_ERR_DTYPE, "case %d: cand and ref dtypes differ", i);
+    if (!same_shape(c.cand, c.ref))
+      return fail(VC_ERR_SHAPE, "case %d: cand and ref shapes differ", i);
+    const uint64_t m = (uint64_t)numel_of(c.ref);
+    if (m >= (1ull << 31)) return fail(VC_ERR_LIMIT, "case %d has 2^31 elements or more", i);
+    total += m;
+    largest = std::max(largest, m);
+  }
+  plan.unit = probe_unit(total, largest);
+  const uint64_t ch = 4ull * plan.unit;
+  plan.cases.resize(n);
+  plan.chunk_first.resize(n);
+  plan.group_first.resize(n);
+  for (int32_t i = 0; i < n; ++i) {
+    vck::NpCase &d = plan.cases[i];
+    memset(&d, 0, sizeof d);
+    d.cand = (const uint8_t *)cases[i].cand.data;
+    d.ref = (const uint8_t *)cases[i].ref.data;
+    d.numel = (uint64_t)numel_of(cases[i].ref);
+    d.dtype = cases[i].ref.dtype;
+    d.chunk_begin = plan.total_chunks;
+    const uint64_t nc = std::max<uint64_t>(1, (d.numel + ch - 1) / ch);
+    d.n_chunks = (uint32_t)nc;
+    plan.chunk_first[i] = plan.total_chunks;
+    plan.group_first[i] = plan.total_groups;
+    plan.total_chunks += nc;
+    plan.total_groups += (nc + vck::kProbeGroupChunks - 1) / vck::kProbeGroupChunks;
+  }
+  plan.blob_bytes = (sizeof(vck::NpCase) + 2 * sizeof(uint64_t)) * (size_t)n;
+  size_t off = align_up(plan.blob_bytes);
+  plan.off_recs = off;
+  off += align_up(sizeof(vck::NpRec) * (size_t)plan.total_chunks);
+  plan.off_grecs = off;
+  off += align_up(sizeof(vck::NpRec) * (size_t)plan.total_groups);
+  plan.bytes = off + kAlign;
+  return VC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -866,6 +930,71 @@ vc_status vcheck_tensor_stats(const vc_tensor *tensors, int32_t n_tensors, vc_ts
     st = hip_check(vck::launch_probe(P, plan.total_chunks, plan.total_groups, stream,
                                      prof_begin, prof_end),
                    "probe launch");
+  // the staging slot is reused once the prologue has read it
+  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
+  if (se == VC_OK) slot->pending = true;
+  return st != VC_OK ? st : se;
+}
+
+vc_status vcheck_nearpass_workspace(const vc_case *cases, int32_t n_cases, size_t *bytes) {
+  g_last_error.clear();
+  if (bytes == nullptr) return fail(VC_ERR_NULL, "bytes is NULL");
+  NpPlan plan;
+  const vc_status st = make_np_plan(cases, n_cases, plan);
+  if (st != VC_OK) return st;
+  *bytes = plan.bytes;
+  return VC_OK;
+}
+
+vc_status vcheck_nearpass(const vc_case *cases, int32_t n_cases, const vc_tol *tol,
+                          vc_nearpass *out, void *ws, size_t ws_bytes, void *stream_) {
+  g_last_error.clear();
+  NpPlan plan;
+  vc_status st = make_np_plan(cases, n_cases, plan);
+  if (st != VC_OK) return st;
+  st = check_tols(tol, 1);
+  if (st != VC_OK) return st;
+  if (n_cases == 0) return VC_OK;
+  if (out == nullptr) return fail(VC_ERR_NULL, "out is NULL");
+  if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < plan.bytes)
+    return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
+  const hipStream_t stream = (hipStream_t)stream_;
+  uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
+  const size_t n = (size_t)n_cases;
+  std::vector<uint8_t> blob(plan.blob_bytes);
+  memcpy(blob.data(), plan.cases.data(), sizeof(vck::NpCase) * n);
+  memcpy(blob.data() + sizeof(vck::NpCase) * n, plan.chunk_first.data(), 8 * n);
+  memcpy(blob.data() + (sizeof(vck::NpCase) + 8) * n, plan.group_first.data(), 8 * n);
+  std::unique_lock<std::mutex> lock;
+  Slot *slot = nullptr;
+  st = stage_blob(blob.data(), blob.size(), lock, slot);
+  if (st != VC_OK) return st;
+  vck::Prologue Q;
+  memset(&Q, 0, sizeof Q);
+  Q.blob_src = (const uint8_t *)slot->dev;
+  Q.blob_dst = base;
+  Q.blob_bytes = plan.blob_bytes;
+  Q.n_cases = 1;  // (no suite rates to clear)
+  vck::NpParams P;
+  memset(&P, 0, sizeof P);
+  P.cases = (const vck::NpCase *)base;
+  P.chunk_first = (const uint64_t *)(base + sizeof(vck::NpCase) * n);
+  P.group_first = (const uint64_t *)(base + (sizeof(vck::NpCase) + 8) * n);
+  P.n_cases = n_cases;
+  P.unit = plan.unit;
+  P.atol = tol->atol;
+  P.rtol = tol->rtol;
+  P.recs = (vck::NpRec *)(base + plan.off_recs);
+  P.grecs = (vck::NpRec *)(base + plan.off_grecs);
+  P.out = out;
+  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
+  g_prof_begin = g_prof_end = nullptr;
+  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  if (st == VC_OK)
+    st = hip_check(vck::launch_nearpass(P, plan.total_chunks, plan.total_groups, stream,
+                                        prof_begin, prof_end),
+                   "near-pass launch");
   // the staging slot is reused once the prologue has read it
   const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
   if (se == VC_OK) slot->pending = true;

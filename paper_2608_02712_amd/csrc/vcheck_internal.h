@@ -200,6 +200,51 @@ struct ProbeParams {
   vc_tstats *out;                // [n]
 };
 
+// ---- near-pass statistics (vcheck_probe.hip) -------------------------------
+
+constexpr int kRatioBins = 32;
+constexpr int kUlpBins = 18;
+
+// One case of the near-pass statistics (48 bytes); chunks and groups as for
+// the probe.
+struct NpCase {
+  const uint8_t *cand;
+  const uint8_t *ref;
+  uint64_t numel;
+  uint64_t chunk_begin;
+  uint32_t n_chunks;
+  int32_t dtype;
+  uint64_t pad;
+};
+static_assert(sizeof(NpCase) == 48, "NpCase layout");
+
+struct NpRec {
+  uint64_t n_pairs, n_fail, n_zero_tol;
+  double max_ratio;
+  int64_t argmax_ratio;  // index within the case; -1 when none
+  uint32_t max_ulp_fail, pad0;
+  uint32_t ratio_hist[kRatioBins];
+  uint32_t ulp_hist[kUlpBins];
+  uint32_t pad1[2];
+};
+static_assert(sizeof(NpRec) == 256, "NpRec layout");
+static_assert(sizeof(vc_nearpass) == 56 + 8 * (kRatioBins + kUlpBins), "vc_nearpass layout");
+
+struct NpParams {
+  const NpCase *cases;
+  const uint64_t *chunk_first;
+  const uint64_t *group_first;
+  int32_t n_cases;
+  uint32_t unit;
+  double atol, rtol;
+  NpRec *recs;
+  NpRec *grecs;
+  vc_nearpass *out;
+};
+
+hipError_t launch_nearpass(const NpParams &p, uint64_t n_chunks, uint64_t n_groups,
+                           hipStream_t s, hipEvent_t begin, hipEvent_t end);
+
 // Launches the probe's streaming and merge kernels; `begin` / `end`
 // (nullable) are recorded around the streaming kernel.
 hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_groups,

@@ -1,4 +1,5 @@
-// vcheck_probe.hip -- gfx950 kernels of the tensor-statistics probe.
+// vcheck_probe.hip -- gfx950 kernels of the diagnostic statistics: the
+// tensor-statistics probe and the near-pass statistics.
 //
 // The diagnostic instrumentation of the repair loop records multi-level
 // tensor statistics at pipeline boundaries (Sec. 4.2; the instrumentation
@@ -382,7 +383,304 @@ __global__ __launch_bounds__(kPThreads) void probe_final_kernel(const ProbeParam
   write_out(P.out + ti, T, r, h);
 }
 
+// ---------------------------------------------------------------- near-pass
+//
+// Per case: finite pairs, failures, zero-tolerance violations, the largest
+// violation ratio d / t with its first index, and histograms of the ratio's
+// binary exponent (failures) and of the distance on the binary16 / bfloat16
+// grid. Same decomposition as the probe: one block per chunk, each wave one
+// contiguous quarter; chunk records merged per group of 256, then per case.
+// The largest ratio is tracked per lane under a wave-uniform threshold (the
+// wave's best so far): an element becomes a candidate only when its exact
+// ratio beats the threshold (fma(-T, t, d) > 0, whose sign is exact), so the
+// binary64 division runs for candidates and failing elements only.
+
+constexpr int kNpRowWords = 15;  // 52 8-bit counters (50 used) and a pad word: an odd stride
+
+struct NpLds {
+  union {
+    uint32_t hist[kPWaves * 64 * kNpRowWords];
+    struct {
+      uint64_t c[3][kPThreads];
+      double mv[kPThreads];
+      int64_t mi[kPThreads];
+      uint32_t mu[kPThreads];
+    };
+  };
+  uint32_t item;
+};
+
+__device__ __forceinline__ void np_pick(double &v, int64_t &i, double v2, int64_t i2) {
+  if (i2 < 0) return;
+  if (i < 0 || v2 > v || (v2 == v && i2 < i)) {
+    v = v2;
+    i = i2;
+  }
+}
+
+// Fixed-order reduction of the partials in s into r (valid in thread 0).
+__device__ void np_reduce(NpLds &s, NpRec &r) {
+  const uint32_t t = threadIdx.x;
+  for (uint32_t w = kPThreads / 2; w >= 1; w >>= 1) {
+    __syncthreads();
+    if (t < w) {
+#pragma unroll
+      for (int f = 0; f < 3; ++f) s.c[f][t] += s.c[f][t + w];
+      np_pick(s.mv[t], s.mi[t], s.mv[t + w], s.mi[t + w]);
+      s.mu[t] = max(s.mu[t], s.mu[t + w]);
+    }
+  }
+  __syncthreads();
+  if (t == 0) {
+    r.n_pairs = s.c[0][0];
+    r.n_fail = s.c[1][0];
+    r.n_zero_tol = s.c[2][0];
+    r.argmax_ratio = s.mi[0];
+    r.max_ratio = s.mi[0] < 0 ? 0.0 : s.mv[0];
+    r.max_ulp_fail = s.mu[0];
+  }
+}
+
+// Grid pattern of element j: binary16 rounding of a binary32 value, the
+// stored pattern for 16-bit storage.
+template <int DT>
+__device__ __forceinline__ uint32_t grid_bits(const p32x4 &q, int j) {
+  if constexpr (DT == VC_F32) {
+    const _Float16 h = (_Float16)__uint_as_float(q[j]);  // nearest, ties to even
+    return (uint32_t)__builtin_bit_cast(uint16_t, h);
+  } else {
+    const uint32_t w = q[j >> 1];
+    return (j & 1) ? (w >> 16) : (w & 0xffffu);
+  }
+}
+
+template <int DT>
+__device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, uint32_t U,
+                         double atol, double rtol, NpRec *rec) {
+  constexpr int V = DT == VC_F32 ? 4 : 8;
+  constexpr int ES = DT == VC_F32 ? 4 : 2;
+  constexpr uint32_t ITER = 64 * V;
+  constexpr uint32_t kExpMask = DT == VC_BF16 ? 0x7f80u : 0x7c00u;
+  const uint32_t t = threadIdx.x, lane = t & 63u;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  uint32_t *const row = s.hist + t * kNpRowWords;
+  for (int w = 0; w < kNpRowWords; ++w) row[w] = 0;
+  const uint64_t w0 = min(c0 + (uint64_t)wave * U, c1), w1 = min(w0 + U, c1);
+  const bool vec = ((uintptr_t)C.cand % 16) == 0 && ((uintptr_t)C.ref % 16) == 0;
+  uint32_t n_pairs = 0, n_fail = 0, n_zt = 0, mu = 0;
+  double lb = -1.0, T = -1.0;  // lane best ratio, wave threshold (-1: none)
+  uint32_t li = 0xffffffffu;
+  for (uint64_t b = w0; b < w1; b += ITER) {
+    const uint64_t i0 = b + (uint64_t)lane * V;
+    const bool full = vec && b + ITER <= w1;
+    const p32x4 cq = full ? pload16(C.cand + i0 * ES) : pload_guarded<DT>(C.cand, i0, w1);
+    const p32x4 rq = full ? pload16(C.ref + i0 * ES) : pload_guarded<DT>(C.ref, i0, w1);
+    const uint32_t o0 = (uint32_t)(i0 - c0);
+    bool cand_any = false;
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const float cf = pdec<DT>(cq, j), rf = pdec<DT>(rq, j);
+      const bool fin = i0 + j < w1 && __builtin_fabsf(cf) <= 3.40282347e38f &&
+                       __builtin_fabsf(rf) <= 3.40282347e38f;
+      if (!fin) continue;
+      ++n_pairs;
+      const double r = (double)rf;
+      const double d = __builtin_fabs((double)cf - r);
+      const double tt = atol + rtol * __builtin_fabs(r);
+      const bool fail = d > tt;
+      n_fail += fail ? 1u : 0u;
+      if (tt == 0.0) {
+        n_zt += d > 0.0 ? 1u : 0u;
+      } else if (fail || T < 0.0 || __builtin_fma(-T, tt, d) > 0.0) {
+        const double qr = d / tt;
+        if (qr > lb || li == 0xffffffffu) {
+          lb = qr;
+          li = o0 + (uint32_t)j;
+          cand_any = true;
+        }
+        if (fail) {
+          const int e = (int)((__double_as_longlong(qr) >> 52) & 0x7ff) - 1023;  // qr >= 1
+          const int bin = min(e, kRatioBins - 1);
+          atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+        }
+      }
+      const uint32_t hc = grid_bits<DT>(cq, j), hr = grid_bits<DT>(rq, j);
+      const bool inside = (hc & kExpMask) != kExpMask && (hr & kExpMask) != kExpMask;
+      const int kc = (hc & 0x8000u) ? -(int)(hc & 0x7fffu) : (int)(hc & 0x7fffu);
+      const int kr = (hr & 0x8000u) ? -(int)(hr & 0x7fffu) : (int)(hr & 0x7fffu);
+      const uint32_t dist = (uint32_t)abs(kc - kr);
+      const int ub = inside ? (dist == 0 ? 0 : 32 - __builtin_clz(dist)) : kUlpBins - 1;
+      const int ubin = kRatioBins + ub;
+      atomicAdd(row + (ubin >> 2), 1u << ((ubin & 3) * 8));
+      if (fail) mu = max(mu, inside ? dist : 0xffffffffu);
+    }
+    if (__ballot(cand_any) != 0) {  // raise the wave threshold
+      double v = li == 0xffffffffu ? -1.0 : lb;
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) v = max(v, __shfl_xor(v, m));
+      T = v;
+    }
+  }
+  // histograms: thread t sums bin t % 64 (52 used) over the rows of lanes
+  // (t / 64) * 64 .. + 63, then the four partial sums in order
+  __syncthreads();
+  const uint32_t bin = t & 63u, part = t >> 6;
+  uint32_t h = 0;
+  if (bin < (uint32_t)(kRatioBins + kUlpBins))
+    for (uint32_t l = part * 64; l < part * 64 + 64; ++l)
+      h += (s.hist[l * kNpRowWords + (bin >> 2)] >> ((bin & 3) * 8)) & 0xffu;
+  __syncthreads();
+  s.c[0][t] = h;
+  __syncthreads();
+  if (t < (uint32_t)(kRatioBins + kUlpBins)) {
+    const uint32_t tot =
+        (uint32_t)(s.c[0][t] + s.c[0][t + 64] + s.c[0][t + 128] + s.c[0][t + 192]);
+    if (t < (uint32_t)kRatioBins) rec->ratio_hist[t] = tot;
+    else rec->ulp_hist[t - kRatioBins] = tot;
+  }
+  __syncthreads();
+  s.c[0][t] = n_pairs;
+  s.c[1][t] = n_fail;
+  s.c[2][t] = n_zt;
+  s.mv[t] = lb;
+  s.mi[t] = li == 0xffffffffu ? -1 : (int64_t)(c0 + li);
+  s.mu[t] = mu;
+  NpRec r;
+  np_reduce(s, r);
+  if (t == 0) {
+    rec->n_pairs = r.n_pairs;
+    rec->n_fail = r.n_fail;
+    rec->n_zero_tol = r.n_zero_tol;
+    rec->max_ratio = r.max_ratio;
+    rec->argmax_ratio = r.argmax_ratio;
+    rec->max_ulp_fail = r.max_ulp_fail;
+    rec->pad0 = 0;
+  }
+}
+
+__global__ __launch_bounds__(kPThreads) void nearpass_kernel(const NpParams P) {
+  __shared__ NpLds s;
+  const uint64_t chunk = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const uint32_t ci = find_first(P.chunk_first, (uint32_t)P.n_cases, chunk);
+    if (threadIdx.x == 0) s.item = ci;
+  }
+  __syncthreads();
+  const NpCase C = P.cases[s.item];
+  const uint64_t CH = 4ull * P.unit;
+  const uint64_t c0 = (chunk - C.chunk_begin) * CH;
+  const uint64_t c1 = max(c0, min(c0 + CH, C.numel));
+  NpRec *const rec = P.recs + chunk;
+  switch (C.dtype) {
+    case VC_F32: np_chunk<VC_F32>(s, C, c0, c1, P.unit, P.atol, P.rtol, rec); break;
+    case VC_F16: np_chunk<VC_F16>(s, C, c0, c1, P.unit, P.atol, P.rtol, rec); break;
+    default: np_chunk<VC_BF16>(s, C, c0, c1, P.unit, P.atol, P.rtol, rec); break;
+  }
+}
+
+// Merges records recs[0 .. n) (n <= 256) in a fixed order: totals in r
+// (thread 0), histogram bin t (t < 50) in hist.
+__device__ void np_merge(NpLds &s, const NpRec *recs, uint32_t n, NpRec &r, uint64_t &hist) {
+  const uint32_t t = threadIdx.x;
+  const bool has = t < n;
+  const NpRec *const x = recs + (has ? t : 0);
+  s.c[0][t] = has ? x->n_pairs : 0;
+  s.c[1][t] = has ? x->n_fail : 0;
+  s.c[2][t] = has ? x->n_zero_tol : 0;
+  s.mv[t] = has ? x->max_ratio : 0.0;
+  s.mi[t] = has ? x->argmax_ratio : -1;
+  s.mu[t] = has ? x->max_ulp_fail : 0u;
+  np_reduce(s, r);
+  const uint32_t bin = t & 63u, part = t >> 6;
+  uint64_t h = 0;
+  if (bin < (uint32_t)(kRatioBins + kUlpBins))
+    for (uint32_t i = part; i < n; i += 4)
+      h += bin < (uint32_t)kRatioBins ? recs[i].ratio_hist[bin] : recs[i].ulp_hist[bin - kRatioBins];
+  __syncthreads();
+  s.c[0][t] = h;
+  __syncthreads();
+  hist = t < 64 ? s.c[0][t] + s.c[0][t + 64] + s.c[0][t + 128] + s.c[0][t + 192] : 0;
+}
+
+__device__ void np_write(vc_nearpass *o, const NpCase &C, const NpRec &r, uint64_t h) {
+  const uint32_t t = threadIdx.x;
+  if (t < (uint32_t)kRatioBins) o->ratio_hist[t] = h;
+  else if (t < (uint32_t)(kRatioBins + kUlpBins)) o->ulp_hist[t - kRatioBins] = h;
+  if (t == 0) {
+    o->numel = C.numel;
+    o->n_pairs = r.n_pairs;
+    o->n_fail = r.n_fail;
+    o->n_zero_tol = r.n_zero_tol;
+    o->max_ratio = r.max_ratio;
+    o->argmax_ratio = r.argmax_ratio;
+    o->max_ulp_fail = r.max_ulp_fail;
+    o->reserved = 0;
+  }
+}
+
+__global__ __launch_bounds__(kPThreads) void nearpass_merge_kernel(const NpParams P) {
+  __shared__ NpLds s;
+  const uint64_t g = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const uint32_t ci = find_first(P.group_first, (uint32_t)P.n_cases, g);
+    if (threadIdx.x == 0) s.item = ci;
+  }
+  __syncthreads();
+  const uint32_t ci = s.item;
+  const NpCase C = P.cases[ci];
+  const uint64_t first = C.chunk_begin + (g - P.group_first[ci]) * kProbeGroupChunks;
+  const uint32_t n = (uint32_t)min((uint64_t)kProbeGroupChunks,
+                                   C.chunk_begin + C.n_chunks - first);
+  NpRec r;
+  uint64_t h;
+  np_merge(s, P.recs + first, n, r, h);
+  if (C.n_chunks <= kProbeGroupChunks) {
+    np_write(P.out + ci, C, r, h);
+    return;
+  }
+  NpRec *const gr = P.grecs + g;
+  if (threadIdx.x < (uint32_t)kRatioBins) gr->ratio_hist[threadIdx.x] = (uint32_t)h;
+  else if (threadIdx.x < (uint32_t)(kRatioBins + kUlpBins))
+    gr->ulp_hist[threadIdx.x - kRatioBins] = (uint32_t)h;
+  if (threadIdx.x == 0) {
+    gr->n_pairs = r.n_pairs;
+    gr->n_fail = r.n_fail;
+    gr->n_zero_tol = r.n_zero_tol;
+    gr->max_ratio = r.max_ratio;
+    gr->argmax_ratio = r.argmax_ratio;
+    gr->max_ulp_fail = r.max_ulp_fail;
+    gr->pad0 = 0;
+  }
+}
+
+__global__ __launch_bounds__(kPThreads) void nearpass_final_kernel(const NpParams P) {
+  __shared__ NpLds s;
+  const uint32_t ci = blockIdx.x;
+  const NpCase C = P.cases[ci];
+  if (C.n_chunks <= kProbeGroupChunks) return;
+  const uint32_t n_groups = (C.n_chunks + kProbeGroupChunks - 1) / kProbeGroupChunks;
+  NpRec r;
+  uint64_t h;
+  np_merge(s, P.grecs + P.group_first[ci], n_groups, r, h);
+  np_write(P.out + ci, C, r, h);
+}
+
 }  // namespace
+
+hipError_t launch_nearpass(const NpParams &p, uint64_t n_chunks, uint64_t n_groups,
+                           hipStream_t s, hipEvent_t begin, hipEvent_t end) {
+  hipError_t e;
+  if (begin != nullptr && (e = hipEventRecord(begin, s)) != hipSuccess) return e;
+  hipLaunchKernelGGL(nearpass_kernel, dim3((uint32_t)n_chunks), dim3(kPThreads), 0, s, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (end != nullptr && (e = hipEventRecord(end, s)) != hipSuccess) return e;
+  hipLaunchKernelGGL(nearpass_merge_kernel, dim3((uint32_t)n_groups), dim3(kPThreads), 0, s, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(nearpass_final_kernel, dim3((uint32_t)p.n_cases), dim3(kPThreads), 0, s, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_groups,
                         hipStream_t s, hipEvent_t begin, hipEvent_t end) {

@@ -95,6 +95,14 @@ TSTATS_DTYPE = np.dtype([
 ])
 assert TSTATS_DTYPE.itemsize == 608
 
+RATIO_BINS, ULP_BINS = 32, 18
+NEARPASS_DTYPE = np.dtype([
+    ("numel", "<u8"), ("n_pairs", "<u8"), ("n_fail", "<u8"), ("n_zero_tol", "<u8"),
+    ("max_ratio", "<f8"), ("argmax_ratio", "<i8"), ("max_ulp_fail", "<u4"), ("reserved", "<u4"),
+    ("ratio_hist", "<u8", (RATIO_BINS,)), ("ulp_hist", "<u8", (ULP_BINS,)),
+])
+assert NEARPASS_DTYPE.itemsize == 456
+
 _LIB = None
 
 
@@ -135,9 +143,14 @@ def lib() -> ctypes.CDLL:
                                       ctypes.c_size_t, P]
     L.vcheck_tensor_stats_workspace.argtypes = [ctypes.POINTER(VcTensor), ctypes.c_int32,
                                                 ctypes.POINTER(ctypes.c_size_t)]
+    L.vcheck_nearpass.argtypes = [ctypes.POINTER(VcCase), ctypes.c_int32, ctypes.POINTER(VcTol),
+                                  P, P, ctypes.c_size_t, P]
+    L.vcheck_nearpass_workspace.argtypes = [ctypes.POINTER(VcCase), ctypes.c_int32,
+                                            ctypes.POINTER(ctypes.c_size_t)]
     for name in ("vcheck_compare", "vcheck_localize", "vcheck_integrity", "vcheck_sweep",
                  "vcheck_workspace_bytes", "vcheck_tensor_stats",
-                 "vcheck_tensor_stats_workspace"):
+                 "vcheck_tensor_stats_workspace", "vcheck_nearpass",
+                 "vcheck_nearpass_workspace"):
         getattr(L, name).restype = ctypes.c_int32
     if L.vcheck_abi_version() != 1:
         raise RuntimeError("libvcheck.so ABI version mismatch")
@@ -441,4 +454,56 @@ def vcheck_tensor_stats(tensors, stream=None) -> list[dict]:
     if ts.tensors:
         ts.launch(stream)
     return ts.results()
+
+
+class NearPass:
+    """Prepared near-pass statistics over a fixed list of (cand, ref) device
+    tensor pairs at one tolerance pair; launch() enqueues vcheck_nearpass,
+    results() reads one dict per case (plus the derived fp16_ceiling: the
+    case fails, and only within one grid step)."""
+
+    def __init__(self, cases, atol: float, rtol: float):
+        self.cases = [(c, r) for c, r, *_ in cases]
+        n = len(self.cases)
+        self._keep = []
+        arr = (VcCase * max(n, 1))()
+        for i, (c, r) in enumerate(self.cases):
+            arr[i].cand = tensor_desc(c)
+            arr[i].ref = tensor_desc(r)
+            arr[i].inputs = None
+            arr[i].n_inputs = 0
+        self.desc = arr
+        self.tol = _tols([(atol, rtol, 0)])
+        size = ctypes.c_size_t(0)
+        _check(lib().vcheck_nearpass_workspace(self.desc, n, ctypes.byref(size)))
+        dev = self.cases[0][1].device if n else torch.device("cuda")
+        self.ws = _ws(size.value, dev)
+        self.out = torch.zeros(max(n, 1) * NEARPASS_DTYPE.itemsize, dtype=torch.uint8,
+                               device=dev)
+
+    def launch(self, stream=None) -> None:
+        _check(lib().vcheck_nearpass(self.desc, len(self.cases), self.tol, self.out.data_ptr(),
+                                     self.ws.data_ptr(), self.ws.numel(), _stream_ptr(stream)))
+
+    def results(self) -> list[dict]:
+        torch.cuda.synchronize(self.out.device)
+        arr = np.frombuffer(self.out.cpu().numpy().tobytes(), dtype=NEARPASS_DTYPE)
+        res = []
+        for i in range(len(self.cases)):
+            d = {k: arr[k][i].item() for k in NEARPASS_DTYPE.names
+                 if k not in ("ratio_hist", "ulp_hist", "reserved")}
+            d["ratio_hist"] = [int(v) for v in arr["ratio_hist"][i]]
+            d["ulp_hist"] = [int(v) for v in arr["ulp_hist"][i]]
+            d["fp16_ceiling"] = d["n_fail"] > 0 and d["max_ulp_fail"] <= 1
+            res.append(d)
+        return res
+
+
+def vcheck_nearpass(cases, atol: float, rtol: float, stream=None) -> list[dict]:
+    """Near-pass statistics of (cand, ref) device tensor pairs at one
+    tolerance pair (violation ratios and grid distances; see vcheck.h)."""
+    np_ = NearPass(cases, atol, rtol)
+    if np_.cases:
+        np_.launch(stream)
+    return np_.results()
 

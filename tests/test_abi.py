@@ -212,3 +212,32 @@ def test_tensor_stats_host_checks(L):
     # an empty batch enqueues nothing
     assert L.vcheck_tensor_stats(None, 0, None, None, 0, None) == 0
     assert vc.TSTATS_DTYPE.itemsize == 608
+
+
+def test_nearpass_host_checks(L):
+    """The near-pass statistics reject malformed arguments on the host."""
+    def case(c, r):
+        k = vc.VcCase()
+        k.cand, k.ref, k.inputs, k.n_inputs = c, r, None, 0
+        return k
+
+    size = ctypes.c_size_t(0)
+    ok = (vc.VcCase * 2)(case(desc(), desc()), case(desc(vc.VC_F16, (9,)), desc(vc.VC_F16, (9,))))
+    assert L.vcheck_nearpass_workspace(ok, 2, ctypes.byref(size)) == 0 and size.value > 0
+    bad = (vc.VcCase * 1)(case(desc(vc.VC_F16, (9,)), desc(vc.VC_BF16, (9,))))
+    assert L.vcheck_nearpass_workspace(bad, 1, ctypes.byref(size)) == VC_ERR_DTYPE
+    bad = (vc.VcCase * 1)(case(desc(vc.VC_F32, (9,)), desc(vc.VC_F32, (3, 3))))
+    assert L.vcheck_nearpass_workspace(bad, 1, ctypes.byref(size)) == ERR_CODES["VC_ERR_SHAPE"]
+    bad = (vc.VcCase * 1)(case(desc(vc.VC_F32, (9,), data=FAKE + 1), desc(vc.VC_F32, (9,))))
+    assert L.vcheck_nearpass_workspace(bad, 1, ctypes.byref(size)) == VC_ERR_ALIGN
+    assert L.vcheck_nearpass_workspace(ok, -1, ctypes.byref(size)) == VC_ERR_LIMIT
+    assert L.vcheck_nearpass_workspace(None, 1, ctypes.byref(size)) == VC_ERR_NULL
+    t = tol()
+    neg = tol(atol=-1.0)
+    assert L.vcheck_nearpass(ok, 2, ctypes.byref(neg), FAKE, FAKE, 1 << 30, None) == \
+        ERR_CODES["VC_ERR_TOL"]
+    assert L.vcheck_nearpass(ok, 2, None, FAKE, FAKE, 1 << 30, None) == VC_ERR_NULL
+    assert L.vcheck_nearpass(ok, 2, ctypes.byref(t), None, FAKE, 1 << 30, None) == VC_ERR_NULL
+    assert L.vcheck_nearpass(ok, 2, ctypes.byref(t), FAKE, FAKE, 8, None) == VC_ERR_WORKSPACE
+    assert L.vcheck_nearpass(None, 0, ctypes.byref(t), None, None, 0, None) == 0
+    assert vc.NEARPASS_DTYPE.itemsize == 456
