@@ -11,7 +11,8 @@ records around them.
 
 Headline line: the fp16 batch of 64 cases of 2048x2048 (the configuration the
 metric is quoted on). ``probe`` reports the tensor-statistics probe over the
-128 cand and ref tensors of that batch in one call. ``workloads`` holds the same figures for all five
+128 cand and ref tensors of that batch in one call, ``nearpass`` the near-pass
+statistics of its 64 cases. ``workloads`` holds the same figures for all five
 workloads, measured in the same run. ``roofline`` reports the main streaming
 kernel's achieved HBM bandwidth (algorithmic bytes / its event-timed average
 duration) against the 8 TB/s peak; ``cpu_baseline`` times the CPU oracle on a
@@ -206,6 +207,68 @@ def measure_probe(w, steps, warmup, flush):
     return out
 
 
+def measure_nearpass(w, steps, warmup, flush):
+    """Near-pass statistics over every case of workload w at its primary
+    tolerance pair, one call: call time (events around the call, cache
+    flushed before it) and the streaming kernel's time."""
+    import torch
+
+    import oracle
+    import workloads as wl
+    from paper_2608_02712_amd import vcheck as vc
+
+    atol, rtol = w.tols[w.primary][:2]
+    npass = vc.NearPass([(c.cand, c.ref) for c in w.cases], atol, rtol)
+    for _ in range(warmup):
+        npass.launch()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for quad in evs:  # (torch only times events it has seen recorded)
+        for e in quad:
+            e.record(stream)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        flush.fill_(i & 0xFF)
+        evs[i][0].record(stream)
+        npass.launch(stream)
+        evs[i][1].record(stream)
+    for i in range(steps):
+        flush.fill_((i + 1) & 0xFF)
+        vc.vcheck_profile_events(evs[i][2], evs[i][3])
+        npass.launch(stream)
+    torch.cuda.synchronize()
+    call = sorted(a.elapsed_time(b) for a, b, _, _ in evs)[steps // 2]
+    kern = sum(c.elapsed_time(d) for _, _, c, d in evs) / steps
+    nbytes = w.ref_cand_bytes
+    res = npass.results()
+    spent, done = 0.0, 0
+    for case in w.cases:
+        c, r = wl.raw_numpy(case.cand).reshape(-1), wl.raw_numpy(case.ref).reshape(-1)
+        t0 = time.perf_counter()
+        oracle.nearpass(c, r, wl.dtype_code(case.ref.dtype), atol, rtol)
+        spent += time.perf_counter() - t0
+        done += c.nbytes + r.nbytes
+        if spent >= 2.0:
+            break
+    out = {
+        "workload": "near-pass statistics of %s at (%g, %g)" % (w.name, atol, rtol),
+        "n_cases": len(w.cases),
+        "bytes": nbytes,
+        "ms_per_call": round(call, 5),
+        "gbps": round(nbytes / (call * 1e-3) / 1e9, 2),
+        "pct_hbm_peak": round(100.0 * nbytes / (call * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "cases_per_s": round(len(w.cases) / (call * 1e-3), 1),
+        "stream_kernel_ms": round(kern, 5),
+        "stream_kernel_gbps": round(nbytes / (kern * 1e-3) / 1e9, 2),
+        "fp16_ceiling_cases": sum(1 for d in res if d["fp16_ceiling"]),
+        "oracle_one_thread_gbps": round(done / spent / 1e9, 4),
+    }
+    log("near-pass: %.3f ms/call, %.1f GB/s (%.1f%% of peak), streaming kernel %.3f ms" % (
+        call, out["gbps"], out["pct_hbm_peak"], kern))
+    return out
+
+
 def cpu_baseline(w, seconds):
     """The CPU oracle on whole cases of the workload: first one thread until
     the time budget is used (at least one case), then the same cases spread
@@ -305,9 +368,10 @@ def main():
     w, head = measure(first, args.steps, args.warmup, flush)
     results[first] = head
     cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds)
-    probe = None
+    probe = nearpass = None
     if not args.only:
         probe = measure_probe(w, args.steps, args.warmup, flush)
+        nearpass = measure_nearpass(w, args.steps, args.warmup, flush)
     del w
     torch.cuda.empty_cache()
     if not args.headline_only and not args.only:
@@ -346,6 +410,7 @@ def main():
         "cpu_baseline": cpu,
         "workloads": {str(k): v for k, v in sorted(results.items())},
         "probe": probe,
+        "nearpass": nearpass,
     }
     print(json.dumps(line), flush=True)
 
