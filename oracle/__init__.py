@@ -121,6 +121,10 @@ def load(path: str | None = None) -> ctypes.CDLL:
                                  ctypes.c_double, ctypes.POINTER(NearPass)]
     lib.orc_round_binary16.restype = ctypes.c_uint16
     lib.orc_round_binary16.argtypes = [ctypes.c_double]
+    lib.orc_content_hash.restype = ctypes.c_uint64
+    lib.orc_content_hash.argtypes = [ctypes.c_int32, _P, ctypes.c_int64]
+    lib.orc_splitmix_finalize.restype = ctypes.c_uint64
+    lib.orc_splitmix_finalize.argtypes = [ctypes.c_uint64]
     lib.orc_tensor_stats.restype = None
     lib.orc_tensor_stats.argtypes = [ctypes.c_int32, _P, ctypes.c_int64, ctypes.POINTER(TStats)]
     return lib
@@ -279,3 +283,10 @@ def nearpass(cand: np.ndarray, ref: np.ndarray, dtype: int, atol: float, rtol: f
     d["ratio_hist"] = [int(v) for v in st.ratio_hist]
     d["ulp_hist"] = [int(v) for v in st.ulp_hist]
     return d
+
+
+def content_hash(raw: np.ndarray, dtype: int, lib=None) -> int:
+    """Content hash of one tensor's raw storage (see the C header)."""
+    lib = lib or default_lib()
+    raw = _raw(raw, dtype).reshape(-1)
+    return int(lib.orc_content_hash(dtype, _ptr(raw) if raw.size else None, raw.size))

@@ -402,3 +402,23 @@ void orc_nearpass(int32_t dtype, const void *cand, const void *ref, int64_t n, d
     if (fail && dist > out->max_ulp_fail) out->max_ulp_fail = dist;
   }
 }
+
+/* ---- content hash ------------------------------------------------------------ */
+
+uint64_t orc_splitmix_finalize(uint64_t z) {
+  z ^= z >> 30;
+  z *= 0xBF58476D1CE4E5B9ull;
+  z ^= z >> 27;
+  z *= 0x94D049BB133111EBull;
+  z ^= z >> 31;
+  return z;
+}
+
+uint64_t orc_content_hash(int32_t dtype, const void *x, int64_t n) {
+  uint64_t h = orc_splitmix_finalize(0x243F6A8885A308D3ull ^ ((uint64_t)dtype << 56) ^ (uint64_t)n);
+  for (int64_t i = 0; i < n; ++i) {
+    const uint64_t w = bits_of(dtype, x, i);
+    h += orc_splitmix_finalize(w ^ ((uint64_t)i * 0x9E3779B97F4A7C15ull));
+  }
+  return h;
+}

@@ -731,7 +731,52 @@ def pin_nearpass_handbuilt(lib):
         assert lib.orc_round_binary16(v) == h, (v, hex(lib.orc_round_binary16(v)))
 
 
+def pin_hash_splitmix(lib):
+    """The finalizer against the published SplitMix64 sequence: seeded with
+    0, the generator's first outputs are M(k * 0x9E3779B97F4A7C15) for
+    k = 1, 2, 3 (Steele, Lea and Flood's reference values)."""
+    g = 0x9E3779B97F4A7C15
+    want = [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+    for k, w in zip((1, 2, 3), want):
+        assert lib.orc_splitmix_finalize((k * g) % 2 ** 64) == w
+    assert lib.orc_splitmix_finalize(0) == 0
+
+
+def pin_hash_composition(lib):
+    """The content hash as the finalizer's sum over elements and its
+    invariants: any change of a value, of the order, of the length or of the
+    storage type changes it; a zero tensor of four elements sums the three
+    published SplitMix64 outputs (M(0) = 0)."""
+    m = lib.orc_splitmix_finalize
+    g = 0x9E3779B97F4A7C15
+    rng = np.random.default_rng(26084)
+    for dt in (F32, F16, BF16):
+        for n in (0, 1, 9, 1000):
+            raw = rng.integers(0, 2 ** (32 if dt == F32 else 16), n, dtype=np.uint64).astype(
+                np.uint32 if dt == F32 else np.uint16)
+            h = m(0x243F6A8885A308D3 ^ (dt << 56) ^ n)
+            for i, w in enumerate(raw.tolist()):
+                h = (h + m(int(w) ^ ((i * g) % 2 ** 64))) % 2 ** 64
+            assert oracle.content_hash(as_storage(raw, dt), dt, lib=lib) == h
+            if n >= 2:
+                swapped = raw.copy()
+                swapped[[0, 1]] = swapped[[1, 0]]
+                if swapped[0] != swapped[1]:
+                    assert oracle.content_hash(as_storage(swapped, dt), dt, lib=lib) != h
+                bumped = raw.copy()
+                bumped[n // 2] ^= 1
+                assert oracle.content_hash(as_storage(bumped, dt), dt, lib=lib) != h
+    z = np.zeros(4, dtype=np.float32)
+    published = (0xE220A8397B1DCDAF + 0x6E789E6AA1B965F4 + 0x06C45D188009454F) % 2 ** 64
+    meta = m(0x243F6A8885A308D3 ^ (F32 << 56) ^ 4)
+    assert oracle.content_hash(z, F32, lib=lib) == (meta + published) % 2 ** 64
+    h16 = oracle.content_hash(np.zeros(4, np.uint16), F16, lib=lib)
+    assert h16 != oracle.content_hash(np.zeros(4, np.uint16), BF16, lib=lib)
+    assert h16 != oracle.content_hash(np.zeros(5, np.uint16), F16, lib=lib)
+
+
 PINS = [
+    pin_hash_splitmix, pin_hash_composition,
     pin_nearpass_handbuilt, pin_nearpass_numpy,
     pin_tstats_handbuilt, pin_tstats_numpy,
     pin_gate_ties, pin_suite_handbuilt, pin_flags_handbuilt, pin_decode, pin_no_fma,

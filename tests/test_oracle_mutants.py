@@ -64,6 +64,10 @@ MUTANTS = [
     ("suite_ignores_status", "const int ok = status[c] >= 0 &&", "const int ok ="),
     ("tstats_argmin_last_tie", "v < out->min", "v <= out->min"),
     ("np_ratio_last_tie", "q > out->max_ratio", "q >= out->max_ratio"),
+    ("hash_no_index", "orc_splitmix_finalize(w ^ ((uint64_t)i * 0x9E3779B97F4A7C15ull))",
+     "orc_splitmix_finalize(w)"),
+    ("hash_shift", "  z ^= z >> 27;\n", "  z ^= z >> 28;\n"),
+    ("hash_no_dtype", "^ ((uint64_t)dtype << 56)", "^ 0"),
     ("np_fail_ge", "const int fail = d > t;", "const int fail = d >= t;"),
     ("np_round_ties_up", "(frac == 0.5 && fmod(kr, 2.0) != 0.0)", "(frac == 0.5)"),
     ("np_key_unsigned", "return (h & 0x8000u) ? -mag : mag;", "return h;"),
