@@ -338,15 +338,37 @@ vc_status vcheck_nearpass(const vc_case *cases, int32_t n_cases, const vc_tol *t
 /* Workspace bytes for vcheck_nearpass over the same cases. */
 vc_status vcheck_nearpass_workspace(const vc_case *cases, int32_t n_cases, size_t *bytes);
 
+/* ---- content hash ---------------------------------------------------------
+ *
+ * Content hashes of tensors, for the immutable evidence of a full-coverage
+ * evaluation (Sec. 4.3: acceptance backed by full-coverage evidence; the
+ * per-case pass/fail record; Sec. S4 reproducibility artifacts). With w_i
+ * the stored bit pattern of element i (zero-extended), n elements and
+ * storage code D:
+ *   H = M(0x243F6A8885A308D3 ^ (D << 56) ^ n) + sum_i M(w_i ^ (i * G)) mod 2^64,
+ * G = 0x9E3779B97F4A7C15 and M the 64-bit finalizer of the SplitMix64
+ * generator (z ^= z >> 30; z *= 0xBF58476D1CE4E5B9; z ^= z >> 27;
+ * z *= 0x94D049BB133111EB; z ^= z >> 31). Not cryptographic: it detects
+ * changed, reordered or truncated outputs between evaluations. */
+
+/* Hashes of tensors[0 .. n_tensors) into out[0 .. n_tensors) (device
+ * uint64_t; overwritten). Workspace: vcheck_content_hash_workspace. Errors
+ * as for vcheck_tensor_stats. n_tensors = 0 enqueues nothing. */
+vc_status vcheck_content_hash(const vc_tensor *tensors, int32_t n_tensors, uint64_t *out,
+                              void *workspace, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for vcheck_content_hash over the same tensors. */
+vc_status vcheck_content_hash_workspace(const vc_tensor *tensors, int32_t n_tensors,
+                                        size_t *bytes);
+
 /* Profiling hook (tracing): the next vcheck_compare / _localize / _integrity /
- * _sweep / _tensor_stats / _nearpass call made on this thread records
- * `begin_event` on its stream just before its first streaming-kernel launch
- * and `end_event` just after its last one, so hipEventElapsedTime gives the
- * duration of the streaming kernels alone (without the prologue and the
- * merge kernels). Both are
- * hipEvent_t handles created by the caller; the hook is consumed by that one
- * call. Pass NULL, NULL to clear it. Returns VC_OK, or VC_ERR_NULL when only
- * one of the two is NULL. */
+ * _sweep / _tensor_stats / _nearpass / _content_hash call made on this thread
+ * records `begin_event` on its stream just before its first streaming-kernel
+ * launch and `end_event` just after its last one, so hipEventElapsedTime
+ * gives the duration of the streaming kernels alone (without the prologue
+ * and the merge kernels). Both are hipEvent_t handles created by the caller;
+ * the hook is consumed by that one call. Pass NULL, NULL to clear it.
+ * Returns VC_OK, or VC_ERR_NULL when only one of the two is NULL. */
 vc_status vcheck_profile_events(void *begin_event, void *end_event);
 
 /* Workspace bytes for a sweep over `cases` (also for the single-case entry

@@ -1000,3 +1000,64 @@ vc_status vcheck_nearpass(const vc_case *cases, int32_t n_cases, const vc_tol *t
   if (se == VC_OK) slot->pending = true;
   return st != VC_OK ? st : se;
 }
+
+vc_status vcheck_content_hash_workspace(const vc_tensor *tensors, int32_t n_tensors,
+                                        size_t *bytes) {
+  g_last_error.clear();
+  if (bytes == nullptr) return fail(VC_ERR_NULL, "bytes is NULL");
+  ProbePlan plan;
+  const vc_status st = make_probe_plan(tensors, n_tensors, plan);
+  if (st != VC_OK) return st;
+  *bytes = align_up(plan.blob_bytes) + kAlign;  // the tensor table only
+  return VC_OK;
+}
+
+vc_status vcheck_content_hash(const vc_tensor *tensors, int32_t n_tensors, uint64_t *out,
+                              void *ws, size_t ws_bytes, void *stream_) {
+  g_last_error.clear();
+  ProbePlan plan;
+  vc_status st = make_probe_plan(tensors, n_tensors, plan);
+  if (st != VC_OK) return st;
+  if (n_tensors == 0) return VC_OK;
+  if (out == nullptr) return fail(VC_ERR_NULL, "out is NULL");
+  const size_t need = align_up(plan.blob_bytes) + kAlign;
+  if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < need)
+    return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, need);
+  const hipStream_t stream = (hipStream_t)stream_;
+  uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
+  const size_t n = (size_t)n_tensors;
+  std::vector<uint8_t> blob(plan.blob_bytes);
+  memcpy(blob.data(), plan.tensors.data(), sizeof(vck::ProbeTensor) * n);
+  memcpy(blob.data() + sizeof(vck::ProbeTensor) * n, plan.chunk_first.data(), 8 * n);
+  memcpy(blob.data() + (sizeof(vck::ProbeTensor) + 8) * n, plan.group_first.data(), 8 * n);
+  std::unique_lock<std::mutex> lock;
+  Slot *slot = nullptr;
+  st = stage_blob(blob.data(), blob.size(), lock, slot);
+  if (st != VC_OK) return st;
+  vck::Prologue Q;
+  memset(&Q, 0, sizeof Q);
+  Q.blob_src = (const uint8_t *)slot->dev;
+  Q.blob_dst = base;
+  Q.blob_bytes = plan.blob_bytes;
+  Q.zero = (uint32_t *)out;  // the sums start at zero
+  Q.zero_words = 2 * n;
+  Q.n_cases = 1;  // (no suite rates to clear)
+  vck::HashParams P;
+  memset(&P, 0, sizeof P);
+  P.tensors = (const vck::ProbeTensor *)base;
+  P.chunk_first = (const uint64_t *)(base + sizeof(vck::ProbeTensor) * n);
+  P.n_tensors = n_tensors;
+  P.unit = plan.unit;
+  P.out = (unsigned long long *)out;
+  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
+  g_prof_begin = g_prof_end = nullptr;
+  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  if (st == VC_OK)
+    st = hip_check(vck::launch_hash(P, plan.total_chunks, stream, prof_begin, prof_end),
+                   "hash launch");
+  // the staging slot is reused once the prologue has read it
+  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
+  if (se == VC_OK) slot->pending = true;
+  return st != VC_OK ? st : se;
+}

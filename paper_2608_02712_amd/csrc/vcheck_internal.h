@@ -245,6 +245,19 @@ struct NpParams {
 hipError_t launch_nearpass(const NpParams &p, uint64_t n_chunks, uint64_t n_groups,
                            hipStream_t s, hipEvent_t begin, hipEvent_t end);
 
+// Content hash: the probe's tensor table; out[t] is cleared by the prologue
+// and receives one 64-bit atomic addition per chunk.
+struct HashParams {
+  const ProbeTensor *tensors;
+  const uint64_t *chunk_first;
+  int32_t n_tensors;
+  uint32_t unit;
+  unsigned long long *out;
+};
+
+hipError_t launch_hash(const HashParams &p, uint64_t n_chunks, hipStream_t s, hipEvent_t begin,
+                       hipEvent_t end);
+
 // Launches the probe's streaming and merge kernels; `begin` / `end`
 // (nullable) are recorded around the streaming kernel.
 hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_groups,

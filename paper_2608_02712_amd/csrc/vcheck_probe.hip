@@ -1,5 +1,6 @@
-// vcheck_probe.hip -- gfx950 kernels of the diagnostic statistics: the
-// tensor-statistics probe and the near-pass statistics.
+// vcheck_probe.hip -- gfx950 kernels of the diagnostic statistics and the
+// evidence: the tensor-statistics probe, the near-pass statistics and the
+// content hash.
 //
 // The diagnostic instrumentation of the repair loop records multi-level
 // tensor statistics at pipeline boundaries (Sec. 4.2; the instrumentation
@@ -665,7 +666,99 @@ __global__ __launch_bounds__(kPThreads) void nearpass_final_kernel(const NpParam
   np_write(P.out + ci, C, r, h);
 }
 
+// ---------------------------------------------------------------- content hash
+//
+// H = M(0x243F6A8885A308D3 ^ (D << 56) ^ n) + sum_i M(w_i ^ i * G) mod 2^64,
+// with M the SplitMix64 finalizer (Steele, Lea and Flood, 2014) and w_i the
+// stored pattern of element i. The sum is order-free: every block adds its
+// chunk's part to the tensor's word with one 64-bit integer atomic, and the
+// block holding the tensor's first chunk adds the length / type term.
+
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z ^= z >> 30;
+  z *= 0xBF58476D1CE4E5B9ull;
+  z ^= z >> 27;
+  z *= 0x94D049BB133111EBull;
+  z ^= z >> 31;
+  return z;
+}
+
+template <int DT>
+__device__ __forceinline__ uint32_t raw_bits(const p32x4 &q, int j) {
+  if constexpr (DT == VC_F32) {
+    return q[j];
+  } else {
+    const uint32_t w = q[j >> 1];
+    return (j & 1) ? (w >> 16) : (w & 0xffffu);
+  }
+}
+
+template <int DT>
+__device__ uint64_t hash_chunk(const ProbeTensor &T, uint64_t c0, uint64_t c1, uint32_t U) {
+  constexpr int V = DT == VC_F32 ? 4 : 8;
+  constexpr int ES = DT == VC_F32 ? 4 : 2;
+  constexpr uint32_t ITER = 64 * V;
+  constexpr uint64_t G = 0x9E3779B97F4A7C15ull;
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint64_t w0 = min(c0 + (uint64_t)wave * U, c1), w1 = min(w0 + U, c1);
+  const bool vec = ((uintptr_t)T.data % 16) == 0;
+  uint64_t h = 0;
+  for (uint64_t b = w0; b < w1; b += ITER) {
+    const uint64_t i0 = b + (uint64_t)lane * V;
+    const p32x4 q = (vec && b + ITER <= w1) ? pload16(T.data + i0 * ES)
+                                            : pload_guarded<DT>(T.data, i0, w1);
+#pragma unroll
+    for (int j = 0; j < V; ++j)
+      if (i0 + j < w1) h += mix64((uint64_t)raw_bits<DT>(q, j) ^ ((i0 + j) * G));
+  }
+  return h;
+}
+
+__global__ __launch_bounds__(kPThreads) void hash_kernel(const HashParams P) {
+  __shared__ uint64_t part[kPWaves];
+  __shared__ uint32_t item;
+  const uint64_t chunk = blockIdx.x;
+  if (threadIdx.x < 64) {
+    const uint32_t ti = find_first(P.chunk_first, (uint32_t)P.n_tensors, chunk);
+    if (threadIdx.x == 0) item = ti;
+  }
+  __syncthreads();
+  const uint32_t ti = item;
+  const ProbeTensor T = P.tensors[ti];
+  const uint64_t CH = 4ull * P.unit;
+  const uint64_t c0 = (chunk - T.chunk_begin) * CH;
+  const uint64_t c1 = max(c0, min(c0 + CH, T.numel));
+  uint64_t h;
+  switch (T.dtype) {
+    case VC_F32: h = hash_chunk<VC_F32>(T, c0, c1, P.unit); break;
+    case VC_F16: h = hash_chunk<VC_F16>(T, c0, c1, P.unit); break;
+    default: h = hash_chunk<VC_BF16>(T, c0, c1, P.unit); break;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) h += __shfl_xor(h, m);
+  if ((threadIdx.x & 63u) == 0) part[threadIdx.x >> 6] = h;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t s = part[0] + part[1] + part[2] + part[3];
+    if (chunk == T.chunk_begin)
+      s += mix64(0x243F6A8885A308D3ull ^ ((uint64_t)(uint32_t)T.dtype << 56) ^ T.numel);
+    atomicAdd(P.out + ti, (unsigned long long)s);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_hash(const HashParams &p, uint64_t n_chunks, hipStream_t s, hipEvent_t begin,
+                       hipEvent_t end) {
+  hipError_t e;
+  if (begin != nullptr && (e = hipEventRecord(begin, s)) != hipSuccess) return e;
+  hipLaunchKernelGGL(hash_kernel, dim3((uint32_t)n_chunks), dim3(kPThreads), 0, s, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (end != nullptr && (e = hipEventRecord(end, s)) != hipSuccess) return e;
+  return hipSuccess;
+}
 
 hipError_t launch_nearpass(const NpParams &p, uint64_t n_chunks, uint64_t n_groups,
                            hipStream_t s, hipEvent_t begin, hipEvent_t end) {

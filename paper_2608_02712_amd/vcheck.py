@@ -16,6 +16,8 @@ raises.
 from __future__ import annotations
 
 import ctypes
+import hashlib
+import json
 import os
 
 import numpy as np
@@ -143,6 +145,10 @@ def lib() -> ctypes.CDLL:
                                       ctypes.c_size_t, P]
     L.vcheck_tensor_stats_workspace.argtypes = [ctypes.POINTER(VcTensor), ctypes.c_int32,
                                                 ctypes.POINTER(ctypes.c_size_t)]
+    L.vcheck_content_hash.argtypes = [ctypes.POINTER(VcTensor), ctypes.c_int32, P, P,
+                                      ctypes.c_size_t, P]
+    L.vcheck_content_hash_workspace.argtypes = [ctypes.POINTER(VcTensor), ctypes.c_int32,
+                                                ctypes.POINTER(ctypes.c_size_t)]
     L.vcheck_nearpass.argtypes = [ctypes.POINTER(VcCase), ctypes.c_int32, ctypes.POINTER(VcTol),
                                   P, P, ctypes.c_size_t, P]
     L.vcheck_nearpass_workspace.argtypes = [ctypes.POINTER(VcCase), ctypes.c_int32,
@@ -150,7 +156,8 @@ def lib() -> ctypes.CDLL:
     for name in ("vcheck_compare", "vcheck_localize", "vcheck_integrity", "vcheck_sweep",
                  "vcheck_workspace_bytes", "vcheck_tensor_stats",
                  "vcheck_tensor_stats_workspace", "vcheck_nearpass",
-                 "vcheck_nearpass_workspace"):
+                 "vcheck_nearpass_workspace", "vcheck_content_hash",
+                 "vcheck_content_hash_workspace"):
         getattr(L, name).restype = ctypes.c_int32
     if L.vcheck_abi_version() != 1:
         raise RuntimeError("libvcheck.so ABI version mismatch")
@@ -507,3 +514,97 @@ def vcheck_nearpass(cases, atol: float, rtol: float, stream=None) -> list[dict]:
         np_.launch(stream)
     return np_.results()
 
+
+class ContentHash:
+    """Prepared content hashes of a fixed list of device tensors (see
+    vcheck.h): launch() enqueues vcheck_content_hash, results() returns one
+    64-bit integer per tensor."""
+
+    def __init__(self, tensors):
+        self.tensors = list(tensors)
+        n = len(self.tensors)
+        self.desc = (VcTensor * max(n, 1))(*[tensor_desc(t) for t in self.tensors])
+        size = ctypes.c_size_t(0)
+        _check(lib().vcheck_content_hash_workspace(self.desc, n, ctypes.byref(size)))
+        dev = self.tensors[0].device if n else torch.device("cuda")
+        self.ws = _ws(size.value, dev)
+        self.out = torch.zeros(max(n, 1), dtype=torch.int64, device=dev)
+
+    def launch(self, stream=None) -> None:
+        _check(lib().vcheck_content_hash(self.desc, len(self.tensors), self.out.data_ptr(),
+                                         self.ws.data_ptr(), self.ws.numel(),
+                                         _stream_ptr(stream)))
+
+    def results(self) -> list[int]:
+        torch.cuda.synchronize(self.out.device)
+        return [int(v) for v in self.out.cpu().numpy()[:len(self.tensors)].view(np.uint64)]
+
+
+def vcheck_content_hash(tensors, stream=None) -> list[int]:
+    """Content hashes of device tensors (one pass; see vcheck.h)."""
+    h = ContentHash(tensors)
+    if h.tensors:
+        h.launch(stream)
+    return h.results()
+
+
+def _evidence_digest(record: dict) -> str:
+    body = json.dumps(record, sort_keys=True, separators=(",", ":")).encode()
+    return hashlib.sha256(body).hexdigest()
+
+
+def escalate(compact, extended, tols, primary: int = 0, gate: float = 1.0, tile=None,
+             k: int = 0, integrity: bool = False, evidence_path: str | None = None) -> dict:
+    """Two-stage validation with full-coverage evidence (Sec. 4.3, the
+    validation-escalation panel of the mechanisms figure; Sec. S2.2).
+
+    The compact case set runs first; only when its certified match rate at
+    the primary pair reaches `gate` does the extended set (the full coverage:
+    every shape and dtype) run, as one vcheck_sweep. Acceptance requires the
+    extended set to certify every case (numerically passing at the primary
+    pair, no detector flag). The evidence record holds, per stage and case,
+    the pass bits, mismatch counts, detector flags and the content hashes of
+    cand and ref, the stage's match rates and a hash of its case set; the
+    record's own SHA-256 digest makes later edits detectable. Written as JSON
+    to `evidence_path` when given.
+
+    compact / extended: lists of (cand, ref) or (cand, ref, inputs)."""
+
+    def stage(cases):
+        res = vcheck_sweep(cases, tols, primary=primary, tile=tile, k=k, integrity=integrity)
+        tensors = [t for c in cases for t in (c[0], c[1])]
+        hashes = vcheck_content_hash(tensors)
+        rows = []
+        for i in range(len(cases)):
+            flags = res["integrity"][i]["flags"] if res.get("integrity") else 0
+            rows.append({
+                "pass": [int(x) for x in res["pass"][i]],
+                "mismatches": [int(x) for x in res["mismatches"][i]],
+                "flags": int(flags),
+                "cand_hash": "%016x" % hashes[2 * i],
+                "ref_hash": "%016x" % hashes[2 * i + 1],
+            })
+        set_digest = hashlib.sha256("".join(
+            r["cand_hash"] + r["ref_hash"] for r in rows).encode()).hexdigest()
+        return {"n_cases": len(cases), "match_rate": [float(x) for x in res["match_rate"]],
+                "numeric_rate": [float(x) for x in res["numeric_rate"]],
+                "case_set_hash": set_digest, "cases": rows}
+
+    record = {"tols": [list(map(float, t[:2])) for t in tols], "primary": primary,
+              "gate": gate, "compact": stage(compact), "extended": None}
+    if record["compact"]["match_rate"][primary] >= gate:
+        record["extended"] = stage(extended)
+    ext = record["extended"]
+    record["accepted"] = bool(ext is not None and ext["n_cases"] > 0 and
+                              ext["match_rate"][primary] == 1.0)
+    record["digest"] = _evidence_digest(record)
+    if evidence_path is not None:
+        with open(evidence_path, "w") as f:
+            json.dump(record, f, indent=1, sort_keys=True)
+    return record
+
+
+def verify_evidence(record: dict) -> bool:
+    """Whether an evidence record still matches its own digest."""
+    body = {k: v for k, v in record.items() if k != "digest"}
+    return _evidence_digest(body) == record.get("digest")

@@ -241,3 +241,15 @@ def test_nearpass_host_checks(L):
     assert L.vcheck_nearpass(ok, 2, ctypes.byref(t), FAKE, FAKE, 8, None) == VC_ERR_WORKSPACE
     assert L.vcheck_nearpass(None, 0, ctypes.byref(t), None, None, 0, None) == 0
     assert vc.NEARPASS_DTYPE.itemsize == 456
+
+
+def test_content_hash_host_checks(L):
+    size = ctypes.c_size_t(0)
+    arr = (vc.VcTensor * 2)(desc(), desc(vc.VC_BF16, (3, 3)))
+    assert L.vcheck_content_hash_workspace(arr, 2, ctypes.byref(size)) == 0 and size.value > 0
+    assert L.vcheck_content_hash_workspace(arr, -1, ctypes.byref(size)) == VC_ERR_LIMIT
+    bad = (vc.VcTensor * 1)(desc(dtype=9))
+    assert L.vcheck_content_hash_workspace(bad, 1, ctypes.byref(size)) == VC_ERR_DTYPE
+    assert L.vcheck_content_hash(arr, 2, None, FAKE, 1 << 20, None) == VC_ERR_NULL
+    assert L.vcheck_content_hash(arr, 2, FAKE, FAKE, 4, None) == VC_ERR_WORKSPACE
+    assert L.vcheck_content_hash(None, 0, None, None, 0, None) == 0
