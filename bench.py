@@ -12,7 +12,8 @@ records around them.
 Headline line: the fp16 batch of 64 cases of 2048x2048 (the configuration the
 metric is quoted on). ``probe`` reports the tensor-statistics probe over the
 128 cand and ref tensors of that batch in one call, ``nearpass`` the near-pass
-statistics of its 64 cases. ``workloads`` holds the same figures for all five
+statistics of its 64 cases, ``content_hash`` the content hashes of its 128
+tensors. ``workloads`` holds the same figures for all five
 workloads, measured in the same run. ``roofline`` reports the main streaming
 kernel's achieved HBM bandwidth (algorithmic bytes / its event-timed average
 duration) against the 8 TB/s peak; ``cpu_baseline`` times the CPU oracle on a
@@ -269,6 +270,53 @@ def measure_nearpass(w, steps, warmup, flush):
     return out
 
 
+def measure_hash(w, steps, warmup, flush):
+    """Content hashes of every cand and ref tensor of workload w, one call
+    (the evidence of a full-coverage evaluation): call time, events around
+    the call, cache flushed before it."""
+    import torch
+
+    import oracle
+    import workloads as wl
+    from paper_2608_02712_amd import vcheck as vc
+
+    tensors = [t for c in w.cases for t in (c.cand, c.ref)]
+    ch = vc.ContentHash(tensors)
+    for _ in range(warmup):
+        ch.launch()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+    for i in range(steps):
+        flush.fill_(i & 0xFF)
+        evs[i][0].record(stream)
+        ch.launch(stream)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    call = sorted(a.elapsed_time(b) for a, b in evs)[steps // 2]
+    nbytes = sum(t.numel() * t.element_size() for t in tensors)
+    spent, done = 0.0, 0
+    for t in tensors:
+        raw = wl.raw_numpy(t).reshape(-1)
+        t0 = time.perf_counter()
+        oracle.content_hash(raw, wl.dtype_code(t.dtype))
+        spent += time.perf_counter() - t0
+        done += raw.nbytes
+        if spent >= 1.0:
+            break
+    out = {
+        "workload": "content hashes of the %d cand and ref tensors of %s" % (len(tensors), w.name),
+        "bytes": nbytes,
+        "ms_per_call": round(call, 5),
+        "gbps": round(nbytes / (call * 1e-3) / 1e9, 2),
+        "pct_hbm_peak": round(100.0 * nbytes / (call * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "oracle_one_thread_gbps": round(done / spent / 1e9, 4),
+    }
+    log("content hash: %.3f ms/call, %.1f GB/s (%.1f%% of peak)" % (
+        call, out["gbps"], out["pct_hbm_peak"]))
+    return out
+
+
 def cpu_baseline(w, seconds):
     """The CPU oracle on whole cases of the workload: first one thread until
     the time budget is used (at least one case), then the same cases spread
@@ -368,10 +416,11 @@ def main():
     w, head = measure(first, args.steps, args.warmup, flush)
     results[first] = head
     cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds)
-    probe = nearpass = None
+    probe = nearpass = chash = None
     if not args.only:
         probe = measure_probe(w, args.steps, args.warmup, flush)
         nearpass = measure_nearpass(w, args.steps, args.warmup, flush)
+        chash = measure_hash(w, args.steps, args.warmup, flush)
     del w
     torch.cuda.empty_cache()
     if not args.headline_only and not args.only:
@@ -411,6 +460,7 @@ def main():
         "workloads": {str(k): v for k, v in sorted(results.items())},
         "probe": probe,
         "nearpass": nearpass,
+        "content_hash": chash,
     }
     print(json.dumps(line), flush=True)
 

@@ -608,3 +608,50 @@ def verify_evidence(record: dict) -> bool:
     """Whether an evidence record still matches its own digest."""
     body = {k: v for k, v in record.items() if k != "digest"}
     return _evidence_digest(body) == record.get("digest")
+
+
+class BestCandidate:
+    """State-continuous repair bookkeeping (Sec. 4.4; the mechanisms figure's
+    state-continuous panel): the engine keeps the highest-scoring candidate,
+    and after `patience` (two) consecutive attempts that do not improve on
+    it, it rolls back to that candidate.
+
+    record(name, score) takes an attempt's score, the certified match rate
+    at the primary pair of its full-coverage evaluation (vcheck_sweep's
+    match_rate, or an evidence record's), and returns "promote" (a new best:
+    strictly higher score, or the first attempt), "continue" (not better,
+    fewer than `patience` such attempts in a row) or "rollback" (the
+    patience-th non-improving attempt in a row: continue from `best`; the
+    count restarts)."""
+
+    def __init__(self, patience: int = 2):
+        if patience < 1:
+            raise ValueError("patience must be at least 1")
+        self.patience = patience
+        self.best = None
+        self.best_score = None
+        self.stale = 0
+        self.history = []
+
+    def record(self, name, score: float) -> str:
+        score = float(score)
+        if self.best_score is None or score > self.best_score:
+            self.best, self.best_score, self.stale = name, score, 0
+            decision = "promote"
+        else:
+            self.stale += 1
+            decision = "continue"
+            if self.stale >= self.patience:
+                decision = "rollback"
+                self.stale = 0
+        self.history.append((name, score, decision))
+        return decision
+
+    def record_evidence(self, name, record: dict) -> str:
+        """record() with the score of an escalate() evidence record: the
+        extended set's certified match rate at the primary pair, or 0 when
+        the compact set stopped the escalation or the record was edited."""
+        if not verify_evidence(record) or record.get("extended") is None:
+            return self.record(name, 0.0)
+        return self.record(name, record["extended"]["match_rate"][record["primary"]])
+
