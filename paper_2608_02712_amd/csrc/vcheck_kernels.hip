@@ -774,15 +774,21 @@ void main_kernel(const Params P) {
     g.do_tiles = do_tiles ? 1u : 0u;
     if (do_tiles && cend > cstart) {
       const uint64_t th = (uint64_t)P.tile_h, tw = (uint64_t)P.tile_w;
-      const uint64_t row0 = cstart / cols, col0 = cstart - row0 * cols;
-      g.tiles_c = tiles_c;
-      g.trow0 = row0 / th;
-      g.rrem0 = (uint32_t)(row0 - g.trow0 * th);
       g.wide = cols >= (1ull << 31) ? 1u : 0u;
+      // 32-bit magic-number divisions where the operands fit (the usual
+      // case); 64-bit division otherwise
+      constexpr uint64_t k32 = 1ull << 32;
+      const uint64_t row0 = (!g.wide && cstart < k32)
+                                ? div_by((uint32_t)cstart, dcs.cols_div.m, dcs.cols_div.shifts)
+                                : cstart / cols;
+      const uint64_t col0 = cstart - row0 * cols;
+      g.tiles_c = tiles_c;
+      g.trow0 = row0 < k32 ? div_by((uint32_t)row0, P.th_div.m, P.th_div.shifts) : row0 / th;
+      g.rrem0 = (uint32_t)(row0 - g.trow0 * th);
       g.col0 = (uint32_t)col0;
       g.cols32 = (uint32_t)cols;
       g.room = cols - col0;
-      g.tcol0 = col0 / tw;
+      g.tcol0 = col0 < k32 ? div_by((uint32_t)col0, P.tw_div.m, P.tw_div.shifts) : col0 / tw;
       g.crem0 = (uint32_t)(col0 - g.tcol0 * tw);
       g.cdiv = dcs.cols_div;
       g.hdiv = P.th_div;
@@ -796,11 +802,13 @@ void main_kernel(const Params P) {
       const uint64_t t_first = tile_at(g, 0, dr_first), t_last = tile_at(g, last, dr_first);
       const uint32_t dr_last =
           g.wide ? ((uint64_t)last >= g.room ? 1u : 0u) : div_by(g.col0 + last, g.cdiv.m, g.cdiv.shifts);
-      const uint64_t rr_last = (uint64_t)g.rrem0 + dr_last;
-      const uint64_t tr_last = g.trow0 + rr_last / th;
+      const uint32_t rr_last = g.rrem0 + dr_last;  // below 2^31: a chunk spans < 2^18 rows
+      const uint32_t rq_last = div_by(rr_last, P.th_div.m, P.th_div.shifts);
+      const uint64_t tr_last = g.trow0 + rq_last;
       const bool multi = dr_last > 0;
       const uint64_t t_min = (multi && g.rrem0 + 1 < th) ? g.trow0 * tiles_c : t_first;
-      const uint64_t t_max = (multi && rr_last % th != 0) ? tr_last * tiles_c + tiles_c - 1 : t_last;
+      const uint64_t t_max =
+          (multi && rr_last != rq_last * (uint32_t)th) ? tr_last * tiles_c + tiles_c - 1 : t_last;
       if (t_max - t_min < (uint64_t)kTileWindow) {
         g.win_base = t_min;
         g.win_len = (uint32_t)(t_max - t_min + 1);
