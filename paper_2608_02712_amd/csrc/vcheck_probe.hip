@@ -704,13 +704,15 @@ __device__ uint64_t hash_chunk(const ProbeTensor &T, uint64_t c0, uint64_t c1, u
   const uint64_t w0 = min(c0 + (uint64_t)wave * U, c1), w1 = min(w0 + U, c1);
   const bool vec = ((uintptr_t)T.data % 16) == 0;
   uint64_t h = 0;
-  for (uint64_t b = w0; b < w1; b += ITER) {
+  // i * G for the lane's first element, advanced by a constant per step
+  uint64_t ig = (w0 + (uint64_t)lane * V) * G;
+  for (uint64_t b = w0; b < w1; b += ITER, ig += (uint64_t)ITER * G) {
     const uint64_t i0 = b + (uint64_t)lane * V;
     const p32x4 q = (vec && b + ITER <= w1) ? pload16(T.data + i0 * ES)
                                             : pload_guarded<DT>(T.data, i0, w1);
 #pragma unroll
     for (int j = 0; j < V; ++j)
-      if (i0 + j < w1) h += mix64((uint64_t)raw_bits<DT>(q, j) ^ ((i0 + j) * G));
+      if (i0 + j < w1) h += mix64((uint64_t)raw_bits<DT>(q, j) ^ (ig + (uint64_t)j * G));
   }
   return h;
 }
