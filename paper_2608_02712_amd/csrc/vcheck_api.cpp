@@ -9,6 +9,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "vcheck_internal.h"
@@ -646,6 +647,44 @@ vc_status make_probe_plan(const vc_tensor *tensors, int32_t n, ProbePlan &plan) 
   return VC_OK;
 }
 
+// Runs one diagnostic call: stages the descriptor blob (`parts`, copied
+// back to back) in a pinned slot, enqueues the prologue (copying it to
+// `base`, clearing `zero_words` words at `zero`) and then `launch` (which
+// receives the profiling events), and records the slot's event behind them.
+template <typename F>
+vc_status run_diagnostic(const std::vector<std::pair<const void *, size_t>> &parts, uint8_t *base,
+                         uint32_t *zero, uint64_t zero_words, hipStream_t stream,
+                         const char *what, F launch) {
+  size_t total = 0;
+  for (const auto &p : parts) total += p.second;
+  std::vector<uint8_t> blob(total);
+  size_t at = 0;
+  for (const auto &p : parts) {
+    memcpy(blob.data() + at, p.first, p.second);
+    at += p.second;
+  }
+  std::unique_lock<std::mutex> lock;
+  Slot *slot = nullptr;
+  vc_status st = stage_blob(blob.data(), blob.size(), lock, slot);
+  if (st != VC_OK) return st;
+  vck::Prologue Q;
+  memset(&Q, 0, sizeof Q);
+  Q.blob_src = (const uint8_t *)slot->dev;
+  Q.blob_dst = base;
+  Q.blob_bytes = total;
+  Q.zero = zero;
+  Q.zero_words = zero_words;
+  Q.n_cases = 1;  // (no suite rates to clear)
+  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
+  g_prof_begin = g_prof_end = nullptr;
+  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  if (st == VC_OK) st = hip_check(launch(prof_begin, prof_end), what);
+  // the staging slot is reused once the prologue has read it
+  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
+  if (se == VC_OK) slot->pending = true;
+  return st != VC_OK ? st : se;
+}
+
 // ---- near-pass statistics -------------------------------------------------
 
 struct NpPlan {
@@ -896,23 +935,8 @@ vc_status vcheck_tensor_stats(const vc_tensor *tensors, int32_t n_tensors, vc_ts
   if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
   if (ws_bytes < plan.bytes)
     return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
-  const hipStream_t stream = (hipStream_t)stream_;
   uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
   const size_t n = (size_t)n_tensors;
-  std::vector<uint8_t> blob(plan.blob_bytes);
-  memcpy(blob.data(), plan.tensors.data(), sizeof(vck::ProbeTensor) * n);
-  memcpy(blob.data() + sizeof(vck::ProbeTensor) * n, plan.chunk_first.data(), 8 * n);
-  memcpy(blob.data() + (sizeof(vck::ProbeTensor) + 8) * n, plan.group_first.data(), 8 * n);
-  std::unique_lock<std::mutex> lock;
-  Slot *slot = nullptr;
-  st = stage_blob(blob.data(), blob.size(), lock, slot);
-  if (st != VC_OK) return st;
-  vck::Prologue Q;
-  memset(&Q, 0, sizeof Q);
-  Q.blob_src = (const uint8_t *)slot->dev;
-  Q.blob_dst = base;
-  Q.blob_bytes = plan.blob_bytes;
-  Q.n_cases = 1;  // (no suite rates to clear)
   vck::ProbeParams P;
   memset(&P, 0, sizeof P);
   P.tensors = (const vck::ProbeTensor *)base;
@@ -923,17 +947,15 @@ vc_status vcheck_tensor_stats(const vc_tensor *tensors, int32_t n_tensors, vc_ts
   P.recs = (vck::ProbeRec *)(base + plan.off_recs);
   P.grecs = (vck::ProbeRec *)(base + plan.off_grecs);
   P.out = out;
-  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
-  g_prof_begin = g_prof_end = nullptr;
-  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
-  if (st == VC_OK)
-    st = hip_check(vck::launch_probe(P, plan.total_chunks, plan.total_groups, stream,
-                                     prof_begin, prof_end),
-                   "probe launch");
-  // the staging slot is reused once the prologue has read it
-  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
-  if (se == VC_OK) slot->pending = true;
-  return st != VC_OK ? st : se;
+  const hipStream_t stream = (hipStream_t)stream_;
+  return run_diagnostic({{plan.tensors.data(), sizeof(vck::ProbeTensor) * n},
+                         {plan.chunk_first.data(), 8 * n},
+                         {plan.group_first.data(), 8 * n}},
+                        base, nullptr, 0, stream, "probe launch",
+                        [&](hipEvent_t b, hipEvent_t e) {
+                          return vck::launch_probe(P, plan.total_chunks, plan.total_groups,
+                                                   stream, b, e);
+                        });
 }
 
 vc_status vcheck_nearpass_workspace(const vc_case *cases, int32_t n_cases, size_t *bytes) {
@@ -959,23 +981,8 @@ vc_status vcheck_nearpass(const vc_case *cases, int32_t n_cases, const vc_tol *t
   if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
   if (ws_bytes < plan.bytes)
     return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
-  const hipStream_t stream = (hipStream_t)stream_;
   uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
   const size_t n = (size_t)n_cases;
-  std::vector<uint8_t> blob(plan.blob_bytes);
-  memcpy(blob.data(), plan.cases.data(), sizeof(vck::NpCase) * n);
-  memcpy(blob.data() + sizeof(vck::NpCase) * n, plan.chunk_first.data(), 8 * n);
-  memcpy(blob.data() + (sizeof(vck::NpCase) + 8) * n, plan.group_first.data(), 8 * n);
-  std::unique_lock<std::mutex> lock;
-  Slot *slot = nullptr;
-  st = stage_blob(blob.data(), blob.size(), lock, slot);
-  if (st != VC_OK) return st;
-  vck::Prologue Q;
-  memset(&Q, 0, sizeof Q);
-  Q.blob_src = (const uint8_t *)slot->dev;
-  Q.blob_dst = base;
-  Q.blob_bytes = plan.blob_bytes;
-  Q.n_cases = 1;  // (no suite rates to clear)
   vck::NpParams P;
   memset(&P, 0, sizeof P);
   P.cases = (const vck::NpCase *)base;
@@ -988,17 +995,15 @@ vc_status vcheck_nearpass(const vc_case *cases, int32_t n_cases, const vc_tol *t
   P.recs = (vck::NpRec *)(base + plan.off_recs);
   P.grecs = (vck::NpRec *)(base + plan.off_grecs);
   P.out = out;
-  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
-  g_prof_begin = g_prof_end = nullptr;
-  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
-  if (st == VC_OK)
-    st = hip_check(vck::launch_nearpass(P, plan.total_chunks, plan.total_groups, stream,
-                                        prof_begin, prof_end),
-                   "near-pass launch");
-  // the staging slot is reused once the prologue has read it
-  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
-  if (se == VC_OK) slot->pending = true;
-  return st != VC_OK ? st : se;
+  const hipStream_t stream = (hipStream_t)stream_;
+  return run_diagnostic({{plan.cases.data(), sizeof(vck::NpCase) * n},
+                         {plan.chunk_first.data(), 8 * n},
+                         {plan.group_first.data(), 8 * n}},
+                        base, nullptr, 0, stream, "near-pass launch",
+                        [&](hipEvent_t b, hipEvent_t e) {
+                          return vck::launch_nearpass(P, plan.total_chunks, plan.total_groups,
+                                                      stream, b, e);
+                        });
 }
 
 vc_status vcheck_content_hash_workspace(const vc_tensor *tensors, int32_t n_tensors,
@@ -1024,25 +1029,8 @@ vc_status vcheck_content_hash(const vc_tensor *tensors, int32_t n_tensors, uint6
   if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
   if (ws_bytes < need)
     return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, need);
-  const hipStream_t stream = (hipStream_t)stream_;
   uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
   const size_t n = (size_t)n_tensors;
-  std::vector<uint8_t> blob(plan.blob_bytes);
-  memcpy(blob.data(), plan.tensors.data(), sizeof(vck::ProbeTensor) * n);
-  memcpy(blob.data() + sizeof(vck::ProbeTensor) * n, plan.chunk_first.data(), 8 * n);
-  memcpy(blob.data() + (sizeof(vck::ProbeTensor) + 8) * n, plan.group_first.data(), 8 * n);
-  std::unique_lock<std::mutex> lock;
-  Slot *slot = nullptr;
-  st = stage_blob(blob.data(), blob.size(), lock, slot);
-  if (st != VC_OK) return st;
-  vck::Prologue Q;
-  memset(&Q, 0, sizeof Q);
-  Q.blob_src = (const uint8_t *)slot->dev;
-  Q.blob_dst = base;
-  Q.blob_bytes = plan.blob_bytes;
-  Q.zero = (uint32_t *)out;  // the sums start at zero
-  Q.zero_words = 2 * n;
-  Q.n_cases = 1;  // (no suite rates to clear)
   vck::HashParams P;
   memset(&P, 0, sizeof P);
   P.tensors = (const vck::ProbeTensor *)base;
@@ -1050,14 +1038,13 @@ vc_status vcheck_content_hash(const vc_tensor *tensors, int32_t n_tensors, uint6
   P.n_tensors = n_tensors;
   P.unit = plan.unit;
   P.out = (unsigned long long *)out;
-  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
-  g_prof_begin = g_prof_end = nullptr;
-  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
-  if (st == VC_OK)
-    st = hip_check(vck::launch_hash(P, plan.total_chunks, stream, prof_begin, prof_end),
-                   "hash launch");
-  // the staging slot is reused once the prologue has read it
-  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
-  if (se == VC_OK) slot->pending = true;
-  return st != VC_OK ? st : se;
+  const hipStream_t stream = (hipStream_t)stream_;
+  // the prologue clears the sums
+  return run_diagnostic({{plan.tensors.data(), sizeof(vck::ProbeTensor) * n},
+                         {plan.chunk_first.data(), 8 * n},
+                         {plan.group_first.data(), 8 * n}},
+                        base, (uint32_t *)out, 2 * n, stream, "hash launch",
+                        [&](hipEvent_t b, hipEvent_t e) {
+                          return vck::launch_hash(P, plan.total_chunks, stream, b, e);
+                        });
 }
