@@ -305,6 +305,8 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
     }
     g.case_hi = plan.table.size();
     g.n_chunks = chunk - g.chunk_lo;
+    if (g.n_chunks > 0x7fffffffull)
+      return fail(VC_ERR_LIMIT, "the cases of one dtype need more than 2^31 - 1 blocks");
     if (g.case_hi > g.case_lo) plan.groups.push_back(g);
   }
   plan.total_chunks = chunk;
@@ -637,6 +639,8 @@ vc_status make_probe_plan(const vc_tensor *tensors, int32_t n, ProbePlan &plan) 
     plan.total_chunks += nc;
     plan.total_groups += (nc + vck::kProbeGroupChunks - 1) / vck::kProbeGroupChunks;
   }
+  if (plan.total_chunks > 0x7fffffffull)
+    return fail(VC_ERR_LIMIT, "the batch needs more than 2^31 - 1 blocks");
   plan.blob_bytes = (sizeof(vck::ProbeTensor) + 2 * sizeof(uint64_t)) * (size_t)n;
   size_t off = align_up(plan.blob_bytes);
   plan.off_recs = off;
@@ -739,6 +743,8 @@ vc_status make_np_plan(const vc_case *cases, int32_t n, NpPlan &plan) {
     plan.total_chunks += nc;
     plan.total_groups += (nc + vck::kProbeGroupChunks - 1) / vck::kProbeGroupChunks;
   }
+  if (plan.total_chunks > 0x7fffffffull)
+    return fail(VC_ERR_LIMIT, "the batch needs more than 2^31 - 1 blocks");
   plan.blob_bytes = (sizeof(vck::NpCase) + 2 * sizeof(uint64_t)) * (size_t)n;
   size_t off = align_up(plan.blob_bytes);
   plan.off_recs = off;
