@@ -343,8 +343,8 @@ vc_status vcheck_nearpass_workspace(const vc_case *cases, int32_t n_cases, size_
  * Content hashes of tensors, for the immutable evidence of a full-coverage
  * evaluation (Sec. 4.3: acceptance backed by full-coverage evidence; the
  * per-case pass/fail record; Sec. S4 reproducibility artifacts). With w_i
- * the stored bit pattern of element i (zero-extended), n elements and
- * storage code D:
+ * the i-th 64-bit word of the tensor's storage (bytes 8i .. 8i+7 read
+ * little-endian, the last word zero-padded), n elements and storage code D:
  *   H = M(0x243F6A8885A308D3 ^ (D << 56) ^ n) + sum_i M(w_i ^ (i * G)) mod 2^64,
  * G = 0x9E3779B97F4A7C15 and M the 64-bit finalizer of the SplitMix64
  * generator (z ^= z >> 30; z *= 0xBF58476D1CE4E5B9; z ^= z >> 27;

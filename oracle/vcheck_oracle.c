@@ -416,8 +416,12 @@ uint64_t orc_splitmix_finalize(uint64_t z) {
 
 uint64_t orc_content_hash(int32_t dtype, const void *x, int64_t n) {
   uint64_t h = orc_splitmix_finalize(0x243F6A8885A308D3ull ^ ((uint64_t)dtype << 56) ^ (uint64_t)n);
-  for (int64_t i = 0; i < n; ++i) {
-    const uint64_t w = bits_of(dtype, x, i);
+  const int64_t nbytes = n * (dtype == ORC_F32 ? 4 : 2);
+  const unsigned char *p = (const unsigned char *)x;
+  for (int64_t i = 0; 8 * i < nbytes; ++i) {
+    /* word i: bytes 8i .. 8i+7, little-endian, missing bytes zero */
+    uint64_t w = 0;
+    for (int b = 0; b < 8 && 8 * i + b < nbytes; ++b) w |= (uint64_t)p[8 * i + b] << (8 * b);
     h += orc_splitmix_finalize(w ^ ((uint64_t)i * 0x9E3779B97F4A7C15ull));
   }
   return h;

@@ -147,14 +147,15 @@ void orc_nearpass(int32_t dtype, const void *cand, const void *ref, int64_t n, d
 
 /* Content hash of one tensor, for the immutable evidence of a full-coverage
  * evaluation (Sec. 4.3: per-case results backed by full-coverage evidence;
- * Sec. S4 reproducibility artifacts): with w_i the stored bit pattern of
- * element i (zero-extended to 64 bits), n elements and storage code D,
+ * Sec. S4 reproducibility artifacts): with w_i the i-th 64-bit word of the
+ * tensor's storage (bytes 8i .. 8i+7 read little-endian, the last word
+ * zero-padded; ceil(n * size / 8) words), n elements and storage code D,
  *   H = M(0x243F6A8885A308D3 ^ (D << 56) ^ n) + sum_i M(w_i ^ (i * G))
  * modulo 2^64, where G = 0x9E3779B97F4A7C15 and M is the 64-bit finalizer of
  * the SplitMix64 generator (Steele, Lea and Flood, 2014):
  *   z ^= z >> 30; z *= 0xBF58476D1CE4E5B9; z ^= z >> 27;
  *   z *= 0x94D049BB133111EB; z ^= z >> 31.
- * The sum is order-free, so any partition of the elements hashes alike. */
+ * The sum is order-free, so any partition of the words hashes alike. */
 uint64_t orc_content_hash(int32_t dtype, const void *x, int64_t n);
 
 /* The finalizer M above. */

@@ -670,9 +670,12 @@ __global__ __launch_bounds__(kPThreads) void nearpass_final_kernel(const NpParam
 //
 // H = M(0x243F6A8885A308D3 ^ (D << 56) ^ n) + sum_i M(w_i ^ i * G) mod 2^64,
 // with M the SplitMix64 finalizer (Steele, Lea and Flood, 2014) and w_i the
-// stored pattern of element i. The sum is order-free: every block adds its
-// chunk's part to the tensor's word with one 64-bit integer atomic, and the
-// block holding the tensor's first chunk adds the length / type term.
+// i-th 64-bit little-endian word of the tensor's storage (the last one
+// zero-padded). A lane's 16 bytes of a step are two words; chunk and step
+// boundaries fall on 1 KiB, so no word straddles them. The sum is order-free:
+// every block adds its chunk's part to the tensor's sum with one 64-bit
+// integer atomic, and the block holding the tensor's first chunk adds the
+// length / type term.
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {
   z ^= z >> 30;
@@ -681,16 +684,6 @@ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
   z *= 0x94D049BB133111EBull;
   z ^= z >> 31;
   return z;
-}
-
-template <int DT>
-__device__ __forceinline__ uint32_t raw_bits(const p32x4 &q, int j) {
-  if constexpr (DT == VC_F32) {
-    return q[j];
-  } else {
-    const uint32_t w = q[j >> 1];
-    return (j & 1) ? (w >> 16) : (w & 0xffffu);
-  }
 }
 
 template <int DT>
@@ -703,16 +696,18 @@ __device__ uint64_t hash_chunk(const ProbeTensor &T, uint64_t c0, uint64_t c1, u
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint64_t w0 = min(c0 + (uint64_t)wave * U, c1), w1 = min(w0 + U, c1);
   const bool vec = ((uintptr_t)T.data % 16) == 0;
+  constexpr int EW = 8 / ES;  // elements per word
   uint64_t h = 0;
-  // i * G for the lane's first element, advanced by a constant per step
-  uint64_t ig = (w0 + (uint64_t)lane * V) * G;
-  for (uint64_t b = w0; b < w1; b += ITER, ig += (uint64_t)ITER * G) {
+  // i * G for the lane's first word (its element offset times ES / 8; w0 is
+  // a multiple of 1024 elements), advanced by a constant per step
+  uint64_t ig = ((w0 + (uint64_t)lane * V) / EW) * G;
+  for (uint64_t b = w0; b < w1; b += ITER, ig += (uint64_t)(ITER / EW) * G) {
     const uint64_t i0 = b + (uint64_t)lane * V;
+    // elements past w1 load as zero: the zero padding of the last word
     const p32x4 q = (vec && b + ITER <= w1) ? pload16(T.data + i0 * ES)
                                             : pload_guarded<DT>(T.data, i0, w1);
-#pragma unroll
-    for (int j = 0; j < V; ++j)
-      if (i0 + j < w1) h += mix64((uint64_t)raw_bits<DT>(q, j) ^ (ig + (uint64_t)j * G));
+    if (i0 < w1) h += mix64(((uint64_t)q[1] << 32 | q[0]) ^ ig);
+    if (i0 + EW < w1) h += mix64(((uint64_t)q[3] << 32 | q[2]) ^ (ig + G));
   }
   return h;
 }

@@ -743,20 +743,25 @@ def pin_hash_splitmix(lib):
 
 
 def pin_hash_composition(lib):
-    """The content hash as the finalizer's sum over elements and its
-    invariants: any change of a value, of the order, of the length or of the
-    storage type changes it; a zero tensor of four elements sums the three
-    published SplitMix64 outputs (M(0) = 0)."""
+    """The content hash as the finalizer's sum over 64-bit storage words and
+    its invariants: any change of a value, of the order, of the length or of
+    the storage type changes it; the words depend on the bytes alone (a
+    binary32 tensor and the 16-bit view of its bytes differ in the length /
+    type term only); a zero tensor of four words sums the three published
+    SplitMix64 outputs (M(0) = 0)."""
     m = lib.orc_splitmix_finalize
     g = 0x9E3779B97F4A7C15
     rng = np.random.default_rng(26084)
     for dt in (F32, F16, BF16):
-        for n in (0, 1, 9, 1000):
+        for n in (0, 1, 3, 4, 9, 1000):
             raw = rng.integers(0, 2 ** (32 if dt == F32 else 16), n, dtype=np.uint64).astype(
                 np.uint32 if dt == F32 else np.uint16)
             h = m(0x243F6A8885A308D3 ^ (dt << 56) ^ n)
-            for i, w in enumerate(raw.tolist()):
-                h = (h + m(int(w) ^ ((i * g) % 2 ** 64))) % 2 ** 64
+            # words built with Python integers from the little-endian bytes
+            data = raw.astype('<u4' if dt == F32 else '<u2').tobytes()
+            for i in range(0, len(data), 8):
+                w = int.from_bytes(data[i:i + 8], 'little')
+                h = (h + m(w ^ ((i // 8 * g) % 2 ** 64))) % 2 ** 64
             assert oracle.content_hash(as_storage(raw, dt), dt, lib=lib) == h
             if n >= 2:
                 swapped = raw.copy()
@@ -766,10 +771,19 @@ def pin_hash_composition(lib):
                 bumped = raw.copy()
                 bumped[n // 2] ^= 1
                 assert oracle.content_hash(as_storage(bumped, dt), dt, lib=lib) != h
-    z = np.zeros(4, dtype=np.float32)
     published = (0xE220A8397B1DCDAF + 0x6E789E6AA1B965F4 + 0x06C45D188009454F) % 2 ** 64
-    meta = m(0x243F6A8885A308D3 ^ (F32 << 56) ^ 4)
-    assert oracle.content_hash(z, F32, lib=lib) == (meta + published) % 2 ** 64
+    for dt, z in ((F32, np.zeros(8, np.float32)), (F16, np.zeros(16, np.uint16)),
+                  (BF16, np.zeros(13, np.uint16))):
+        meta = m(0x243F6A8885A308D3 ^ (dt << 56) ^ z.size)
+        assert oracle.content_hash(z, dt, lib=lib) == (meta + published) % 2 ** 64
+    # the same bytes as binary32, binary16 and bfloat16: equal word sums
+    x = rng.integers(0, 2 ** 32, 37, dtype=np.uint64).astype(np.uint32)
+    body = set()
+    for dt, v, n in ((F32, x.view(np.float32), 37), (F16, x.view(np.uint16), 74),
+                     (BF16, x.view(np.uint16), 74)):
+        body.add((oracle.content_hash(v, dt, lib=lib) - m(0x243F6A8885A308D3 ^ (dt << 56) ^ n))
+                 % 2 ** 64)
+    assert len(body) == 1
     h16 = oracle.content_hash(np.zeros(4, np.uint16), F16, lib=lib)
     assert h16 != oracle.content_hash(np.zeros(4, np.uint16), BF16, lib=lib)
     assert h16 != oracle.content_hash(np.zeros(5, np.uint16), F16, lib=lib)

@@ -67,6 +67,8 @@ MUTANTS = [
     ("hash_no_index", "orc_splitmix_finalize(w ^ ((uint64_t)i * 0x9E3779B97F4A7C15ull))",
      "orc_splitmix_finalize(w)"),
     ("hash_shift", "  z ^= z >> 27;\n", "  z ^= z >> 28;\n"),
+    ("hash_word_big_endian", "<< (8 * b);", "<< (56 - 8 * b);"),
+    ("hash_tail_dropped", "8 * i < nbytes; ++i", "8 * i + 8 <= nbytes; ++i"),
     ("hash_no_dtype", "^ ((uint64_t)dtype << 56)", "^ 0"),
     ("np_fail_ge", "const int fail = d > t;", "const int fail = d >= t;"),
     ("np_round_ties_up", "(frac == 0.5 && fmod(kr, 2.0) != 0.0)", "(frac == 0.5)"),
