@@ -33,6 +33,7 @@ namespace {
 constexpr int kPWaves = 4;
 constexpr int kPThreads = kPWaves * 64;
 constexpr int kRowWords = kHistBins / 4 + 1;  // 8-bit counters plus one pad word
+static_assert(kHistBins % 4 == 0, "the pad word's first byte is bin kHistBins");
 
 #define PRB_GLOBAL __attribute__((address_space(1)))
 
@@ -183,11 +184,52 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
   float mn = __builtin_inff(), mx = -__builtin_inff();
   uint32_t imn = 0xffffffffu, imx = 0xffffffffu;  // offsets from c0
   double sm = 0.0, sq = 0.0, sa = 0.0;
+  // the wave's extremes so far (uniform; valid once some element is finite)
+  float wmn = __builtin_inff(), wmx = -__builtin_inff();
+  bool have_ext = false;
   for (uint64_t b = w0; b < w1; b += ITER) {
     const uint64_t i0 = b + (uint64_t)lane * V;
-    const p32x4 q = (vec && b + ITER <= w1) ? pload16(T.data + i0 * ES)
-                                            : pload_guarded<DT>(T.data, i0, w1);
+    const bool full = vec && b + ITER <= w1;
+    const p32x4 q = full ? pload16(T.data + i0 * ES) : pload_guarded<DT>(T.data, i0, w1);
     const uint32_t o0 = (uint32_t)(i0 - c0);
+    if (full && have_ext) {
+      // Usual step: every element finite (an exponent field of all ones
+      // carries into the sign bit when its lowest bit is added) and none
+      // beyond the wave's extremes, so no lane's first minimum or maximum can
+      // change (an element equal to an extreme comes after it). Such a step
+      // only adds to the sums, counts and histogram, with no branch; a zero
+      // is counted in the row's spare byte (bin kHistBins).
+      constexpr uint32_t kMag = DT == VC_F32 ? 0x7fffffffu : 0x7fff7fffu;
+      constexpr uint32_t kTop = DT == VC_F32 ? 0x80000000u : 0x80008000u;
+      constexpr uint32_t kCarry =
+          DT == VC_F32 ? 0x00800000u : (DT == VC_BF16 ? 0x00800080u : 0x04000400u);
+      uint32_t nf = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) nf |= (q[w] & kMag) + kCarry;
+      float x[V];
+      float smn = __builtin_inff(), smx = -__builtin_inff();
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        x[j] = pdec<DT>(q, j);
+        smn = __builtin_fminf(smn, x[j]);
+        smx = __builtin_fmaxf(smx, x[j]);
+      }
+      if (__ballot((nf & kTop) != 0 || smn < wmn || smx > wmx) == 0) {
+        n_fin += V;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const double xd = (double)x[j];
+          sm += xd;
+          sq = __builtin_fma(xd, xd, sq);
+          sa += __builtin_fabs(xd);
+          const int e = (int)((__float_as_uint(x[j]) >> 23) & 0xffu);
+          const int bin =
+              x[j] == 0.0f ? kHistBins : min(max(e - 127 - kHistEmin + 1, 0), kHistBins - 1);
+          atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+        }
+        continue;
+      }
+    }
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       if (i0 + j >= w1) break;
@@ -219,7 +261,19 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
         atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
       }
     }
+    // raise the wave's extremes to the lanes' (lanes with no finite element
+    // hold +inf / -inf)
+    float a = mn, z = mx;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      a = __builtin_fminf(a, __shfl_xor(a, m));
+      z = __builtin_fmaxf(z, __shfl_xor(z, m));
+    }
+    wmn = a;
+    wmx = z;
+    have_ext = __ballot(imn != 0xffffffffu) != 0;
   }
+  n_zero += row[kRowWords - 1] & 0xffu;  // zeros of the usual steps
   // histogram: thread t sums bin t % 64 over the rows of lanes
   // (t / 64) * 64 .. + 63, then the four partial sums are added in order
   __syncthreads();
