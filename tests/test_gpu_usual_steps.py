@@ -1,0 +1,109 @@
+"""GPU parity of the probe and near-pass kernels on data shaped for their
+branch-free usual-step paths: long runs of finite, tame steps, with the
+events that must leave those paths planted late in a wave's range.
+
+Probe: a strict new minimum and maximum after many usual steps, ties of
+both extremes after them (the first index must win), zeros of both signs
+throughout (counted on the usual path in a spare histogram byte), binary16
+subnormals and one late NaN.
+
+Near-pass: pairs well inside the tolerance, with late failures, a late new
+largest ratio followed by an exact tie (first index), zeros of both signs
+(grid distance 0 between -0 and +0), opposite-sign pairs a few grid steps
+apart and one late infinity."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_02712_amd import vcheck as vc
+from tests import oracle_pins
+
+pytestmark = pytest.mark.gpu
+
+N = (1 << 20) + 77  # several chunks, a ragged tail
+DTYPES = (oracle.F32, oracle.F16, oracle.BF16)
+
+
+def _store(x, dt):
+    x = np.asarray(x, np.float32)
+    return x.view(np.uint32).copy() if dt == oracle.F32 else oracle_pins.to_raw16(x, dt)
+
+
+def _tensor(torch, raw, dt):
+    if dt == oracle.F32:
+        return torch.from_numpy(raw.view(np.float32).copy()).cuda()
+    t = torch.from_numpy(raw.view(np.int16).copy())
+    return t.view(torch.float16 if dt == oracle.F16 else torch.bfloat16).cuda()
+
+
+def _view(raw, dt):
+    return raw.view(np.float32) if dt == oracle.F32 else raw
+
+
+def _probe_data(rng):
+    x = rng.uniform(-1.0, 1.0, N).astype(np.float32)
+    zeros = rng.choice(N, N // 10, replace=False)
+    x[zeros] = np.where(rng.random(zeros.size) < 0.5, -0.0, 0.0).astype(np.float32)
+    x[rng.choice(N, 500, replace=False)] = 3e-7  # binary16 subnormal
+    # late strict extremes, then exact ties of both
+    x[700_001], x[700_003] = -5.0, 6.0
+    x[900_000], x[1_000_000] = -5.0, 6.0
+    x[N - 3] = np.nan
+    return x
+
+
+def test_probe_usual_steps_parity():
+    import torch
+
+    rng = np.random.default_rng(2608_71)
+    x = _probe_data(rng)
+    raws = [(_store(x, dt), dt) for dt in DTYPES]
+    print("probe usual steps: %d tensors of %d elements" % (len(raws), N), flush=True)
+    res = vc.vcheck_tensor_stats([_tensor(torch, raw, dt) for raw, dt in raws])
+    for (raw, dt), got in zip(raws, res):
+        want = oracle.tensor_stats(_view(raw, dt), dt)
+        for k in ("numel", "nan", "inf", "zero", "n_finite", "argmin", "argmax", "hist"):
+            assert got[k] == want[k], (dt, k, got[k], want[k])
+        for k in ("min", "max"):
+            assert np.float64(got[k]).tobytes() == np.float64(want[k]).tobytes(), (dt, k)
+        for k in ("sum", "sum_sq", "sum_abs"):
+            assert abs(got[k] - want[k]) <= 1e-6 * max(want["sum_abs"], want["sum_sq"]), (dt, k)
+        assert (got["argmin"], got["argmax"]) == (700_001, 700_003)
+        assert got["zero"] > N // 20  # most planted zeros survive the later plants
+
+
+def _nearpass_data(rng):
+    r = rng.uniform(0.5, 2.0, N).astype(np.float32) * np.where(rng.random(N) < 0.5, -1, 1)
+    c = (r * (1 + 1e-4 * rng.standard_normal(N))).astype(np.float32)
+    zeros = rng.choice(N, N // 20, replace=False)
+    r[zeros] = -0.0
+    c[zeros] = 0.0
+    # opposite signs a few grid steps apart around zero
+    tiny = rng.choice(N, 300, replace=False)
+    r[tiny], c[tiny] = 6e-8, -1.2e-7
+    # late failures, a late largest ratio and its exact tie
+    c[800_000] = r[800_000] + np.float32(0.25)
+    r[900_000], c[900_000] = 1.0, 1.5
+    r[950_000], c[950_000] = 1.0, 1.5
+    c[N - 5] = np.inf
+    return c, r
+
+
+@pytest.mark.parametrize("atol,rtol", [(1e-3, 1e-3), (0.0, 1e-2)])
+def test_nearpass_usual_steps_parity(atol, rtol):
+    import torch
+
+    rng = np.random.default_rng(2608_72)
+    c, r = _nearpass_data(rng)
+    cases = [(_store(c, dt), _store(r, dt), dt) for dt in DTYPES]
+    print("nearpass usual steps: %d cases of %d elements, atol %g rtol %g"
+          % (len(cases), N, atol, rtol), flush=True)
+    res = vc.vcheck_nearpass([(_tensor(torch, cr, dt), _tensor(torch, rr, dt))
+                              for cr, rr, dt in cases], atol, rtol)
+    for (cr, rr, dt), got in zip(cases, res):
+        want = oracle.nearpass(_view(cr, dt), _view(rr, dt), dt, atol, rtol)
+        for k in ("numel", "n_pairs", "n_fail", "n_zero_tol", "argmax_ratio", "max_ulp_fail",
+                  "ratio_hist", "ulp_hist"):
+            assert got[k] == want[k], (dt, k, got[k], want[k])
+        assert np.float64(got["max_ratio"]).tobytes() == np.float64(want["max_ratio"]).tobytes()
+        assert got["n_fail"] > 0 and got["argmax_ratio"] >= 0
