@@ -531,21 +531,23 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
     const p32x4 cq = full ? pload16(C.cand + i0 * ES) : pload_guarded<DT>(C.cand, i0, w1);
     const p32x4 rq = full ? pload16(C.ref + i0 * ES) : pload_guarded<DT>(C.ref, i0, w1);
     const uint32_t o0 = (uint32_t)(i0 - c0);
-    if constexpr (DT != VC_F32) {
-      // Usual step of 16-bit data: every pair finite, nothing failing and no
-      // candidate for the largest ratio (T >= 0 and d - T t <= 0, an exact
-      // sign). It only counts its pairs and their grid distances, without
-      // branches: a key's magnitude and sign are the pattern's, so equal
-      // signs give |hc - hr| and opposite signs the sum of the magnitudes.
+    {
+      // Usual step: every pair finite, nothing failing and no candidate for
+      // the largest ratio (T >= 0 and d - T t <= 0, an exact sign). It only
+      // counts its pairs and their grid distances, without branches: a key's
+      // magnitude and sign are the grid pattern's, so equal signs give
+      // |hc - hr| and opposite signs the sum of the magnitudes.
       if (full && T >= 0.0) {
-        // a half word is not finite when its exponent field is all ones:
-        // adding the field's lowest bit then carries into the sign bit
-        constexpr uint32_t kCarry = DT == VC_BF16 ? 0x00800080u : 0x04000400u;
+        // a value is not finite when its exponent field is all ones: adding
+        // the field's lowest bit then carries into the sign bit
+        constexpr uint32_t kMag = DT == VC_F32 ? 0x7fffffffu : 0x7fff7fffu;
+        constexpr uint32_t kTop = DT == VC_F32 ? 0x80000000u : 0x80008000u;
+        constexpr uint32_t kCarry =
+            DT == VC_F32 ? 0x00800000u : (DT == VC_BF16 ? 0x00800080u : 0x04000400u);
         uint32_t nf = 0;
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-          nf |= ((cq[w] & 0x7fff7fffu) + kCarry) | ((rq[w] & 0x7fff7fffu) + kCarry);
-        bool other = (nf & 0x80008000u) != 0;
+        for (int w = 0; w < 4; ++w) nf |= ((cq[w] & kMag) + kCarry) | ((rq[w] & kMag) + kCarry);
+        bool other = (nf & kTop) != 0;
 #pragma unroll
         for (int j = 0; j < V; ++j) {
           const double r = (double)pdec<DT>(rq, j);
@@ -560,7 +562,12 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
             const uint32_t hc = grid_bits<DT>(cq, j), hr = grid_bits<DT>(rq, j);
             const uint32_t dist = ((hc ^ hr) & 0x8000u) ? (hc & 0x7fffu) + (hr & 0x7fffu)
                                                         : (uint32_t)abs((int)hc - (int)hr);
-            const int ubin = kRatioBins + 31 - __builtin_clz(2u * dist + 1u);
+            int ubin = kRatioBins + 31 - __builtin_clz(2u * dist + 1u);
+            // binary32 values beyond the binary16 range sit outside the grid
+            if constexpr (DT == VC_F32)
+              ubin = ((hc & kExpMask) == kExpMask || (hr & kExpMask) == kExpMask)
+                         ? kRatioBins + kUlpBins - 1
+                         : ubin;
             atomicAdd(row + (ubin >> 2), 1u << ((ubin & 3) * 8));
           }
           continue;

@@ -10,7 +10,7 @@ subnormals and one late NaN.
 Near-pass: pairs well inside the tolerance, with late failures, a late new
 largest ratio followed by an exact tie (first index), zeros of both signs
 (grid distance 0 between -0 and +0), opposite-sign pairs a few grid steps
-apart and one late infinity."""
+apart, values beyond the binary16 range and one late infinity."""
 import numpy as np
 import pytest
 
@@ -26,7 +26,10 @@ DTYPES = (oracle.F32, oracle.F16, oracle.BF16)
 
 def _store(x, dt):
     x = np.asarray(x, np.float32)
-    return x.view(np.uint32).copy() if dt == oracle.F32 else oracle_pins.to_raw16(x, dt)
+    if dt == oracle.F32:
+        return x.view(np.uint32).copy()
+    with np.errstate(over="ignore"):  # beyond 65504 binary16 storage holds infinities
+        return oracle_pins.to_raw16(x, dt)
 
 
 def _tensor(torch, raw, dt):
@@ -81,6 +84,10 @@ def _nearpass_data(rng):
     # opposite signs a few grid steps apart around zero
     tiny = rng.choice(N, 300, replace=False)
     r[tiny], c[tiny] = 6e-8, -1.2e-7
+    # beyond the binary16 range (outside the grid for binary32 storage)
+    big = rng.choice(N, 400, replace=False)
+    r[big] = 1e5
+    c[big] = np.float32(1e5) * np.float32(1 + 1e-6)
     # late failures, a late largest ratio and its exact tie
     c[800_000] = r[800_000] + np.float32(0.25)
     r[900_000], c[900_000] = 1.0, 1.5
