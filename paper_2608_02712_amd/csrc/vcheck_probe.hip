@@ -534,9 +534,9 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
     {
       // Usual step: every pair finite, nothing failing and no candidate for
       // the largest ratio (T >= 0 and d - T t <= 0, an exact sign). It only
-      // counts its pairs and their grid distances, without branches: a key's
-      // magnitude and sign are the grid pattern's, so equal signs give
-      // |hc - hr| and opposite signs the sum of the magnitudes.
+      // counts its pairs and their grid distances, in one pass with no exit:
+      // a key's magnitude and sign are the grid pattern's, so equal signs
+      // give |hc - hr| and opposite signs the sum of the magnitudes.
       if (full && T >= 0.0) {
         // a value is not finite when its exponent field is all ones: adding
         // the field's lowest bit then carries into the sign bit
