@@ -109,7 +109,7 @@ def measure(cfg, steps, warmup, flush):
     from paper_2608_02712_amd import vcheck as vc
 
     t = time.perf_counter()
-    w = wl.CONFIGS[cfg]("cuda")
+    w = wl.WORKLOADS[cfg]("cuda")
     torch.cuda.synchronize()
     log("workload %d (%s) generated in %.1f s" % (cfg, w.name, time.perf_counter() - t))
     sw = vc.Sweep([(c.cand, c.ref, c.inputs) for c in w.cases], w.tols, primary=w.primary,

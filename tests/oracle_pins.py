@@ -326,12 +326,12 @@ def pin_invariants(lib):
         assert a.stats[key] + b.stats[key] == whole.stats[key], key
 
 
-def pin_config1(lib):
+def pin_fp32_single(lib):
     """Closed form of workload 1 at full size: 1536 mismatches (rows
     1000-1023 x cols 960-1023), first 64 = 1024960..1025023, tile map 768 at
     tiles (31,30) and (31,31) and 0 elsewhere, max_abs = max |ref| over the
     zeroed block."""
-    w = wl.config1(device="cpu")
+    w = wl.fp32_single(device="cpu")
     case = w.cases[0]
     cand, ref = case.cand.numpy(), case.ref.numpy()
     block = np.abs(ref[1000:, 960:].astype(np.float64))
@@ -346,11 +346,11 @@ def pin_config1(lib):
     assert st["nan_cand"] == st["inf_cand"] == 0 and st["n_finite"] == 1024 * 1024
 
 
-def pin_config2(lib):
+def pin_fp16_batch(lib):
     """Workload 2 structure (4 cases of 256x256): per case 4096 shifted-tile
     mismatches + 3 NaNs = 4099, nan_cand = 3, tile map = 4096 at the shifted
     tile plus one per NaN in its tile; first-k = the smallest fault indices."""
-    w = wl.config2(device="cpu", n_cases=4, rows=256, cols=256)
+    w = wl.fp16_batch(device="cpu", n_cases=4, rows=256, cols=256)
     for case, f in zip(w.cases, w.meta["faults"]):
         cand, ref = wl.raw_numpy(case.cand), wl.raw_numpy(case.ref)
         res = oracle.validate_case(cand, ref, F16, (256, 256), w.tols, tile=w.tile, k=w.k, lib=lib)
@@ -366,11 +366,11 @@ def pin_config2(lib):
         assert res.first_k.tolist() == expect_k
 
 
-def pin_config3(lib):
+def pin_bf16_bursts(lib):
     """Workload 3 structure (2x256x512 bf16): inf_cand = 512 and mismatches =
     512 + the scaled faults that torch.isclose rejects; the rest is
     bit-identical, so max_abs is attained at a scaled fault."""
-    w = wl.config3(device="cpu", shape=(2, 256, 512), fault_fraction=1e-4)
+    w = wl.bf16_bursts(device="cpu", shape=(2, 256, 512), fault_fraction=1e-4)
     case = w.cases[0]
     cand, ref = wl.raw_numpy(case.cand).reshape(-1), wl.raw_numpy(case.ref).reshape(-1)
     res = oracle.validate_case(cand, ref, BF16, (2, 256, 512), w.tols, tile=w.tile, k=w.k, lib=lib)
@@ -386,12 +386,12 @@ def pin_config3(lib):
     assert res.first_k.tolist() == fails[:64]
 
 
-def pin_config4(lib):
+def pin_fp32_sweep(lib):
     """Workload 4 structure (40 odd-shaped cases, 2^14 elements max): at
     pairs 1e-4 and 1e-3 the mismatches are exactly the injected faults, which
     all sit in the last tile; first-k lists them; counts are monotone across
     the 4 pairs; the suite match rate at (1e-3, 1e-3) is 20/40."""
-    w = wl.config4(device="cpu", n_cases=40, max_log2=14, n_cauchy=4, n_faulted=20,
+    w = wl.fp32_sweep(device="cpu", n_cases=40, max_log2=14, n_cauchy=4, n_faulted=20,
                    fixed=[(1, 7), (3, 1003), (257, 51), (1, 1)])
     mism, status = [], []
     for i, case in enumerate(w.cases):
@@ -411,12 +411,12 @@ def pin_config4(lib):
     assert all(a <= b for a, b in zip(rate, rate[1:])), rate
 
 
-def pin_config5(lib):
+def pin_fp32_integrity(lib):
     """Workload 5 classes (20 cases of 64x64): each class raises exactly its
     flag (correct: none, copy: INPUT_COPY with copy_input 0, zero: ALL_ZERO,
     constant: CONSTANT, bf16: LOWPREC_BF16); the zero class has max_rel 1.0
     and sum_abs = fsum |ref|; the certified match rate is #correct / 20."""
-    w = wl.config5(device="cpu", n_cases=20, rows=64, cols=64)
+    w = wl.fp32_integrity(device="cpu", n_cases=20, rows=64, cols=64)
     want_flag = {wl.CLASS_CORRECT: 0, wl.CLASS_COPY: oracle.FLAG_INPUT_COPY,
                  wl.CLASS_ZERO: oracle.FLAG_ALL_ZERO, wl.CLASS_CONSTANT: oracle.FLAG_CONSTANT,
                  wl.CLASS_BF16: oracle.FLAG_LOWPREC_BF16}
@@ -795,5 +795,5 @@ PINS = [
     pin_tstats_handbuilt, pin_tstats_numpy,
     pin_gate_ties, pin_suite_handbuilt, pin_flags_handbuilt, pin_decode, pin_no_fma,
     pin_metrics_numpy, pin_gate_isclose, pin_localize_numpy, pin_invariants, pin_integrity_counts,
-    pin_config5, pin_config4, pin_config2, pin_config3, pin_config1,
+    pin_fp32_integrity, pin_fp32_sweep, pin_fp16_batch, pin_bf16_bursts, pin_fp32_single,
 ]

@@ -36,8 +36,8 @@ def check_case(res, w, i, tag):
     return o
 
 
-def test_config1_full():
-    w = wl.config1("cuda")
+def test_fp32_single_full():
+    w = wl.fp32_single("cuda")
     ref = w.cases[0].ref
     assert ref[1000:, 960:].abs().min().item() > 2e-5
     res = run_sweep(w)
@@ -50,8 +50,8 @@ def test_config1_full():
     assert res["match_rate"].tolist() == [0.0]
 
 
-def test_config2_full():
-    w = wl.config2("cuda")
+def test_fp16_batch_full():
+    w = wl.fp16_batch("cuda")
     res = run_sweep(w)
     for i in (0, 17, 41, 63):
         check_case(res, w, i, "cfg2 case %d" % i)
@@ -64,8 +64,8 @@ def test_config2_full():
     assert res["match_rate"].tolist() == [0.0]
 
 
-def test_config3_full():
-    w = wl.config3("cuda")
+def test_bf16_bursts_full():
+    w = wl.bf16_bursts("cuda")
     res = run_sweep(w)
     o = check_case(res, w, 0, "cfg3")
     assert res["stats"][0]["inf_cand"] == 512
@@ -76,8 +76,8 @@ def test_config3_full():
     assert o.mismatches == [512 + int(bad.sum())]
 
 
-def test_config4_full():
-    w = wl.config4("cuda")
+def test_fp32_sweep_full():
+    w = wl.fp32_sweep("cuda")
     res = run_sweep(w)
     sample = sorted(set(range(5)) | set(range(5, 500, 9)) | set(w.meta["faulted"][:20]))
     for i in sample:
@@ -92,8 +92,8 @@ def test_config4_full():
     assert res["match_rate"][3] == 0.5 and res["match_rate"][2] == 0.5
 
 
-def test_config5_full():
-    w = wl.config5("cuda")
+def test_fp32_integrity_full():
+    w = wl.fp32_integrity("cuda")
     res = run_sweep(w)
     classes = w.meta["classes"]
     want = {wl.CLASS_CORRECT: 0, wl.CLASS_COPY: vc.FLAG_INPUT_COPY, wl.CLASS_ZERO: vc.FLAG_ALL_ZERO,

@@ -88,7 +88,7 @@ def _distinct(rng: np.random.Generator, n: int, count: int, reject=None) -> np.n
 
 
 # --------------------------------------------------------------------------- 1
-def config1(device="cuda", rows: int = 1024, cols: int = 1024, seed: int | None = None) -> Workload:
+def fp32_single(device="cuda", rows: int = 1024, cols: int = 1024, seed: int | None = None) -> Workload:
     """fp32 single case; ref ~ N(0,1), cand = ref + 1e-7 N(0,1); the last 24
     rows x last 64 cols of cand are set to 0.0 (rows 1000-1023, cols 960-1023
     at full size). atol = rtol = 1e-5, 32x32 tiles, first-k = 64."""
@@ -104,7 +104,7 @@ def config1(device="cuda", rows: int = 1024, cols: int = 1024, seed: int | None 
 
 
 # --------------------------------------------------------------------------- 2
-def config2(device="cuda", n_cases: int = 64, rows: int = 2048, cols: int = 2048,
+def fp16_batch(device="cuda", n_cases: int = 64, rows: int = 2048, cols: int = 2048,
             tile: int = 64, seed: int | None = None) -> Workload:
     """fp16 batch. Per case: r32 ~ N(0,1), ref = fp16(r32), cand =
     fp16(r32 + 1e-4 N(0,1)); one seeded tile-aligned 64x64 block gets
@@ -140,7 +140,7 @@ def config2(device="cuda", n_cases: int = 64, rows: int = 2048, cols: int = 2048
 
 
 # --------------------------------------------------------------------------- 3
-def config3(device="cuda", shape=(4, 8192, 8192), burst: int = 512, seed: int | None = None,
+def bf16_bursts(device="cuda", shape=(4, 8192, 8192), burst: int = 512, seed: int | None = None,
             fault_fraction: float = 1e-6) -> Workload:
     """bf16 single large case. ref = bf16(U(-4,4)); cand = bf16(fp32(ref)),
     bit-identical to ref; floor(1e-6 n) seeded positions get
@@ -175,7 +175,7 @@ CONFIG4_FIXED_SHAPES = [(1, 7), (3, 1000003), (257, 513), (1, 1), (1, 16777216)]
 CONFIG4_TOLS = [(1e-6, 1e-6, 0), (1e-5, 1e-5, 0), (1e-4, 1e-4, 0), (1e-3, 1e-3, 0)]
 
 
-def config4_shapes(n_cases: int = 500, max_log2: int = 24, seed: int | None = None,
+def fp32_sweep_shapes(n_cases: int = 500, max_log2: int = 24, seed: int | None = None,
                    fixed=CONFIG4_FIXED_SHAPES):
     """Seeded odd shapes: log2(numel) ~ U(0, max_log2), R = 2^U(0, log2 numel),
     C = ceil(numel / R) forced odd, R*C <= 2^max_log2. The fixed shapes come
@@ -206,7 +206,7 @@ def _aligned_offsets(sizes, align_elems: int):
     return offs, cur
 
 
-def config4(device="cuda", n_cases: int = 500, max_log2: int = 24, tile: int = 64,
+def fp32_sweep(device="cuda", n_cases: int = 500, max_log2: int = 24, tile: int = 64,
             n_cauchy: int = 50, n_faulted: int = 250, seed: int | None = None,
             fixed=CONFIG4_FIXED_SHAPES) -> Workload:
     """fp32 coverage sweep. ref ~ N(0,1) except n_cauchy seeded cases with
@@ -217,7 +217,7 @@ def config4(device="cuda", n_cases: int = 500, max_log2: int = 24, tile: int = 6
     pair (1e-3, 1e-3), 64x64 tiles, first-k = 64. Cases are packed into one
     buffer at 256-byte aligned offsets."""
     seed = config_seed(4) if seed is None else seed
-    shapes = config4_shapes(n_cases, max_log2, seed, fixed)
+    shapes = fp32_sweep_shapes(n_cases, max_log2, seed, fixed)
     rng = _rng(seed + 100000)
     cauchy = set(rng.choice(n_cases, size=min(n_cauchy, n_cases), replace=False).tolist())
     faulted = set(rng.choice(n_cases, size=min(n_faulted, n_cases), replace=False).tolist())
@@ -261,7 +261,7 @@ CLASS_CORRECT, CLASS_COPY, CLASS_ZERO, CLASS_CONSTANT, CLASS_BF16 = range(5)
 CLASS_NAMES = ["correct", "input_copy", "all_zero", "constant", "bf16_computed"]
 
 
-def config5_classes(n_cases: int = 256, seed: int | None = None) -> np.ndarray:
+def fp32_integrity_classes(n_cases: int = 256, seed: int | None = None) -> np.ndarray:
     """Seeded shuffle of n slots assigning class (slot mod 5)."""
     seed = config_seed(5) if seed is None else seed
     classes = np.arange(n_cases) % 5
@@ -269,14 +269,14 @@ def config5_classes(n_cases: int = 256, seed: int | None = None) -> np.ndarray:
     return classes
 
 
-def config5(device="cuda", n_cases: int = 256, rows: int = 4096, cols: int = 4096,
+def fp32_integrity(device="cuda", n_cases: int = 256, rows: int = 4096, cols: int = 4096,
             seed: int | None = None) -> Workload:
     """fp32 integrity batch. Per case: x ~ N(0,1), ref = x*0.5 + 1 (fp32);
     cand by class: correct = ref + 1e-7 N(0,1); input copy = x; all-zero;
     constant fill 1.0; bf16-computed = fp32(bf16(bf16(bf16(x)*0.5) + 1)).
     atol = rtol = 1e-5; the detectors get x as operator input 0."""
     seed = config_seed(5) if seed is None else seed
-    classes = config5_classes(n_cases, seed)
+    classes = fp32_integrity_classes(n_cases, seed)
     x_all = torch.empty(n_cases, rows, cols, device=device, dtype=torch.float32)
     ref_all = torch.empty_like(x_all)
     cand_all = torch.empty_like(x_all)
@@ -303,7 +303,7 @@ def config5(device="cuda", n_cases: int = 256, rows: int = 4096, cols: int = 409
                     integrity=True, meta={"classes": classes})
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
+WORKLOADS = {1: fp32_single, 2: fp16_batch, 3: bf16_bursts, 4: fp32_sweep, 5: fp32_integrity}
 
 
 def raw_numpy(t: torch.Tensor) -> np.ndarray:
