@@ -395,8 +395,8 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build validates on a single MI355X "
-              "(--gpus 1); multi-GPU runs are not part of it.", file=sys.stderr)
+        print("bench.py measures one GPU only: the validation path runs on a single MI355X "
+              "(--gpus 1); runs on several GPUs are not measured.", file=sys.stderr)
         sys.exit(2)
 
     import torch
