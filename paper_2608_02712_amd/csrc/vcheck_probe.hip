@@ -184,21 +184,23 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
   float mn = __builtin_inff(), mx = -__builtin_inff();
   uint32_t imn = 0xffffffffu, imx = 0xffffffffu;  // offsets from c0
   double sm = 0.0, sq = 0.0, sa = 0.0;
-  // the wave's extremes so far (uniform; valid once some element is finite)
+  // the wave's extremes so far (uniform; +inf / -inf before any finite
+  // element)
   float wmn = __builtin_inff(), wmx = -__builtin_inff();
-  bool have_ext = false;
   for (uint64_t b = w0; b < w1; b += ITER) {
     const uint64_t i0 = b + (uint64_t)lane * V;
     const bool full = vec && b + ITER <= w1;
     const p32x4 q = full ? pload16(T.data + i0 * ES) : pload_guarded<DT>(T.data, i0, w1);
     const uint32_t o0 = (uint32_t)(i0 - c0);
-    if (full && have_ext) {
+    if (full) {
       // Usual step: every element finite (an exponent field of all ones
-      // carries into the sign bit when its lowest bit is added) and none
-      // beyond the wave's extremes, so no lane's first minimum or maximum can
-      // change (an element equal to an extreme comes after it). Such a step
-      // only adds to the sums, counts and histogram, with no branch; a zero
-      // is counted in the row's spare byte (bin kHistBins).
+      // carries into the sign bit when its lowest bit is added). It adds to
+      // the sums, counts and histogram with no branch per element (a zero is
+      // counted in the row's spare byte, bin kHistBins). When no element lies
+      // beyond the wave's extremes no lane's first minimum or maximum can
+      // change (an element equal to an extreme comes after it); otherwise the
+      // lanes take their new extremes by selects, in index order, and the
+      // wave's extremes are raised.
       constexpr uint32_t kMag = DT == VC_F32 ? 0x7fffffffu : 0x7fff7fffu;
       constexpr uint32_t kTop = DT == VC_F32 ? 0x80000000u : 0x80008000u;
       constexpr uint32_t kCarry =
@@ -206,15 +208,15 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
       uint32_t nf = 0;
 #pragma unroll
       for (int w = 0; w < 4; ++w) nf |= (q[w] & kMag) + kCarry;
-      float x[V];
-      float smn = __builtin_inff(), smx = -__builtin_inff();
+      if (__ballot((nf & kTop) != 0) == 0) {
+        float x[V];
+        float smn = __builtin_inff(), smx = -__builtin_inff();
 #pragma unroll
-      for (int j = 0; j < V; ++j) {
-        x[j] = pdec<DT>(q, j);
-        smn = __builtin_fminf(smn, x[j]);
-        smx = __builtin_fmaxf(smx, x[j]);
-      }
-      if (__ballot((nf & kTop) != 0 || smn < wmn || smx > wmx) == 0) {
+        for (int j = 0; j < V; ++j) {
+          x[j] = pdec<DT>(q, j);
+          smn = __builtin_fminf(smn, x[j]);
+          smx = __builtin_fmaxf(smx, x[j]);
+        }
         n_fin += V;
 #pragma unroll
         for (int j = 0; j < V; ++j) {
@@ -226,6 +228,26 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
           const int bin =
               x[j] == 0.0f ? kHistBins : min(max(e - 127 - kHistEmin + 1, 0), kHistBins - 1);
           atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+        }
+        if (__ballot(smn < wmn || smx > wmx) != 0) {
+          // every element is finite: the first one beats the lane's +inf /
+          // -inf start, so no "no extreme yet" test is needed
+#pragma unroll
+          for (int j = 0; j < V; ++j) {
+            const bool lo = x[j] < mn, hi = x[j] > mx;
+            mn = lo ? x[j] : mn;
+            imn = lo ? o0 + (uint32_t)j : imn;
+            mx = hi ? x[j] : mx;
+            imx = hi ? o0 + (uint32_t)j : imx;
+          }
+          float a = mn, z = mx;
+#pragma unroll
+          for (int m = 32; m >= 1; m >>= 1) {
+            a = __builtin_fminf(a, __shfl_xor(a, m));
+            z = __builtin_fmaxf(z, __shfl_xor(z, m));
+          }
+          wmn = a;
+          wmx = z;
         }
         continue;
       }
@@ -271,7 +293,6 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
     }
     wmn = a;
     wmx = z;
-    have_ext = __ballot(imn != 0xffffffffu) != 0;
   }
   n_zero += row[kRowWords - 1] & 0xffu;  // zeros of the usual steps
   // histogram: thread t sums bin t % 64 over the rows of lanes
