@@ -3,7 +3,7 @@
 Each round draws a batch of cases: storage type, rank and shape (0-d,
 empty, ragged, up to a few hundred thousand elements), data mixing random
 bit patterns of every class, near pairs, shifted blocks, bursts of NaN, Inf
-and signed zeros and bit-equal pairs, and random options (one to four
+and signed zeros and bit-equal pairs, and random options (one to eight
 tolerance pairs with or without equal_nan, primary pair, tile shape or none,
 first-k length, detectors on or off). vcheck_sweep must match the oracle
 field for field; the probe, near-pass and content-hash kernels are checked
@@ -71,7 +71,7 @@ def test_random_sweeps(seed):
             c, r = _pairs(rng, int(np.prod(shape)), dt)
             ct, rt = to_device(c, dt, shape), to_device(r, dt, shape)
             cases.append((ct, rt, [ct.clone()] if rng.random() < 0.2 else []))
-        nt = int(rng.integers(1, 5))
+        nt = int(rng.integers(1, 9))
         tols = [(float(rng.choice([0.0, 1e-6, 1e-4, 1e-3, 1e-2])),
                  float(rng.choice([0.0, 1e-6, 1e-4, 1e-3, 1e-2])), int(rng.integers(0, 2)))
                 for _ in range(nt)]

@@ -51,16 +51,26 @@ def test_fp32_single_full():
 
 
 def test_fp16_batch_full():
+    """Every case through the oracle, and every case's tile map and first-k
+    against the closed form of its faults: the shifted tile (4096
+    mismatches) plus one per planted NaN, nothing else."""
     w = wl.fp16_batch("cuda")
     res = run_sweep(w)
-    for i in (0, 17, 41, 63):
-        check_case(res, w, i, "cfg2 case %d" % i)
+    rows = cols = 2048
+    t = w.meta["tile_size"]
     for i, f in enumerate(w.meta["faults"]):
+        check_case(res, w, i, "cfg2 case %d" % i)
         st = res["stats"][i]
         assert st["mismatches"] == 4099 and st["nan_cand"] == 3, i
-        tm = res["tile_maps"][i].reshape(32, 32)
         ti, tj = f["tile"]
-        assert tm[ti, tj] >= 4096 and int(tm.sum()) == 4099
+        want = np.zeros((rows // t, cols // t), dtype=np.uint32)
+        want[ti, tj] = t * t
+        for p in f["nans"]:
+            want[(p // cols) // t, (p % cols) // t] += 1
+        assert np.array_equal(res["tile_maps"][i].reshape(want.shape), want), i
+        blk = ((ti * t + np.arange(t))[:, None] * cols + tj * t + np.arange(t)[None, :]).ravel()
+        fk = np.sort(np.concatenate([blk, np.asarray(f["nans"], dtype=np.int64)]))[:w.k]
+        assert res["first_k"][i].tolist() == fk.tolist(), i
     assert res["match_rate"].tolist() == [0.0]
 
 
