@@ -144,7 +144,10 @@ struct Plan {
 #define VCK_SPLIT 2
 #endif
 uint32_t split_for(int32_t dtype) {
-  return VCK_SPLIT == 2 ? (dtype == VC_F32 ? 0u : 1u) : (uint32_t)VCK_SPLIT;
+  if (VCK_SPLIT == 2) return dtype == VC_F32 ? 0u : 1u;
+  if (VCK_SPLIT == 3) return 2u;
+  if (VCK_SPLIT == 4) return dtype == VC_F32 ? 0u : 2u;
+  return (uint32_t)VCK_SPLIT;
 }
 
 uint32_t unit_for(uint64_t group_elems, int32_t dtype) {

@@ -12,7 +12,7 @@ namespace vck {
 constexpr int kWaveSize = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWaveSize * kWavesPerBlock;
-constexpr int kTileWindow = 2048;  // LDS tile counters per block
+constexpr int kTileWindow = 1024;  // LDS tile counters per block
 constexpr int kGroupChunks = 256;  // chunks merged by one group record
 
 // Unsigned division of a 32-bit numerator by an invariant divisor d

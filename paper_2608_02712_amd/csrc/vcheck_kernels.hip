@@ -314,6 +314,38 @@ __device__ __forceinline__ float diff32(const u32x4 &cq, const u32x4 &rq, int j)
   }
 }
 
+// Binary16 operands of the mixed-precision FMA: the half SEL (0 low, 1 high)
+// of a storage word enters v_fma_mix_f32 as an exactly converted binary32
+// value, so these take no separate conversion.
+// fma(|r|, |x|, y) with r the binary16 half SEL of rw.
+template <int SEL>
+__device__ __forceinline__ float h_fma_rx(uint32_t rw, float x, float y) {
+  float g;
+  if constexpr (SEL)
+    asm("v_fma_mix_f32 %0, |%1|, |%2|, %3 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+        : "=v"(g) : "v"(rw), "v"(x), "v"(y));
+  else
+    asm("v_fma_mix_f32 %0, |%1|, |%2|, %3 op_sel_hi:[1,0,0]" : "=v"(g) : "v"(rw), "v"(x), "v"(y));
+  return g;
+}
+// |r| * |x| with r the binary16 half SEL of rw.
+template <int SEL>
+__device__ __forceinline__ float h_mul_rx(uint32_t rw, float x) {
+  float g;
+  if constexpr (SEL)
+    asm("v_fma_mix_f32 %0, |%1|, |%2|, 0 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+        : "=v"(g) : "v"(rw), "v"(x));
+  else
+    asm("v_fma_mix_f32 %0, |%1|, |%2|, 0 op_sel_hi:[1,0,0]" : "=v"(g) : "v"(rw), "v"(x));
+  return g;
+}
+// |r_lo| * |r_hi| of the two binary16 halves of rw (exact: 22 significant bits).
+__device__ __forceinline__ float h_prod(uint32_t rw) {
+  float g;
+  asm("v_fma_mix_f32 %0, |%1|, |%1|, 0 op_sel:[0,1,0] op_sel_hi:[1,1,0]" : "=v"(g) : "v"(rw));
+  return g;
+}
+
 // Largest binary32 value <= x, for x = -1 or x >= 0 (the running-maximum
 // thresholds); values above the binary32 range give FLT_MAX.
 __device__ __forceinline__ float f32_down(double x) {
@@ -321,6 +353,12 @@ __device__ __forceinline__ float f32_down(double x) {
   float f = (float)x;
   if ((double)f > x) f = __uint_as_float(__float_as_uint(f) - 1u);
   return f;
+}
+
+// Smallest binary32 value > x, for finite x (x = -1 or x >= 0 here).
+__device__ __forceinline__ float f32_next_up(float x) {
+  const uint32_t b = __float_as_uint(x);
+  return x >= 0.0f ? __uint_as_float((b & 0x7fffffffu) + 1u) : __uint_as_float(b - 1u);
 }
 
 // ------------------------------------------------------------ merge helpers
@@ -661,6 +699,8 @@ void main_kernel(const Params P) {
   // binary32 tier: bound on the estimate of |c - r| / |r| under which c - r
   // is exact in binary32 (with a margin for the estimate's error)
   constexpr float QT = ES == 4 ? 0.49f : 0.998f;
+  // the tier-1 range of |r| as strict bounds: 2^-60 <= |r| <= 2^30
+  constexpr float kRangeHiUp = 0x1.000002p30f, kRangeLoDown = 0x1.fffffep-61f;
 
   struct StreamLds {
     uint32_t win[kTileWindow];    // block tile-count window
@@ -732,16 +772,45 @@ void main_kernel(const Params P) {
     rtol[p] = P.rtol[p];
   }
   const float rlo = P.rlo, alo = P.alo, rhi = P.rhi, ahi = P.ahi;
+  const float alo_up = f32_next_up(alo);
 
-  // per-lane exact best (value, chunk offset) and binary64 sums
-  double lb_abs = -1.0, lb_rel = -1.0;
-  uint32_t li_abs = kNone, li_rel = kNone;
+  // Per-lane exact best (value, chunk offset) of d (k = 0) and of the
+  // quotient (k = 1), kept in LDS: only the rare update paths touch them, so
+  // the streaming loop carries no registers for them.
+  __shared__ double s_bv[2][kWavesPerBlock][kWaveSize];
+  __shared__ uint32_t s_bi[2][kWavesPerBlock][kWaveSize];
+  s_bv[0][wave][lane] = -1.0;
+  s_bv[1][wave][lane] = -1.0;
+  s_bi[0][wave][lane] = kNone;
+  s_bi[1][wave][lane] = kNone;
+  // per-lane binary64 sums
   double acc_abs = 0.0, acc_rel = 0.0;
-  // wave-uniform thresholds: the wave's best values so far (-1: none), and
-  // their binary32 images rounded down
-  double T_abs = -1.0, T_rel = -1.0;
-  float thr_abs = -1.0f, b_rel = -1.0f;
-  bool rel_zero = false;  // the wave's best quotient is 0: any d > 0 beats it
+  // Wave-uniform running thresholds, kept in LDS: the rare update paths
+  // (raise_abs, raise_rel) write them and every step reads a snapshot, so
+  // the streaming loop carries no registers for them.
+  //  T_abs, T_rel   the wave's best d and quotient so far (-1: none);
+  //  thr_abs        T_abs rounded down to binary32, thr_abs_up the next float;
+  //  b_rel          T_rel lowered by 2^-20 and rounded down (0 when T_rel = 0);
+  //  rel_zero       T_rel == 0: any d > 0 beats it;
+  //  b_mul, s_rel   the single-pair quotient screen: an element passes when
+  //                 |d| - b_mul |r| < s_rel, b_mul = b_rel (binary32 /
+  //                 bfloat16 storage: at most the exactness bound QT), or 0
+  //                 with s_rel = 2^-149 while T_rel = 0 (any d > 0 is caught).
+  struct WaveThr {
+    double T_abs, T_rel;
+    float thr_abs, thr_abs_up, b_rel, b_mul, s_rel;
+    uint32_t rel_zero;
+  };
+  __shared__ WaveThr s_thr[kWavesPerBlock];
+  {
+    WaveThr t;
+    t.T_abs = t.T_rel = -1.0;
+    t.thr_abs = t.b_rel = t.b_mul = -1.0f;
+    t.thr_abs_up = f32_next_up(-1.0f);
+    t.s_rel = 0.0f;
+    t.rel_zero = 0;
+    s_thr[wave] = t;
+  }
   // wave-uniform counters
   uint32_t mism[NT];
 #pragma unroll
@@ -879,20 +948,28 @@ void main_kernel(const Params P) {
 
   // Raise the wave thresholds to the lanes' bests (after an update).
   auto raise_abs = [&](uint64_t lanes) __attribute__((always_inline)) {
+    const double lb_abs = s_bv[0][wave][lane];
     const double v = popc(lanes) == 1 ? readlane_f64(lb_abs, (uint32_t)__builtin_ctzll(lanes))
                                       : wave_max_val(lb_abs);
-    if (v > T_abs) {
-      T_abs = v;
-      thr_abs = f32_down(v);
+    if (v > s_thr[wave].T_abs) {
+      const float t = f32_down(v);
+      s_thr[wave].T_abs = v;
+      s_thr[wave].thr_abs = t;
+      s_thr[wave].thr_abs_up = f32_next_up(t);
     }
   };
   auto raise_rel = [&](uint64_t lanes) __attribute__((always_inline)) {
+    const double lb_rel = s_bv[1][wave][lane];
     const double v = popc(lanes) == 1 ? readlane_f64(lb_rel, (uint32_t)__builtin_ctzll(lanes))
                                       : wave_max_val(lb_rel);
-    if (v > T_rel) {
-      T_rel = v;
-      b_rel = v > 0.0 ? f32_down(v * (1.0 - 0x1p-20)) : 0.0f;
-      rel_zero = !(v > 0.0);
+    if (v > s_thr[wave].T_rel) {
+      const bool zero = !(v > 0.0);
+      const float b = zero ? 0.0f : f32_down(v * (1.0 - 0x1p-20));
+      s_thr[wave].T_rel = v;
+      s_thr[wave].b_rel = b;
+      s_thr[wave].rel_zero = zero ? 1u : 0u;
+      s_thr[wave].b_mul = zero ? 0.0f : (DT != VC_F16 ? __builtin_fminf(b, QT) : b);
+      s_thr[wave].s_rel = zero ? 0x1p-149f : 0.0f;
     }
   };
   // Tier-1 update of the lane bests for the lanes in absm | relm, given each
@@ -904,15 +981,17 @@ void main_kernel(const Params P) {
   // of them (usually one) is divided exactly in binary64 and compared.
   auto t1_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t absm, uint64_t relm,
                        uint32_t off0, float md, float mq) __attribute__((always_inline)) {
-    if (((absm >> lane) & 1ull) && (double)md > lb_abs) {
+    if (((absm >> lane) & 1ull) && (double)md > s_bv[0][wave][lane]) {
       uint32_t jb = 0;
 #pragma unroll 1
       for (int j = V - 1; j >= 0; --j)
         if (__builtin_fabsf(diff32<DT>(cq, rq, j)) == md) jb = (uint32_t)j;
-      lb_abs = md;
-      li_abs = off0 + jb;
+      s_bv[0][wave][lane] = md;
+      s_bi[0][wave][lane] = off0 + jb;
     }
     if ((relm >> lane) & 1ull) {
+      double lb_rel = s_bv[1][wave][lane];
+      uint32_t li_rel = s_bi[1][wave][lane];
       const float band = mq * (1.0f - 0x1p-19f);
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
@@ -926,6 +1005,51 @@ void main_kernel(const Params P) {
           }
         }
       }
+      s_bv[1][wave][lane] = lb_rel;
+      s_bi[1][wave][lane] = li_rel;
+    }
+    if (absm != 0) raise_abs(absm);
+    if (relm != 0) raise_rel(relm);
+  };
+
+  // Single-pair variant of t1_update: the lanes in relm have a quotient pair
+  // sum at or above the screen threshold, so each computes its elements'
+  // quotient estimates first (largest mq), then proceeds as t1_update.
+  auto t1_update1 = [&](const u32x4 &cq, const u32x4 &rq, uint64_t absm, uint64_t relm,
+                        uint32_t off0, float md) __attribute__((always_inline)) {
+    if (((absm >> lane) & 1ull) && (double)md > s_bv[0][wave][lane]) {
+      uint32_t jb = 0;
+#pragma unroll 1
+      for (int j = V - 1; j >= 0; --j)
+        if (__builtin_fabsf(diff32<DT>(cq, rq, j)) == md) jb = (uint32_t)j;
+      s_bv[0][wave][lane] = md;
+      s_bi[0][wave][lane] = off0 + jb;
+    }
+    if ((relm >> lane) & 1ull) {
+      double lb_rel = s_bv[1][wave][lane];
+      uint32_t li_rel = s_bi[1][wave][lane];
+      float mq = 0.0f;
+#pragma unroll 1
+      for (int j = 0; j < V; ++j) {
+        const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+        const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+        mq = __builtin_fmaxf(mq, d * __builtin_amdgcn_rcpf(a));
+      }
+      const float band = mq * (1.0f - 0x1p-19f);
+#pragma unroll 1
+      for (int j = 0; j < V; ++j) {
+        const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+        const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+        if (d * __builtin_amdgcn_rcpf(a) >= band) {
+          const double q = (double)d / (double)a;
+          if (q > lb_rel) {
+            lb_rel = q;
+            li_rel = off0 + (uint32_t)j;
+          }
+        }
+      }
+      s_bv[1][wave][lane] = lb_rel;
+      s_bi[1][wave][lane] = li_rel;
     }
     if (absm != 0) raise_abs(absm);
     if (relm != 0) raise_rel(relm);
@@ -937,6 +1061,8 @@ void main_kernel(const Params P) {
   auto abs_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
                         __attribute__((always_inline)) {
     if ((lanes >> lane) & 1ull) {
+      double lb_abs = s_bv[0][wave][lane];
+      uint32_t li_abs = s_bi[0][wave][lane];
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
         const double d = __builtin_fabs(dec64<DT>(elem<DT>(cq, j)) - dec64<DT>(elem<DT>(rq, j)));
@@ -946,12 +1072,16 @@ void main_kernel(const Params P) {
           li_abs = o;
         }
       }
+      s_bv[0][wave][lane] = lb_abs;
+      s_bi[0][wave][lane] = li_abs;
     }
     raise_abs(lanes);
   };
   auto rel_update = [&](const u32x4 &cq, const u32x4 &rq, uint64_t lanes, uint32_t off0)
                         __attribute__((always_inline)) {
     if ((lanes >> lane) & 1ull) {
+      double lb_rel = s_bv[1][wave][lane];
+      uint32_t li_rel = s_bi[1][wave][lane];
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
         const double r = dec64<DT>(elem<DT>(rq, j));
@@ -968,6 +1098,8 @@ void main_kernel(const Params P) {
           }
         }
       }
+      s_bv[1][wave][lane] = lb_rel;
+      s_bi[1][wave][lane] = li_rel;
     }
     raise_rel(lanes);
   };
@@ -980,6 +1112,8 @@ void main_kernel(const Params P) {
     uint32_t pb = 0;
     uint32_t nan_c_step = 0, nan_r_step = 0, inf_c_step = 0, inf_r_step = 0;
     uint32_t fin_step = 0, rel_step = 0, undef_step = 0;
+    double lb_abs = s_bv[0][wave][lane], lb_rel = s_bv[1][wave][lane];
+    uint32_t li_abs = s_bi[0][wave][lane], li_rel = s_bi[1][wave][lane];
 #pragma unroll 1
     for (int j = 0; j < V; ++j) {
       const bool valid = (vmask >> j) & 1u;
@@ -1026,6 +1160,10 @@ void main_kernel(const Params P) {
         }
       }
     }
+    s_bv[0][wave][lane] = lb_abs;
+    s_bv[1][wave][lane] = lb_rel;
+    s_bi[0][wave][lane] = li_abs;
+    s_bi[1][wave][lane] = li_rel;
     raise_abs(~0ull);
     raise_rel(~0ull);
     if (lane == 0) {
@@ -1055,7 +1193,8 @@ void main_kernel(const Params P) {
   // step (valid, nothing failing, no new maximum) then commits with one
   // uniform branch, and the counts of failing elements are taken in a second
   // pass over the step only when some element failed.
-  auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, uint32_t &pbm)
+  auto t1_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, uint32_t &pbm,
+                     const WaveThr &th, double &add_a, double &add_q)
                      __attribute__((always_inline)) -> int {
     float sa0 = 0.f, sa1 = 0.f, sq0 = 0.f, sq1 = 0.f;
     float md = 0.f, mq = 0.f, mr = 0.f;
@@ -1103,16 +1242,16 @@ void main_kernel(const Params P) {
     bool ok = __builtin_isfinite(sa + sq) && (mq <= QT || (DT == VC_F16 && md < 1.0f));
     if constexpr (DT != VC_F16) ok = ok && mr <= 0x1p60f;
     const uint64_t bad = ballot(!ok);
-    const uint64_t absm = ballot(md > thr_abs);
-    const uint64_t relm = rel_zero ? ballot(md > 0.0f) : ballot(mq >= b_rel);
+    const uint64_t absm = ballot(md > th.thr_abs);
+    const uint64_t relm = th.rel_zero ? ballot(md > 0.0f) : ballot(mq >= th.b_rel);
     // (binary32 storage, single pair: such a step is deferred whole)
     const bool defer_loc = !kBitsInLds && NT == 1 && fany != 0 && loc_on();
     if ((bad | absm | relm | fany) == 0 && !defer_loc) {
 #pragma unroll
       for (int p = 0; p < NT; ++p) mism[p] += fc1[p];
       ++fast_steps;
-      acc_abs += (double)sa;
-      acc_rel += (double)sq;
+      add_a = (double)sa;
+      add_q = (double)sq;
       return kDone;
     }
     if (bad != 0) return kNotTaken;
@@ -1145,9 +1284,154 @@ void main_kernel(const Params P) {
       }
     }
     ++fast_steps;
-    acc_abs += (double)sa;
-    acc_rel += (double)sq;
+    add_a = (double)sa;
+    add_q = (double)sq;
     if ((absm | relm) != 0) t1_update(cs, rs, absm, relm, off0, md, mq);
+    return res;
+  };
+
+  // Tier 1 for a full step, single tolerance pair. One pass over the step
+  // computes, per lane, in binary32:
+  //  - d = c - r, the sum of |d| and the largest |d| (md);
+  //  - the gate screen g = |d| - rlo |r| (one rounding): every element with
+  //    g <= alo passes the binary64 gate (rlo and alo are the pair shrunk by
+  //    2^-20, more than the rounding of g);
+  //  - the quotient screen e = |d| - b_mul |r| (its sign is exact): an
+  //    element with e < s_rel has a quotient below the running threshold
+  //    and, with binary32 / bfloat16 storage, below the exactness bound QT;
+  //  - for each two consecutive elements the sum of their quotients
+  //    |d| / |r| as (|r1| |d0| + |r0| |d1|) / (|r0| |r1|): one reciprocal
+  //    per two elements, relative error below 6 * 2^-24 (the product of two
+  //    16-bit values is exact); its sum, and for binary16 its maximum p;
+  //  - for binary32 / bfloat16 storage the range of |r|.
+  // One ballot of "finite sums and max(g - alo_up, md - thr_abs_up,
+  // max e - s_rel, exactness and range terms) < 0" commits the usual step.
+  // Any other step is sorted out below, with the outcomes of t1_step.
+  auto t1_single = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, uint32_t &pbm,
+                       const WaveThr &th, double &add_a, double &add_q)
+                       __attribute__((always_inline)) -> int {
+    const float nrlo = -rlo, nb = -th.b_mul;
+    float sa = 0.f, sq = 0.f, md = 0.f, gm = 0.f, em = 0.f, pm = 0.f;
+    float rmx = 0.f, rmn = 0.f;
+#pragma unroll
+    for (int p = 0; p < V / 2; ++p) {
+      float d0, d1, g0, g1, e0, e1, P, N;
+      if constexpr (DT == VC_F16) {
+        const uint32_t rw = rq[p];
+        d0 = diff32<DT>(cq, rq, 2 * p);
+        d1 = diff32<DT>(cq, rq, 2 * p + 1);
+        // (binary32 arithmetic on converted halves, which the compiler maps
+        // onto v_fma_mix_f32 with binary16 operands)
+        const float a0 = __builtin_fabsf(dec32<DT>(rw & 0xffffu));
+        const float a1 = __builtin_fabsf(dec32<DT>(rw >> 16));
+        g0 = __builtin_fmaf(nrlo, a0, __builtin_fabsf(d0));
+        g1 = __builtin_fmaf(nrlo, a1, __builtin_fabsf(d1));
+        e0 = __builtin_fmaf(nb, a0, __builtin_fabsf(d0));
+        e1 = __builtin_fmaf(nb, a1, __builtin_fabsf(d1));
+        P = h_prod(rw);
+        N = h_fma_rx<1>(rw, d0, h_mul_rx<0>(rw, d1));
+      } else {
+        const float r0 = dec32<DT>(elem<DT>(rq, 2 * p)), r1 = dec32<DT>(elem<DT>(rq, 2 * p + 1));
+        d0 = dec32<DT>(elem<DT>(cq, 2 * p)) - r0;
+        d1 = dec32<DT>(elem<DT>(cq, 2 * p + 1)) - r1;
+        const float a0 = __builtin_fabsf(r0), a1 = __builtin_fabsf(r1);
+        g0 = __builtin_fmaf(a0, nrlo, __builtin_fabsf(d0));
+        g1 = __builtin_fmaf(a1, nrlo, __builtin_fabsf(d1));
+        e0 = __builtin_fmaf(a0, nb, __builtin_fabsf(d0));
+        e1 = __builtin_fmaf(a1, nb, __builtin_fabsf(d1));
+        P = a0 * a1;
+        N = __builtin_fmaf(a1, __builtin_fabsf(d0), a0 * __builtin_fabsf(d1));
+        if (p == 0) {
+          rmx = __builtin_fmaxf(a0, a1);
+          rmn = __builtin_fminf(a0, a1);
+        } else {
+          rmx = __builtin_fmaxf(rmx, __builtin_fmaxf(a0, a1));
+          rmn = __builtin_fminf(rmn, __builtin_fminf(a0, a1));
+        }
+      }
+      const float ad0 = __builtin_fabsf(d0), ad1 = __builtin_fabsf(d1);
+      const float q = N * __builtin_amdgcn_rcpf(P);
+      if (p == 0) {
+        gm = __builtin_fmaxf(g0, g1);
+        em = __builtin_fmaxf(e0, e1);
+        md = __builtin_fmaxf(ad0, ad1);
+        sa = ad0 + ad1;
+        sq = q;
+        if constexpr (DT == VC_F16) pm = q;
+      } else {
+        gm = __builtin_fmaxf(gm, __builtin_fmaxf(g0, g1));
+        em = __builtin_fmaxf(em, __builtin_fmaxf(e0, e1));
+        md = __builtin_fmaxf(md, __builtin_fmaxf(ad0, ad1));
+        sa += ad0 + ad1;
+        sq += q;
+        if constexpr (DT == VC_F16) pm = __builtin_fmaxf(pm, q);
+      }
+    }
+    const bool fin = __builtin_isfinite(sa + sq);
+    float x = __builtin_fmaxf(__builtin_fmaxf(gm - alo_up, md - th.thr_abs_up), em - th.s_rel);
+    if constexpr (DT == VC_F16) {
+      // inexact difference: |d| >= 1 and a quotient at or above QT
+      x = __builtin_fmaxf(x, __builtin_fminf(md - 1.0f, pm - QT));
+    } else {
+      // |r| outside [2^-60, 2^30] (a quotient at or above QT is caught by e)
+      x = __builtin_fmaxf(x, __builtin_fmaxf(rmx - kRangeHiUp, kRangeLoDown - rmn));
+    }
+    if (ballot(!(fin && x < 0.0f)) == 0) {
+      ++fast_steps;
+      add_a = (double)sa;
+      add_q = (double)sq;
+      return kDone;
+    }
+    // not exact in binary32, not finite, r = 0 or |r| out of range: tier 2
+    bool ok = fin;
+    if constexpr (DT == VC_F16) {
+      ok = ok && !(md >= 1.0f && pm >= QT);
+    } else {
+      // a quotient at or above QT has e >= 0 with b_mul <= QT, or (best
+      // quotient 0) some d > 0: decided per element
+      bool exq = true;
+      if (em >= th.s_rel) {
+#pragma unroll 1
+        for (int j = 0; j < V; ++j) {
+          const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+          const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+          exq = exq && __builtin_fmaf(a, -QT, d) < 0.0f;
+        }
+      }
+      ok = ok && exq && rmx <= 0x1p30f && rmn >= 0x1p-60f;
+    }
+    if (ballot(!ok) != 0) return kNotTaken;
+    const uint64_t fany = ballot(gm > alo);
+    // (binary32 storage: such a step is deferred whole)
+    if (!kBitsInLds && fany != 0 && loc_on()) return kDefer;
+    int res = kDone;
+    if (fany != 0) {
+      // exact counts, the lane's mismatch bits and the elements between the
+      // bounds
+      uint32_t fcnt = 0, bits = 0;
+      uint64_t amb = 0;
+#pragma unroll 1
+      for (int j = 0; j < V; ++j) {
+        const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+        const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+        const bool f = d > __builtin_fmaf(a, rlo, alo);
+        fcnt += popc(ballot(f));
+        amb |= ballot(f && !(d > __builtin_fmaf(a, rhi, ahi)));
+        bits |= (f ? 1u : 0u) << j;
+      }
+      if (amb != 0) return kNotTaken;
+      mism[0] += fcnt;
+      if (kBitsInLds && loc_on()) {
+        pbm = bits;
+        res = kLocate;
+      }
+    }
+    ++fast_steps;
+    add_a = (double)sa;
+    add_q = (double)sq;
+    const uint64_t absm = ballot(md > th.thr_abs);
+    const uint64_t relm = ballot(em >= th.s_rel);
+    if ((absm | relm) != 0) t1_update1(cq, rq, absm, relm, off0, md);
     return res;
   };
 
@@ -1155,7 +1439,8 @@ void main_kernel(const Params P) {
   // when the step holds a NaN, an infinity or a zero reference, and (single
   // pair) kLocate, with the lane's mismatch bits in pbm, when a mismatch
   // position must be recorded.
-  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, uint32_t &pbm)
+  auto t2_step = [&](const u32x4 &cq, const u32x4 &rq, uint32_t off0, uint32_t &pbm,
+                     const WaveThr &th, double &add_a, double &add_q)
                      __attribute__((always_inline)) -> int {
     double sa = 0.0, sq = 0.0;
     uint32_t fcnt[NT];
@@ -1178,16 +1463,16 @@ void main_kernel(const Params P) {
       }
       sa += d;
       sq += d * __builtin_amdgcn_rcp(a);
-      absm |= ballot(d > T_abs);
-      relm |= ballot(__builtin_fma(-T_rel, a, d) > 0.0);
+      absm |= ballot(d > th.T_abs);
+      relm |= ballot(__builtin_fma(-th.T_rel, a, d) > 0.0);
     }
     if (ballot(!__builtin_isfinite(sa + sq)) != 0) return kNotTaken;
     if (!kBitsInLds && NT == 1 && fcnt[0] != 0 && loc_on()) return kDefer;
 #pragma unroll
     for (int p = 0; p < NT; ++p) mism[p] += fcnt[p];
     ++fast_steps;
-    acc_abs += sa;
-    acc_rel += sq;
+    add_a = sa;
+    add_q = sq;
     if (absm != 0) abs_update(cq, rq, absm, off0);
     if (relm != 0) rel_update(cq, rq, relm, off0);
     if (kBitsInLds && fcnt[0] != 0 && loc_on()) {
@@ -1365,7 +1650,14 @@ void main_kernel(const Params P) {
     const uint32_t m0 = prim_count();
     const bool tried = t1ok && t1_hold == 0;
     uint32_t pbm = 0;
-    int res = tried ? t1_step(cq, rq, off0, pbm) : kNotTaken;
+    const WaveThr th = s_thr[wave];
+    // the step's contributions to the binary64 sums (one update below)
+    double add_a = 0.0, add_q = 0.0;
+    int res = kNotTaken;
+    if (tried) {
+      if constexpr (NT == 1) res = t1_single(cq, rq, off0, pbm, th, add_a, add_q);
+      else res = t1_step(cq, rq, off0, pbm, th, add_a, add_q);
+    }
     if (tried) {
       const bool tame = res != kNotTaken;
       t1_next = tame ? 0u : min(2u * t1_next + 1u, 7u);
@@ -1373,7 +1665,9 @@ void main_kernel(const Params P) {
     } else if (t1_hold > 0) {
       --t1_hold;
     }
-    if (res == kNotTaken) res = t2_step(cq, rq, off0, pbm);
+    if (res == kNotTaken) res = t2_step(cq, rq, off0, pbm, th, add_a, add_q);
+    acc_abs += add_a;
+    acc_rel += add_q;
     if (res == kLocate) {
       // single pair: the lane's mismatch bits wait in LDS; the entry holds
       // the offset, bit 0, the list position and the wave
@@ -1394,17 +1688,26 @@ void main_kernel(const Params P) {
   // wave whose range it continues. (32-bit counters: a chunk holds fewer than
   // 2^18 elements, and uniform 32-bit arithmetic stays on the scalar unit.)
   const uint32_t n_steps = (uint32_t)((cend - cstart) / ITER);  // full steps in the chunk
-  const bool split = P.split != 0;
+  // binary32 storage: round robin; 16-bit storage: rotated rounds
+  constexpr bool split = false;
+  constexpr bool rot = ES == 2;
   const uint32_t q_steps = (n_steps + 3) / 4;
   const uint32_t w_first = split ? min(wave * q_steps, n_steps) : wave;
   const uint32_t w_stride = split ? 1u : 4u;
-  const uint32_t n_full = split ? min(w_first + q_steps, n_steps) - w_first
-                                : (n_steps > wave ? (n_steps - wave + 3) / 4 : 0u);
-  const bool tail_here = split ? wave == 3 : n_steps % 4 == wave;
+  const uint32_t n_rounds = n_steps / 4, n_part = n_steps % 4;
+  const uint32_t n_full = rot ? n_rounds + (((wave + n_rounds) & 3u) < n_part ? 1u : 0u)
+                          : split ? min(w_first + q_steps, n_steps) - w_first
+                                  : (n_steps > wave ? (n_steps - wave + 3) / 4 : 0u);
+  const bool tail_here = rot ? ((n_part - n_rounds) & 3u) == wave
+                         : split ? wave == 3 : n_part == wave;
   const uint32_t lane_off = lane * V;
+  // chunk step index of the wave's step st
+  auto step_idx = [&](uint32_t st) __attribute__((always_inline)) {
+    return rot ? 4u * st + ((wave + st) & 3u) : w_first + w_stride * st;
+  };
   // chunk offset of this lane's first element in the wave's step st
   auto step_off = [&](uint32_t st) __attribute__((always_inline)) {
-    return (w_first + w_stride * st) * ITER + lane_off;
+    return step_idx(st) * ITER + lane_off;
   };
   // Evaluation of one listed step given its list entry: the mismatch
   // positions only (several pairs, bit 0 set), else the exact tier.
@@ -1440,7 +1743,7 @@ void main_kernel(const Params P) {
     const uint32_t lane_b = lane * 16u;
     const uint32_t last = n_full > 0 ? n_full - 1 : 0;
     auto off = [&](uint32_t st) __attribute__((always_inline)) {
-      return (w_first + w_stride * min(st, last)) * ITER * ES + lane_b;
+      return step_idx(min(st, last)) * ITER * ES + lane_b;
     };
     auto ld = [&](const uint8_t *base, uint32_t st) __attribute__((always_inline)) {
       return load16(base + off(st));
@@ -1526,6 +1829,8 @@ void main_kernel(const Params P) {
   }
 
   // wave reductions (fixed butterfly order)
+  double lb_abs = s_bv[0][wave][lane], lb_rel = s_bv[1][wave][lane];
+  uint32_t li_abs = s_bi[0][wave][lane], li_rel = s_bi[1][wave][lane];
   wave_max(lb_abs, li_abs);
   wave_max(lb_rel, li_rel);
 #pragma unroll
