@@ -51,6 +51,19 @@
  *
  * Concurrency: calls on different streams may run concurrently as long as
  * they use different workspaces and outputs.
+ *
+ * Host-side state and blocking. The library keeps, per device and until the
+ * process ends: a ring of 8 pinned host buffers of 256 KiB, allocated once
+ * (by vcheck_init or by the first call that needs it), from which the first
+ * kernel of a one-shot call copies the call's descriptor table (a buffer is
+ * reused only after the event recorded behind the call that read it has
+ * completed: a thread that issues more than 8 such calls ahead of the GPU
+ * waits for the oldest), guarded by a mutex. A descriptor table larger
+ * than 256 KiB (about 1,300 sweep cases) is uploaded with a pageable copy,
+ * which returns only once the runtime has taken the bytes (for pageable
+ * memory it first waits for the stream's earlier work). Per thread: the last
+ * error string and the vcheck_profile_events hook. Nothing else persists
+ * between calls; descriptor planning uses the C++ heap.
  */
 #ifndef VCHECK_H
 #define VCHECK_H
@@ -80,6 +93,7 @@ typedef int32_t vc_status;
 #define VC_ERR_LIMIT (-8)     /* n_tols, n_inputs or n_cases outside its range */
 #define VC_ERR_HIP (-9)       /* HIP runtime / launch failure */
 #define VC_ERR_ALIGN (-10)    /* data pointer not aligned to its element size */
+#define VC_ERR_STATE (-11)    /* a prepared sweep is launched on another device */
 
 typedef enum vc_dtype { VC_F32 = 0, VC_F16 = 1, VC_BF16 = 2 } vc_dtype;
 
@@ -237,6 +251,55 @@ vc_status vcheck_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols
                        const vc_sweep_opts *opts, const vc_sweep_out *out, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* ---- prepared sweeps -------------------------------------------------------
+ *
+ * The repair loop validates every candidate of an operator against the same
+ * case matrix (Sec. 3.2: Validate(K, R, T_ext, tau) for each repaired
+ * kernel; Sec. 4.3: full-coverage evaluation of every accepted candidate):
+ * the case descriptors do not change between candidates when each candidate
+ * writes its outputs into the same buffers. A prepared sweep uploads the
+ * case table once; each launch then runs only the streaming and merge
+ * kernels, with the results of vcheck_sweep.
+ */
+typedef struct vc_plan vc_plan; /* opaque, host memory */
+
+/*
+ * vcheck_plan_sweep -- check and plan a sweep exactly as vcheck_sweep does
+ * (same arguments, same errors), upload its case table into `ws` and clear
+ * the workspace parts that must be zero on entry. Blocks until the upload is
+ * done (it synchronizes `stream`). On success *plan receives a plan that
+ * refers to the descriptors' device pointers, the outputs of `out` and the
+ * workspace: the caller keeps all of them alive, and the workspace for this
+ * plan's use only, until vcheck_plan_free. Host structs (cases, tols, opts,
+ * out) are not referenced after the call. The plan belongs to the current
+ * device.
+ */
+vc_status vcheck_plan_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols,
+                            int32_t n_tols, const vc_sweep_opts *opts, const vc_sweep_out *out,
+                            void *ws, size_t ws_bytes, void *stream, vc_plan **plan);
+
+/*
+ * vcheck_plan_launch -- enqueue one evaluation of a prepared sweep on
+ * `stream`: the outputs are those of vcheck_sweep over the current contents
+ * of the case tensors, valid after the stream syncs. Each launch leaves the
+ * workspace ready for the next one, so launches of one plan must not
+ * overlap (use one stream, or order the streams). Errors: VC_ERR_NULL,
+ * VC_ERR_STATE (current device is not the plan's), VC_ERR_HIP. After a
+ * VC_ERR_HIP, free the plan and prepare a new one.
+ */
+vc_status vcheck_plan_launch(vc_plan *plan, void *stream);
+
+/* Frees a plan (NULL is accepted). Does not wait for launches in flight:
+ * the workspace and outputs must stay alive until they are done. */
+vc_status vcheck_plan_free(vc_plan *plan);
+
+/* ---- library set-up -------------------------------------------------------- */
+
+/* Set-up for the current device: allocates the pinned staging ring (once),
+ * so that later calls on the device allocate nothing. Idempotent; optional
+ * (the first call that needs the ring allocates it). Errors: VC_ERR_HIP. */
+vc_status vcheck_init(void);
+
 /* ---- tensor-statistics probe ---------------------------------------------
  *
  * The multi-level tensor statistics that the engine's diagnostic
@@ -372,8 +435,11 @@ vc_status vcheck_content_hash_workspace(const vc_tensor *tensors, int32_t n_tens
 vc_status vcheck_profile_events(void *begin_event, void *end_event);
 
 /* Workspace bytes for a sweep over `cases` (also for the single-case entry
- * points: one case, n_tols = 1, opts carrying k). Returns VC_OK and writes
- * *bytes, or an error status for arguments the sweep would reject. */
+ * points: one case, n_tols = 1, opts carrying k and, for vcheck_localize,
+ * the tile geometry). opts->tile_h and opts->tile_w of 1 or more size the
+ * workspace for tile maps of that geometry (4 bytes per tile); 0 (or opts
+ * NULL) for a call without tile maps. Returns VC_OK and writes *bytes, or
+ * an error status for arguments the sweep would reject. */
 vc_status vcheck_workspace_bytes(const vc_case *cases, int32_t n_cases, int32_t n_tols,
                                  const vc_sweep_opts *opts, size_t *bytes);
 

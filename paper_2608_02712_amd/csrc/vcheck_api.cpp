@@ -109,20 +109,21 @@ struct Group {
 struct Plan {
   std::vector<vck::DevCase> table;
   std::vector<uint64_t> case_chunk;  // chunk_begin per table entry
-  std::vector<uint64_t> case_group;  // group_begin per table entry
-  std::vector<uint32_t> multi;       // table indices of cases with more than one group
+  std::vector<uint32_t> group_case;  // table index per chunk group (empty: group = table index)
   std::vector<Group> groups;
   uint64_t total_chunks = 0;
   uint64_t total_groups = 0;
   uint64_t tiles_total = 0;
   int32_t n_cases = 0, n_tols = 1, nt_class = 1, k = 0, primary = 0, tile_h = 1, tile_w = 1;
   bool do_tiles = false, do_firstk = false, do_integ = false;
-  // workspace layout: [table | case_chunk | case_group | multi] (the blob
-  // the prologue copies), chunk records, chunk first-k lists, group records,
-  // group first-k lists, then the Counters the prologue clears
-  size_t off_table = 0, off_cc = 0, off_cg = 0, off_multi = 0, blob_bytes = 0;
+  // Workspace layout (each part 256-byte aligned): the descriptor blob
+  // [table | case_chunk | group_case], chunk records, chunk first-k lists,
+  // group records, group first-k lists, then the parts that are zero on
+  // entry: the Counters, the per-case merged-group counts and the tile-count
+  // accumulators.
+  size_t off_table = 0, off_cc = 0, off_gc = 0, blob_bytes = 0;
   size_t off_recs = 0, off_stage = 0, off_grecs = 0, off_gstage = 0;
-  size_t off_ctr = 0, ctr_bytes = 0;
+  size_t off_zero = 0, zero_bytes = 0, off_ctr = 0, off_gdone = 0, off_tacc = 0;
   size_t bytes = 0;
 };
 
@@ -134,21 +135,6 @@ struct Plan {
 #ifndef VCK_WAVE_TARGET
 #define VCK_WAVE_TARGET 16384
 #endif
-// How the four waves of a block share its chunk: with 16-bit storage each
-// wave streams one contiguous quarter, so that the steps of a faulty tile
-// (the same columns of consecutive rows) spread over the four waves; with
-// binary32 storage (rows of 4 KiB and more, where a tile's rows already fall
-// on several waves) they take steps round robin, which streams a little
-// faster there.
-#ifndef VCK_SPLIT
-#define VCK_SPLIT 2
-#endif
-uint32_t split_for(int32_t dtype) {
-  if (VCK_SPLIT == 2) return dtype == VC_F32 ? 0u : 1u;
-  if (VCK_SPLIT == 3) return 2u;
-  if (VCK_SPLIT == 4) return dtype == VC_F32 ? 0u : 2u;
-  return (uint32_t)VCK_SPLIT;
-}
 
 uint32_t unit_for(uint64_t group_elems, int32_t dtype) {
   const uint64_t lo = 1024, hi = 65536 / elem_size(dtype);
@@ -242,6 +228,7 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
       tile_count[i] = ((rows + opts.tile_h - 1) / opts.tile_h) *
                       ((cols + opts.tile_w - 1) / opts.tile_w);
     }
+    d.n_tiles = tile_count[i];
     if (st != VC_OK) {
       d.status = st;
       continue;
@@ -276,6 +263,7 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
   }
   // group by dtype (stable): F32, F16, BF16; chunks numbered in table order
   uint64_t chunk = 0, group = 0;
+  bool multi = false;
   for (int32_t dt : {VC_F32, VC_F16, VC_BF16}) {
     Group g{};
     g.dtype = dt;
@@ -299,12 +287,11 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
       if (nc > 0xffffffffull) return fail(VC_ERR_LIMIT, "case %d is too large", (int)d.orig);
       d.n_chunks = (uint32_t)nc;
       d.n_groups = (uint32_t)((nc + vck::kGroupChunks - 1) / vck::kGroupChunks);
+      if (d.n_groups > 1) multi = true;
       chunk += nc;
       group += d.n_groups;
       plan.table.push_back(d);
       plan.case_chunk.push_back(d.chunk_begin);
-      plan.case_group.push_back(d.group_begin);
-      if (d.n_groups > 1) plan.multi.push_back((uint32_t)(plan.table.size() - 1));
     }
     g.case_hi = plan.table.size();
     g.n_chunks = chunk - g.chunk_lo;
@@ -314,17 +301,21 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
   }
   plan.total_chunks = chunk;
   plan.total_groups = group;
+  if (group > 0x7fffffffull) return fail(VC_ERR_LIMIT, "the sweep needs more than 2^31 - 1 groups");
+  // group -> table index, needed only when some case has several groups
+  if (multi) {
+    plan.group_case.reserve(group);
+    for (size_t t = 0; t < plan.table.size(); ++t)
+      for (uint32_t q = 0; q < plan.table[t].n_groups; ++q) plan.group_case.push_back((uint32_t)t);
+  }
 
   // workspace layout
   const size_t nc = (size_t)n_cases;
-  size_t off = 0;
-  plan.off_table = off;
-  plan.off_cc = off + sizeof(vck::DevCase) * nc;  // 176 * n: 16-byte aligned
-  plan.off_cg = plan.off_cc + sizeof(uint64_t) * nc;
-  plan.off_multi = plan.off_cg + sizeof(uint64_t) * nc;
-  plan.blob_bytes =
-      (plan.off_multi - off + sizeof(uint32_t) * plan.multi.size() + 15) / 16 * 16;
-  off += align_up(plan.blob_bytes);
+  plan.off_table = 0;
+  plan.off_cc = sizeof(vck::DevCase) * nc;  // 176 * n: 16-byte aligned
+  plan.off_gc = plan.off_cc + sizeof(uint64_t) * nc;
+  plan.blob_bytes = (plan.off_gc + sizeof(uint32_t) * plan.group_case.size() + 15) / 16 * 16;
+  size_t off = align_up(plan.blob_bytes);
   plan.off_recs = off;
   off += align_up(sizeof(vck::ChunkRec) * (size_t)plan.total_chunks);
   plan.off_stage = off;
@@ -333,76 +324,110 @@ vc_status make_plan(const vc_case *cases, int32_t n_cases, const vc_tol *tols, i
   off += align_up(sizeof(vck::ChunkRec) * (size_t)plan.total_groups);
   plan.off_gstage = off;
   off += align_up(sizeof(uint32_t) * (size_t)plan.total_groups * (size_t)plan.k);
+  plan.off_zero = off;
   plan.off_ctr = off;
-  plan.ctr_bytes = sizeof(vck::Counters);
-  off += align_up(plan.ctr_bytes);
+  off += align_up(sizeof(vck::Counters));
+  plan.off_gdone = off;
+  off += align_up(sizeof(uint32_t) * std::max<size_t>(nc, 1));
+  plan.off_tacc = off;
+  off += align_up(sizeof(uint32_t) * (size_t)(want_tiles ? plan.tiles_total : 0));
+  plan.zero_bytes = off - plan.off_zero;
   plan.bytes = off + kAlign;  // slack for aligning the caller's base pointer
   return VC_OK;
 }
 
-// ---- pinned staging for descriptor uploads ---------------------------------
-// A small ring of pinned host buffers per device. The prologue kernel reads
-// the descriptor blob straight from the pinned buffer; a slot is reused only
-// after the event recorded behind that kernel has completed.
-struct Slot {
-  void *host = nullptr;
-  void *dev = nullptr;  // device-visible address of `host`
-  size_t cap = 0;
-  hipEvent_t ev = nullptr;
-  bool pending = false;
-};
-struct DeviceStaging {
-  std::mutex mu;
-  Slot slots[8];
-  int next = 0;
-};
-constexpr int kMaxDevices = 64;
-DeviceStaging g_staging[kMaxDevices];
+// The descriptor blob of a plan, as it is laid out at the workspace base.
+std::vector<uint8_t> plan_blob(const Plan &plan) {
+  std::vector<uint8_t> blob(plan.blob_bytes, 0);
+  if (!plan.table.empty())
+    memcpy(blob.data() + plan.off_table, plan.table.data(),
+           sizeof(vck::DevCase) * plan.table.size());
+  if (!plan.case_chunk.empty())
+    memcpy(blob.data() + plan.off_cc, plan.case_chunk.data(),
+           sizeof(uint64_t) * plan.case_chunk.size());
+  if (!plan.group_case.empty())
+    memcpy(blob.data() + plan.off_gc, plan.group_case.data(),
+           sizeof(uint32_t) * plan.group_case.size());
+  return blob;
+}
 
 vc_status hip_check(hipError_t e, const char *what) {
   if (e == hipSuccess) return VC_OK;
   return fail(VC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Takes the next slot of the current device (waiting for its previous use)
-// and fills it with `bytes` bytes of `src`. The caller holds `lock` until it
-// has recorded the slot's event behind the kernel that reads it.
-vc_status stage_blob(const void *src, size_t bytes, std::unique_lock<std::mutex> &lock,
-                     Slot *&slot) {
-  int dev = 0;
+// ---- per-device state --------------------------------------------------------
+// Per device the library keeps, allocated once and held until the process
+// ends: a ring of kSlots pinned host buffers of kSlotBytes each, from which
+// the prologue kernel of a one-shot call copies the call's descriptor blob
+// (a slot is reused only after the event recorded behind the kernels that
+// read it has completed). A blob larger than a slot is uploaded with a
+// pageable hipMemcpyAsync instead, which returns only once the runtime has
+// taken the bytes (waiting for the stream's earlier work).
+constexpr int kSlots = 8;
+constexpr size_t kSlotBytes = 256 * 1024;
+constexpr int kMaxDevices = 64;
+
+struct DeviceState {
+  std::mutex mu;
+  bool ring = false;  // the slots are allocated
+  void *host[kSlots] = {};
+  void *dev[kSlots] = {};  // device-visible addresses of host[]
+  hipEvent_t ev[kSlots] = {};
+  bool pending[kSlots] = {};
+  int next = 0;
+};
+DeviceState g_dev[kMaxDevices];
+
+vc_status current_device(int &dev) {
   vc_status st = hip_check(hipGetDevice(&dev), "hipGetDevice");
   if (st != VC_OK) return st;
   if (dev < 0 || dev >= kMaxDevices) return fail(VC_ERR_HIP, "device id %d out of range", dev);
-  DeviceStaging &ds = g_staging[dev];
+  return VC_OK;
+}
+
+// Allocates the staging ring of a device once (caller holds ds.mu).
+vc_status ensure_ring(DeviceState &ds) {
+  if (ds.ring) return VC_OK;
+  for (int i = 0; i < kSlots; ++i) {
+    vc_status st = hip_check(hipHostMalloc(&ds.host[i], kSlotBytes, hipHostMallocDefault),
+                             "hipHostMalloc");
+    if (st == VC_OK)
+      st = hip_check(hipHostGetDevicePointer(&ds.dev[i], ds.host[i], 0), "hipHostGetDevicePointer");
+    if (st == VC_OK)
+      st = hip_check(hipEventCreateWithFlags(&ds.ev[i], hipEventDisableTiming), "hipEventCreate");
+    if (st != VC_OK) return st;  // (partial allocations are kept for the next attempt)
+  }
+  ds.ring = true;
+  return VC_OK;
+}
+
+// Takes the next slot of the current device (waiting for its previous use
+// to complete) and fills it with `bytes` (<= kSlotBytes) bytes of `src`. The
+// caller holds `lock` until it has recorded ev[slot] behind the kernels that
+// read the slot. `allocate` = false: the ring must already exist.
+vc_status stage_blob(const void *src, size_t bytes, bool allocate,
+                     std::unique_lock<std::mutex> &lock, DeviceState *&dsp, int &slot) {
+  int dev = 0;
+  vc_status st = current_device(dev);
+  if (st != VC_OK) return st;
+  DeviceState &ds = g_dev[dev];
   lock = std::unique_lock<std::mutex>(ds.mu);
-  Slot &sl = ds.slots[ds.next];
-  ds.next = (ds.next + 1) % 8;
-  if (sl.pending) {
-    st = hip_check(hipEventSynchronize(sl.ev), "hipEventSynchronize");
-    if (st != VC_OK) return st;
-    sl.pending = false;
-  }
-  if (sl.ev == nullptr) {
-    st = hip_check(hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming), "hipEventCreate");
+  if (!ds.ring) {
+    if (!allocate) return fail(VC_ERR_STATE, "vcheck_init has not run on device %d", dev);
+    st = ensure_ring(ds);
     if (st != VC_OK) return st;
   }
-  if (sl.cap < bytes) {
-    if (sl.host != nullptr) (void)hipHostFree(sl.host);
-    sl.host = sl.dev = nullptr;
-    sl.cap = 0;
-    const size_t cap = std::max<size_t>(bytes, 64 * 1024);
-    st = hip_check(hipHostMalloc(&sl.host, cap, hipHostMallocDefault), "hipHostMalloc");
+  const int i = ds.next;
+  ds.next = (ds.next + 1) % kSlots;
+  if (ds.pending[i]) {
+    st = hip_check(hipEventSynchronize(ds.ev[i]), "hipEventSynchronize");
     if (st != VC_OK) return st;
-    st = hip_check(hipHostGetDevicePointer(&sl.dev, sl.host, 0), "hipHostGetDevicePointer");
-    if (st != VC_OK) {
-      (void)hipHostFree(sl.host);
-      sl.host = nullptr;
-      return st;
-    }
-    sl.cap = cap;
+    ds.pending[i] = false;
   }
-  memcpy(sl.host, src, bytes);
-  slot = &sl;
+  memcpy(ds.host[i], src, bytes);
+  dsp = &ds;
+  slot = i;
   return VC_OK;
 }
 
@@ -432,15 +457,9 @@ float f32_above(double x) {
   return f;
 }
 
-// Enqueues the planned work. `single` passes the one descriptor by value
-// (no table).
-vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws, size_t ws_bytes,
-              hipStream_t stream, bool single) {
-  if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
-  if (ws_bytes < plan.bytes)
-    return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
-  uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
-
+// Kernel parameters of a planned call whose workspace starts at `base`.
+vck::Params make_params(const Plan &plan, const vc_tol *tols, const Outputs &out, uint8_t *base,
+                        bool single) {
   vck::Params P;
   memset(&P, 0, sizeof P);
   P.n_cases = plan.n_cases;
@@ -478,7 +497,12 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
   P.grecs = (vck::ChunkRec *)(base + plan.off_grecs);
   P.gstage = (uint32_t *)(base + plan.off_gstage);
   P.ctr = (vck::Counters *)(base + plan.off_ctr);
-  P.tile_maps = plan.do_tiles ? out.tile_maps : nullptr;
+  P.gdone = (uint32_t *)(base + plan.off_gdone);
+  P.tile_maps = plan.do_tiles && out.tile_maps != nullptr ? (uint32_t *)(base + plan.off_tacc)
+                                                          : nullptr;
+  P.tile_out = P.tile_maps != nullptr ? out.tile_maps : nullptr;
+  P.tiles_total = P.tile_maps != nullptr ? plan.tiles_total : 0;
+  P.n_groups = plan.total_groups;
   P.stats = out.stats;
   P.mismatches = out.mismatches;
   P.pass_out = out.pass;
@@ -486,86 +510,140 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
   P.integ = out.integ;
   P.match_rate = out.match_rate;
   P.numeric_rate = out.numeric_rate;
-
-  vck::Prologue Q;
-  memset(&Q, 0, sizeof Q);
-  Q.zero = (uint32_t *)(base + plan.off_ctr);
-  Q.zero_words = plan.ctr_bytes / sizeof(uint32_t);
-  Q.tiles = P.tile_maps;
-  Q.n_tiles = P.tile_maps != nullptr ? plan.tiles_total : 0;
-  Q.match_rate = out.match_rate;
-  Q.numeric_rate = out.numeric_rate;
-  Q.n_cases = plan.n_cases;
-  Q.n_tols = plan.n_tols;
-
-  std::unique_lock<std::mutex> lock;
-  Slot *slot = nullptr;
-  std::vector<uint8_t> blob;
   if (single) {
     P.cases = nullptr;
     P.single = plan.table[0];
   } else if (plan.n_cases > 0) {
     P.cases = (const vck::DevCase *)(base + plan.off_table);
     P.case_chunk = (const uint64_t *)(base + plan.off_cc);
-    P.case_group = (const uint64_t *)(base + plan.off_cg);
-    P.multi = (const uint32_t *)(base + plan.off_multi);
-    blob.assign(plan.blob_bytes, 0);
-    memcpy(blob.data(), plan.table.data(), sizeof(vck::DevCase) * plan.table.size());
-    memcpy(blob.data() + (plan.off_cc - plan.off_table), plan.case_chunk.data(),
-           sizeof(uint64_t) * plan.case_chunk.size());
-    memcpy(blob.data() + (plan.off_cg - plan.off_table), plan.case_group.data(),
-           sizeof(uint64_t) * plan.case_group.size());
-    if (!plan.multi.empty())
-      memcpy(blob.data() + (plan.off_multi - plan.off_table), plan.multi.data(),
-             sizeof(uint32_t) * plan.multi.size());
-    const vc_status st = stage_blob(blob.data(), blob.size(), lock, slot);
-    if (st != VC_OK) return st;
-    Q.blob_src = (const uint8_t *)slot->dev;
+    P.group_case = plan.group_case.empty() ? nullptr : (const uint32_t *)(base + plan.off_gc);
+  }
+  return P;
+}
+
+// The prologue of a call: copies the blob from `blob_src` (a pinned slot,
+// or nullptr when it is already in place) and clears the parts of the
+// workspace that must be zero on entry; with no cases, writes zero rates.
+vck::Prologue make_prologue(const Plan &plan, const vck::Params &P, uint8_t *base,
+                            const void *blob_src) {
+  vck::Prologue Q;
+  memset(&Q, 0, sizeof Q);
+  if (blob_src != nullptr) {
+    Q.blob_src = (const uint8_t *)blob_src;
     Q.blob_dst = base + plan.off_table;
     Q.blob_bytes = plan.blob_bytes;
   }
-  // The launches of the call, back to back: no host work or event sits
-  // between them, so the GPU never waits for the host inside a call.
-  auto launch_all = [&]() -> vc_status {
-    vc_status st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  Q.zero = (uint32_t *)(base + plan.off_zero);
+  Q.zero_words = plan.zero_bytes / sizeof(uint32_t);
+  Q.match_rate = P.match_rate;
+  Q.numeric_rate = P.numeric_rate;
+  Q.n_cases = plan.n_cases;
+  Q.n_tols = plan.n_tols;
+  return Q;
+}
+
+// The streaming and finalize launches of a planned call, back to back: no
+// host work or event sits between them (except the optional profiling
+// events), so the GPU never waits for the host inside a call.
+vc_status launch_streaming(const Plan &plan, const vck::Params &P, hipStream_t stream) {
+  hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
+  g_prof_begin = g_prof_end = nullptr;
+  vc_status st = VC_OK;
+  if (prof_begin != nullptr) {
+    st = hip_check(hipEventRecord(prof_begin, stream), "profile begin event");
     if (st != VC_OK) return st;
-    hipEvent_t prof_begin = g_prof_begin, prof_end = g_prof_end;
-    g_prof_begin = g_prof_end = nullptr;
-    if (prof_begin != nullptr) {
-      st = hip_check(hipEventRecord(prof_begin, stream), "profile begin event");
+  }
+  for (const Group &g : plan.groups) {
+    vck::Params G = P;
+    G.chunk_lo = g.chunk_lo;
+    G.case_lo = g.case_lo;
+    G.case_hi = g.case_hi;
+    G.unit_elems = g.unit;
+    st = hip_check(vck::launch_main(g.dtype, plan.nt_class, plan.do_integ ? 1 : 0, G,
+                                    g.n_chunks, stream),
+                   "main kernel launch");
+    if (st != VC_OK) return st;
+  }
+  if (prof_end != nullptr) {
+    st = hip_check(hipEventRecord(prof_end, stream), "profile end event");
+    if (st != VC_OK) return st;
+  }
+  return hip_check(vck::launch_finalize(P, stream), "finalize launch");
+}
+
+// A one-shot call: uploads the blob (a pinned slot read by the prologue, or
+// a pageable copy for a blob larger than a slot), clears the zero-on-entry
+// parts, then launches. `single` passes the one descriptor by value (no
+// table). `allocate` = false (the allocation-free entry point): the blob
+// must fit a slot of an existing ring.
+vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws, size_t ws_bytes,
+              hipStream_t stream, bool single, bool allocate = true) {
+  if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < plan.bytes)
+    return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
+  uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
+  const vck::Params P = make_params(plan, tols, out, base, single);
+
+  std::unique_lock<std::mutex> lock;
+  DeviceState *ds = nullptr;
+  int slot = -1;
+  const void *src = nullptr;
+  vc_status st = VC_OK;
+  if (!single && plan.n_cases > 0) {
+    const std::vector<uint8_t> blob = plan_blob(plan);
+    if (blob.size() <= kSlotBytes) {
+      st = stage_blob(blob.data(), blob.size(), allocate, lock, ds, slot);
+      if (st != VC_OK) return st;
+      src = ds->dev[slot];
+    } else {
+      if (!allocate)
+        return fail(VC_ERR_LIMIT, "the case table (%zu bytes) exceeds the %zu-byte staging slot",
+                    blob.size(), kSlotBytes);
+      st = hip_check(hipMemcpyAsync(base + plan.off_table, blob.data(), blob.size(),
+                                    hipMemcpyHostToDevice, stream),
+                     "descriptor upload");
       if (st != VC_OK) return st;
     }
-    for (const Group &g : plan.groups) {
-      vck::Params G = P;
-      G.chunk_lo = g.chunk_lo;
-      G.case_lo = g.case_lo;
-      G.case_hi = g.case_hi;
-      G.unit_elems = g.unit;
-      G.split = split_for(g.dtype);
-      st = hip_check(vck::launch_main(g.dtype, plan.nt_class, plan.do_integ ? 1 : 0, G,
-                                      g.n_chunks, stream),
-                     "main kernel launch");
-      if (st != VC_OK) return st;
-    }
-    if (prof_end != nullptr) {
-      st = hip_check(hipEventRecord(prof_end, stream), "profile end event");
-      if (st != VC_OK) return st;
-    }
-    const uint64_t n_multi = single ? (plan.table[0].n_groups > 1 ? 1 : 0) : plan.multi.size();
-    return hip_check(vck::launch_finalize(P, plan.total_groups, n_multi, stream),
-                     "finalize launch");
-  };
-  vc_status st = launch_all();
-  if (slot != nullptr) {
-    // The staging slot may be refilled once the prologue has read it; an
-    // event behind the call's last kernel (recorded also after a failed
-    // launch, in case the prologue was enqueued) guards that. The slot's
-    // lock is held until then.
-    const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
-    if (se == VC_OK) slot->pending = true;
+  }
+  const vck::Prologue Q = make_prologue(plan, P, base, src);
+  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  if (st == VC_OK) st = launch_streaming(plan, P, stream);
+  if (ds != nullptr) {
+    // The slot may be refilled once the prologue has read it; an event
+    // behind the call's last kernel (recorded also after a failed launch, in
+    // case the prologue was enqueued) guards that. The lock is held until then.
+    const vc_status se = hip_check(hipEventRecord(ds->ev[slot], stream), "hipEventRecord");
+    if (se == VC_OK) ds->pending[slot] = true;
     if (st == VC_OK) st = se;
   }
   return st;
+}
+
+// Argument checks and plan of a sweep (vcheck_sweep, vcheck_plan_sweep).
+vc_status plan_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols, int32_t n_tols,
+                     const vc_sweep_opts *opts, const vc_sweep_out *out, Plan &plan,
+                     Outputs &oo) {
+  if (out == nullptr) return fail(VC_ERR_NULL, "output descriptor is NULL");
+  if (out->stats == nullptr && n_cases > 0) return fail(VC_ERR_NULL, "out->stats is NULL");
+  vc_sweep_opts o{};
+  if (opts != nullptr) o = *opts;
+  if (o.do_integrity == 1 && out->integ == nullptr && n_cases > 0)
+    return fail(VC_ERR_NULL, "do_integrity is set but out->integ is NULL");
+  const bool want_tiles = out->tile_maps != nullptr;
+  const bool want_firstk = out->first_k != nullptr;
+  if (o.k > 0 && !want_firstk) o.k = 0;
+  const vc_status st =
+      make_plan(cases, n_cases, tols, n_tols, o, want_tiles, want_firstk, false, plan);
+  if (st != VC_OK) return st;
+  oo.stats = out->stats;
+  oo.mismatches = out->mismatches;
+  oo.pass = out->pass;
+  oo.match_rate = out->match_rate;
+  oo.numeric_rate = out->numeric_rate;
+  oo.tile_maps = out->tile_maps;
+  oo.first_k = out->first_k;
+  oo.integ = out->integ;
+  return VC_OK;
 }
 
 vc_case one_case(const vc_tensor *cand, const vc_tensor *ref, const vc_tensor *inputs,
@@ -654,10 +732,12 @@ vc_status make_probe_plan(const vc_tensor *tensors, int32_t n, ProbePlan &plan) 
   return VC_OK;
 }
 
-// Runs one diagnostic call: stages the descriptor blob (`parts`, copied
-// back to back) in a pinned slot, enqueues the prologue (copying it to
-// `base`, clearing `zero_words` words at `zero`) and then `launch` (which
-// receives the profiling events), and records the slot's event behind them.
+// Runs one diagnostic call: uploads the descriptor blob (`parts`, copied
+// back to back, a multiple of 16 bytes) to `base` (staged in a pinned slot
+// that the prologue reads, or a pageable copy when larger than a slot),
+// enqueues the prologue (clearing `zero_words` words at `zero`) and then
+// `launch` (which receives the profiling events), and records the slot's
+// event behind them.
 template <typename F>
 vc_status run_diagnostic(const std::vector<std::pair<const void *, size_t>> &parts, uint8_t *base,
                          uint32_t *zero, uint64_t zero_words, hipStream_t stream,
@@ -671,14 +751,22 @@ vc_status run_diagnostic(const std::vector<std::pair<const void *, size_t>> &par
     at += p.second;
   }
   std::unique_lock<std::mutex> lock;
-  Slot *slot = nullptr;
-  vc_status st = stage_blob(blob.data(), blob.size(), lock, slot);
-  if (st != VC_OK) return st;
+  DeviceState *ds = nullptr;
+  int slot = -1;
   vck::Prologue Q;
   memset(&Q, 0, sizeof Q);
-  Q.blob_src = (const uint8_t *)slot->dev;
-  Q.blob_dst = base;
-  Q.blob_bytes = total;
+  vc_status st = VC_OK;
+  if (total <= kSlotBytes) {
+    st = stage_blob(blob.data(), blob.size(), true, lock, ds, slot);
+    if (st != VC_OK) return st;
+    Q.blob_src = (const uint8_t *)ds->dev[slot];
+    Q.blob_dst = base;
+    Q.blob_bytes = total;
+  } else {
+    st = hip_check(hipMemcpyAsync(base, blob.data(), total, hipMemcpyHostToDevice, stream),
+                   "descriptor upload");
+    if (st != VC_OK) return st;
+  }
   Q.zero = zero;
   Q.zero_words = zero_words;
   Q.n_cases = 1;  // (no suite rates to clear)
@@ -686,10 +774,13 @@ vc_status run_diagnostic(const std::vector<std::pair<const void *, size_t>> &par
   g_prof_begin = g_prof_end = nullptr;
   st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
   if (st == VC_OK) st = hip_check(launch(prof_begin, prof_end), what);
-  // the staging slot is reused once the prologue has read it
-  const vc_status se = hip_check(hipEventRecord(slot->ev, stream), "hipEventRecord");
-  if (se == VC_OK) slot->pending = true;
-  return st != VC_OK ? st : se;
+  if (ds != nullptr) {
+    // the staging slot is reused once the prologue has read it
+    const vc_status se = hip_check(hipEventRecord(ds->ev[slot], stream), "hipEventRecord");
+    if (se == VC_OK) ds->pending[slot] = true;
+    if (st == VC_OK) st = se;
+  }
+  return st;
 }
 
 // ---- near-pass statistics -------------------------------------------------
@@ -759,6 +850,14 @@ vc_status make_np_plan(const vc_case *cases, int32_t n, NpPlan &plan) {
 }
 
 }  // namespace
+
+// A prepared sweep: its plan and kernel parameters (pointing into the
+// caller's workspace, which holds the uploaded case table).
+struct vc_plan {
+  Plan plan;
+  vck::Params P;
+  int device;
+};
 
 extern "C" {
 
@@ -835,28 +934,88 @@ vc_status vcheck_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols
                        const vc_sweep_opts *opts, const vc_sweep_out *out, void *ws,
                        size_t ws_bytes, void *stream) {
   g_last_error.clear();
-  if (out == nullptr) return fail(VC_ERR_NULL, "output descriptor is NULL");
-  if (out->stats == nullptr && n_cases > 0) return fail(VC_ERR_NULL, "out->stats is NULL");
-  vc_sweep_opts o{};
-  if (opts != nullptr) o = *opts;
-  if (o.do_integrity == 1 && out->integ == nullptr && n_cases > 0)
-    return fail(VC_ERR_NULL, "do_integrity is set but out->integ is NULL");
-  const bool want_tiles = out->tile_maps != nullptr;
-  const bool want_firstk = out->first_k != nullptr;
-  if (o.k > 0 && !want_firstk) o.k = 0;
   Plan plan;
-  vc_status st = make_plan(cases, n_cases, tols, n_tols, o, want_tiles, want_firstk, false, plan);
-  if (st != VC_OK) return st;
   Outputs oo;
-  oo.stats = out->stats;
-  oo.mismatches = out->mismatches;
-  oo.pass = out->pass;
-  oo.match_rate = out->match_rate;
-  oo.numeric_rate = out->numeric_rate;
-  oo.tile_maps = out->tile_maps;
-  oo.first_k = out->first_k;
-  oo.integ = out->integ;
+  const vc_status st = plan_sweep(cases, n_cases, tols, n_tols, opts, out, plan, oo);
+  if (st != VC_OK) return st;
   return run(plan, tols, oo, ws, ws_bytes, (hipStream_t)stream, false);
+}
+
+vc_status vcheck_init(void) {
+  g_last_error.clear();
+  int dev = 0;
+  vc_status st = current_device(dev);
+  if (st != VC_OK) return st;
+  DeviceState &ds = g_dev[dev];
+  std::lock_guard<std::mutex> lock(ds.mu);
+  return ensure_ring(ds);
+}
+
+vc_status vcheck_plan_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols,
+                            int32_t n_tols, const vc_sweep_opts *opts, const vc_sweep_out *out,
+                            void *ws, size_t ws_bytes, void *stream_, vc_plan **plan_out) {
+  g_last_error.clear();
+  if (plan_out == nullptr) return fail(VC_ERR_NULL, "plan pointer is NULL");
+  Plan plan;
+  Outputs oo;
+  vc_status st = plan_sweep(cases, n_cases, tols, n_tols, opts, out, plan, oo);
+  if (st != VC_OK) return st;
+  if (ws == nullptr) return fail(VC_ERR_WORKSPACE, "workspace is NULL");
+  if (ws_bytes < plan.bytes)
+    return fail(VC_ERR_WORKSPACE, "workspace has %zu bytes, %zu required", ws_bytes, plan.bytes);
+  int dev = 0;
+  st = current_device(dev);
+  if (st != VC_OK) return st;
+  const hipStream_t stream = (hipStream_t)stream_;
+  uint8_t *base = (uint8_t *)(((uintptr_t)ws + kAlign - 1) / kAlign * kAlign);
+  const vck::Params P = make_params(plan, tols, oo, base, false);
+  // the case table stays in the workspace; the zero-on-entry parts are
+  // cleared once here and by every launch's finalize afterwards
+  if (plan.n_cases > 0) {
+    const std::vector<uint8_t> blob = plan_blob(plan);
+    st = hip_check(hipMemcpyAsync(base + plan.off_table, blob.data(), blob.size(),
+                                  hipMemcpyHostToDevice, stream),
+                   "descriptor upload");
+    if (st != VC_OK) return st;
+  }
+  const vck::Prologue Q = make_prologue(plan, P, base, nullptr);
+  st = hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  if (st == VC_OK) st = hip_check(hipStreamSynchronize(stream), "hipStreamSynchronize");
+  if (st != VC_OK) return st;
+  vc_plan *p = new (std::nothrow) vc_plan;
+  if (p == nullptr) return fail(VC_ERR_LIMIT, "out of host memory");
+  p->plan = std::move(plan);
+  p->P = P;
+  p->device = dev;
+  *plan_out = p;
+  return VC_OK;
+}
+
+vc_status vcheck_plan_launch(vc_plan *plan, void *stream_) {
+  g_last_error.clear();
+  if (plan == nullptr) return fail(VC_ERR_NULL, "plan is NULL");
+  int dev = 0;
+  vc_status st = current_device(dev);
+  if (st != VC_OK) return st;
+  if (dev != plan->device)
+    return fail(VC_ERR_STATE, "the plan was made on device %d, the current device is %d",
+                plan->device, dev);
+  const hipStream_t stream = (hipStream_t)stream_;
+  if (plan->plan.n_cases == 0) {
+    vck::Prologue Q;  // zero rates only
+    memset(&Q, 0, sizeof Q);
+    Q.match_rate = plan->P.match_rate;
+    Q.numeric_rate = plan->P.numeric_rate;
+    Q.n_tols = plan->plan.n_tols;
+    return hip_check(vck::launch_prologue(Q, stream), "prologue launch");
+  }
+  return launch_streaming(plan->plan, plan->P, stream);
+}
+
+vc_status vcheck_plan_free(vc_plan *plan) {
+  g_last_error.clear();
+  delete plan;
+  return VC_OK;
 }
 
 vc_status vcheck_workspace_bytes(const vc_case *cases, int32_t n_cases, int32_t n_tols,
@@ -867,14 +1026,14 @@ vc_status vcheck_workspace_bytes(const vc_case *cases, int32_t n_cases, int32_t 
   if (opts != nullptr) o = *opts;
   if (n_tols < 1 || n_tols > VC_MAX_TOLS)
     return fail(VC_ERR_LIMIT, "n_tols %d outside 1..%d", n_tols, VC_MAX_TOLS);
-  // sizing does not depend on tolerance values or tile geometry
+  // sizing does not depend on tolerance values; tile geometry >= 1 x 1
+  // means tile maps (4 bytes of accumulator per tile)
   vc_tol dummy[VC_MAX_TOLS];
   for (auto &t : dummy) t = vc_tol{0.0, 0.0, 0, 0};
-  o.tile_h = o.tile_h < 1 ? 1 : o.tile_h;
-  o.tile_w = o.tile_w < 1 ? 1 : o.tile_w;
+  const bool tiles = o.tile_h >= 1 && o.tile_w >= 1;
   if (o.primary_tol < 0 || o.primary_tol >= n_tols) o.primary_tol = 0;
   Plan plan;
-  const vc_status st = make_plan(cases, n_cases, dummy, n_tols, o, false, o.k > 0, false, plan);
+  const vc_status st = make_plan(cases, n_cases, dummy, n_tols, o, tiles, o.k > 0, false, plan);
   if (st != VC_OK) return st;
   *bytes = plan.bytes;
   return VC_OK;
@@ -903,6 +1062,7 @@ const char *vcheck_status_str(vc_status status) {
     case VC_ERR_LIMIT: return "a count is outside its supported range";
     case VC_ERR_HIP: return "HIP runtime error";
     case VC_ERR_ALIGN: return "data pointer not aligned to its element size";
+    case VC_ERR_STATE: return "library state does not allow the call (see vcheck_last_error)";
     default: return "unknown status";
   }
 }

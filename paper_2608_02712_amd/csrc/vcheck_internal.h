@@ -38,8 +38,8 @@ __device__ __forceinline__ uint32_t div_by(uint32_t n, uint32_t m, uint32_t shif
 }
 
 // Device-side case descriptor. The host builds one per case, in launch
-// order (grouped by dtype), and the prologue kernel copies the table into
-// the workspace. Every case owns at least one chunk: a case that is not
+// order (grouped by dtype), and uploads the table into the workspace (once
+// for a prepared sweep). Every case owns at least one chunk: a case that is not
 // evaluated (status != 0) or is empty gets one chunk with no elements, so
 // its results are written by the same completion path as every other case.
 struct DevCase {
@@ -61,7 +61,7 @@ struct DevCase {
   uint32_t dtype;
   uint32_t unit_elems;   // elements per wave range; a chunk is 4 of them
   DivMagic cols_div;     // division by cols (when cols < 2^31)
-  uint32_t pad[2];
+  uint64_t n_tiles;      // tiles of the case's map (0 without tile maps)
 };
 static_assert(sizeof(DevCase) == 176, "DevCase layout");
 
@@ -89,8 +89,9 @@ constexpr uint32_t kEqCandRef = 1u;        // bit 0: cand bit-equal to ref
 constexpr int kEqCandInpShift = 8;         // bits 8..15: cand bit-equal to input j
 constexpr int kEqRefInpShift = 16;         // bits 16..23: ref bit-equal to input j
 
-// Suite counters in the workspace (cleared by the prologue, incremented by
-// the finalize launches; the block that completes the last case reads them).
+// Suite counters in the workspace (zero on entry: cleared by the prologue of
+// a one-shot call, and by the block that completes the last case, which
+// reads them, for the next call of a prepared sweep).
 struct Counters {
   uint32_t pass[VC_MAX_TOLS];       // cases passing pair p numerically
   uint32_t cert[VC_MAX_TOLS];       // ... and with no integrity flag
@@ -103,8 +104,8 @@ static_assert(sizeof(Counters) == 128, "Counters layout");
 struct Params {
   const DevCase *cases;        // device table, or nullptr: use `single`
   const uint64_t *case_chunk;  // [table entries] chunk_begin, for the case lookup
-  const uint64_t *case_group;  // [table entries] group_begin, for the case lookup
-  const uint32_t *multi;       // table indices of the cases with more than one group
+  const uint32_t *group_case;  // [groups] table index of each chunk group, or nullptr
+                               // when every case has one group (group = table index)
   int32_t n_cases;             // table entries (= caller cases)
   int32_t n_tols;              // 1 .. 8 (the kernel evaluates NT >= n_tols pairs)
   int32_t primary;
@@ -116,7 +117,6 @@ struct Params {
   int32_t tier1;               // 1: the binary32 fast path is valid for these pairs
   uint32_t unit_elems;         // elements per wave range (one quarter of a chunk)
   uint32_t eqnan_mask;         // bit p: equal_nan of pair p
-  uint32_t split;              // 1: each wave streams one contiguous quarter of a chunk
   uint64_t chunk_lo;           // first global chunk of this launch
   uint64_t case_lo;            // first table index of this launch's cases
   uint64_t case_hi;
@@ -131,7 +131,12 @@ struct Params {
   ChunkRec *grecs;             // [total groups]
   uint32_t *gstage;            // [total groups * k]
   Counters *ctr;
-  uint32_t *tile_maps;         // user tile maps (nullable)
+  uint32_t *gdone;             // [table entries] groups merged (zero on entry)
+  uint32_t *tile_maps;         // tile-count accumulators in the workspace (zero on
+                               // entry), nullable
+  uint32_t *tile_out;          // user tile maps, written by the finalize (nullable)
+  uint64_t tiles_total;        // tiles of all maps of the call
+  uint64_t n_groups;           // chunk groups of the call (finalize blocks that merge)
   // outputs
   vc_stats *stats;
   uint64_t *mismatches;
@@ -143,8 +148,9 @@ struct Params {
   DevCase single;
 };
 
-// Work of the prologue kernel: copy the descriptor blob from pinned host
-// memory, clear the counter area and the tile maps.
+// Work of the prologue kernel of a one-shot call: copy the descriptor blob
+// from pinned host memory (when staged there), clear the counters and the
+// tile-count accumulators.
 struct Prologue {
   const uint8_t *blob_src;  // device-visible pinned host pointer (or nullptr)
   uint8_t *blob_dst;
@@ -267,7 +273,6 @@ hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_grou
 hipError_t launch_prologue(const Prologue &p, hipStream_t s);
 hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint64_t n_chunks,
                        hipStream_t s);
-hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi,
-                           hipStream_t s);
+hipError_t launch_finalize(const Params &p, hipStream_t s);
 
 }  // namespace vck

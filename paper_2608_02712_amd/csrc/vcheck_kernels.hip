@@ -231,6 +231,7 @@ __device__ __forceinline__ DevCase load_case(const VCK_CONST DevCase *t) {
   d.unit_elems = t->unit_elems;
   d.cols_div.m = t->cols_div.m;
   d.cols_div.shifts = t->cols_div.shifts;
+  d.n_tiles = t->n_tiles;
   return d;
 }
 
@@ -369,6 +370,11 @@ __device__ __forceinline__ float f32_next_up(float x) {
 constexpr int kParts = 8;
 constexpr int kPartLen = kBlockThreads / kParts;
 
+static_assert(offsetof(ChunkRec, nfound) == 92 && offsetof(ChunkRec, eq_bits) == 96 &&
+                  offsetof(ChunkRec, amax_abs) == 100 && offsetof(ChunkRec, max_abs) == 112 &&
+                  offsetof(ChunkRec, max_rel) == 120 && offsetof(ChunkRec, sum_abs) == 128,
+              "neutral record layout");
+
 struct MergeScratch {
   ChunkRec rec[kBlockThreads];
   uint64_t part[kParts][kRecCounts];
@@ -425,60 +431,112 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
       u32x4 *dst = (u32x4 *)&s.rec[t];
 #pragma unroll
       for (int q = 0; q < (int)(sizeof(ChunkRec) / 16); ++q) dst[q] = v[q];
+    } else {
+      // the slots past the pass's last record hold the neutral record
+      // (no counts, no entries, all equality bits, no maximum), so the
+      // part loops below run over whole parts without selects
+      u32x4 *dst = (u32x4 *)&s.rec[t];
+      const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int q = 0; q < 6; ++q) dst[q] = z;                   // words 0..23
+      dst[6] = (u32x4){0xffffffffu, kNone, kNone, 0u};           // eq_bits, amax, pad
+      dst[7] = (u32x4){0u, 0xbff00000u, 0u, 0xbff00000u};        // max_abs = max_rel = -1
+      dst[8] = z;                                                // sums
     }
     __syncthreads();
-    // part reductions: part p covers records [32p, 32p + 32) of this pass
+    // part reductions: part p covers records [32p, 32p + 32) of this pass.
+    // Each loop is unrolled with its LDS reads issued first, so the roles
+    // that share a wave do not wait on per-record round trips.
     if (t < (uint32_t)(kParts * kRecCounts)) {
-      const uint32_t f = t % kRecCounts, p = t / kRecCounts;
-      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
-      uint64_t a = 0;
-      for (uint32_t r = lo; r < hi; ++r) a += ((const uint32_t *)&s.rec[r])[f];
+      // a record count is at most 2^25 (one group), so a part fits 32 bits
+      const uint32_t f = t % kRecCounts, p = t / kRecCounts, lo = p * kPartLen;
+      const uint32_t *col = (const uint32_t *)&s.rec[lo] + f;
+      uint32_t xs[kPartLen];
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) xs[j] = col[j * (int)(sizeof(ChunkRec) / 4)];
+      uint32_t a = 0;
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) a += xs[j];
       s.part[p][f] = a;
     } else if (t < (uint32_t)(kParts * kRecCounts + 2 * kParts)) {
-      const uint32_t u = t - kParts * kRecCounts, f = u & 1u, p = u >> 1;
-      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
-      double a = 0.0;
-      for (uint32_t r = lo; r < hi; ++r) a += f ? s.rec[r].sum_rel : s.rec[r].sum_abs;
+      const uint32_t u = t - kParts * kRecCounts, f = u & 1u, p = u >> 1, lo = p * kPartLen;
+      const double *col = f ? &s.rec[lo].sum_rel : &s.rec[lo].sum_abs;
+      double xs[kPartLen];
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) xs[j] = col[j * (int)(sizeof(ChunkRec) / 8)];
+      double a = 0.0;  // (sums are >= 0: a neutral slot adds +0 exactly)
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) a += xs[j];
       s.dpart[f][p] = a;
     } else if (t < (uint32_t)(kParts * kRecCounts + 4 * kParts)) {
+      // Records of a part cover ascending, disjoint element ranges, so on
+      // equal maxima the earlier record holds the smaller index: a strict
+      // comparison keeps it. A record without a maximum holds -1.
       const uint32_t u = t - kParts * kRecCounts - 2 * kParts, f = u & 1u, p = u >> 1;
-      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
+      const uint32_t lo = p * kPartLen;
+      const double *vcol = f ? &s.rec[lo].max_rel : &s.rec[lo].max_abs;
+      const uint32_t *icol = f ? &s.rec[lo].amax_rel : &s.rec[lo].amax_abs;
+      double xs[kPartLen];
+      uint32_t as[kPartLen];
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) {
+        xs[j] = vcol[j * (int)(sizeof(ChunkRec) / 8)];
+        as[j] = icol[j * (int)(sizeof(ChunkRec) / 4)];
+      }
       double v = -1.0;
-      uint64_t ix = UINT64_MAX;
-      for (uint32_t r = lo; r < hi; ++r) {
-        const ChunkRec &x = s.rec[r];
-        const uint32_t a = f ? x.amax_rel : x.amax_abs;
-        if (a != kNone) max_merge(v, ix, f ? x.max_rel : x.max_abs, (uint64_t)(base + r) * span + a);
+      uint32_t bj = 0, ba = 0;
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) {
+        const bool take = xs[j] > v;
+        v = take ? xs[j] : v;
+        bj = take ? (uint32_t)j : bj;
+        ba = take ? as[j] : ba;
       }
       s.mv[f][p] = v;
-      s.mi[f][p] = ix;
+      s.mi[f][p] = v > -1.0 ? (uint64_t)(base + lo + bj) * span + ba : UINT64_MAX;
     } else if (t < (uint32_t)(kParts * kRecCounts + 5 * kParts)) {
-      const uint32_t p = t - kParts * kRecCounts - 4 * kParts;
-      const uint32_t lo = p * kPartLen, hi = min(lo + kPartLen, m);
-      uint32_t e = 0xffffffffu, c = 0;
-      for (uint32_t r = lo; r < hi; ++r) {
-        e &= s.rec[r].eq_bits;
-        c = sat_add(c, s.rec[r].nfound, k);
+      const uint32_t p = t - kParts * kRecCounts - 4 * kParts, lo = p * kPartLen;
+      uint32_t eb[kPartLen], nf[kPartLen];
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) {
+        eb[j] = s.rec[lo + j].eq_bits;
+        nf[j] = s.rec[lo + j].nfound;
+      }
+      uint32_t e = 0xffffffffu, c = 0;  // (entries <= k each: no overflow)
+#pragma unroll
+      for (int j = 0; j < kPartLen; ++j) {
+        e &= eb[j];
+        c += nf[j];
       }
       s.eqp[p] = e;
-      s.nfp[p] = c;
+      s.nfp[p] = min(c, k);
     }
     __syncthreads();
+    // totals over the parts, one role per wave
     if (t < (uint32_t)kRecCounts) {
       uint64_t a = s.cnt[t];
+#pragma unroll
       for (int p = 0; p < kParts; ++p) a += s.part[p][t];
       s.cnt[t] = a;
-    } else if (t == 32 || t == 33) {
-      const uint32_t f = t - 32;
+    } else if (t == 64 || t == 65) {
+      const uint32_t f = t - 64;
       double a = f ? s.sum_rel : s.sum_abs;
+#pragma unroll
       for (int p = 0; p < kParts; ++p) a += s.dpart[f][p];
       if (f) s.sum_rel = a;
       else s.sum_abs = a;
-    } else if (t == 34 || t == 35) {
-      const uint32_t f = t - 34;
+    } else if (t == 128 || t == 129) {
+      const uint32_t f = t - 128;
       double v = f ? s.max_rel : s.max_abs;
       uint64_t ix = f ? s.amax_rel : s.amax_abs;
-      for (int p = 0; p < kParts; ++p) max_merge(v, ix, s.mv[f][p], s.mi[f][p]);
+#pragma unroll
+      for (int p = 0; p < kParts; ++p) {
+        const double x = s.mv[f][p];
+        const uint64_t xi = s.mi[f][p];
+        const bool take = (x > v) | ((x == v) & (xi < ix));
+        v = take ? x : v;
+        ix = take ? xi : ix;
+      }
       if (f) {
         s.max_rel = v;
         s.amax_rel = ix;
@@ -486,12 +544,14 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
         s.max_abs = v;
         s.amax_abs = ix;
       }
-    } else if (t == 36) {
+    } else if (t == 192) {
       uint32_t e = s.eq_all;
+#pragma unroll
       for (int p = 0; p < kParts; ++p) e &= s.eqp[p];
       s.eq_all = e;
-    } else if (t == 37) {
+    } else if (t == 193) {
       uint32_t c = s.nf_total;
+#pragma unroll
       for (int p = 0; p < kParts; ++p) {
         s.nfpre[p] = c;
         c = sat_add(c, s.nfp[p], k);
@@ -502,9 +562,14 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
       // first output position of each record: its part's prefix plus the
       // entries of the records before it in the part
       if (t < m) {
-        const uint32_t p = t / kPartLen;
+        const uint32_t p = t / kPartLen, lo = p * kPartLen;
         uint32_t pos = s.nfpre[p];
-        for (uint32_t r = p * kPartLen; r < t; ++r) pos = sat_add(pos, s.rec[r].nfound, k);
+        uint32_t nf[kPartLen];
+#pragma unroll
+        for (int j = 0; j < kPartLen; ++j) nf[j] = s.rec[lo + j].nfound;
+#pragma unroll
+        for (int j = 0; j < kPartLen; ++j) pos += lo + j < t ? nf[j] : 0u;
+        pos = min(pos, k);  // (pos <= k + 32 k before the clamp)
         s.nfstart[t] = pos;
       }
       __syncthreads();
@@ -525,7 +590,7 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
       }
       __syncthreads();
     }
-    if (t == 37) s.nf_total = sat_add(s.nfpre[kParts - 1], s.nfp[kParts - 1], k);
+    if (t == 193) s.nf_total = sat_add(s.nfpre[kParts - 1], s.nfp[kParts - 1], k);
   }
   __syncthreads();
 }
@@ -632,6 +697,7 @@ __device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P,
     g.reserved = 0;
     if (P.integ != nullptr) P.integ[oi] = g;
   }
+  if (P.match_rate == nullptr && P.numeric_rate == nullptr) return;
   // suite counters
   for (int p = 0; p < nt; ++p) {
     if (ok && cnt(p) == 0) {
@@ -639,7 +705,6 @@ __device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P,
       if (flags == 0) atomicAdd(&P.ctr->cert[p], 1u);
     }
   }
-  if (P.match_rate == nullptr && P.numeric_rate == nullptr) return;
   // The case written last writes the suite rates. Its increment of the
   // completion count acquires what every earlier case released with its
   // own increment (the counter updates above), so it reads final counters.
@@ -654,7 +719,12 @@ __device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P,
                                             __HIP_MEMORY_SCOPE_AGENT);
     if (P.match_rate != nullptr) P.match_rate[p] = (double)cert / nc;
     if (P.numeric_rate != nullptr) P.numeric_rate[p] = (double)num / nc;
+    // every other case has finished with the counters: clear them for the
+    // next call of a prepared sweep
+    P.ctr->pass[p] = 0;
+    P.ctr->cert[p] = 0;
   }
+  P.ctr->done = 0;
 }
 
 // Last table entry (in [lo, hi)) whose value in `first` is <= x; `first`
@@ -756,6 +826,14 @@ void main_kernel(const Params P) {
   const uint64_t cstart = rel_chunk * CH;
   const uint64_t cend = dcs.status != 0 ? cstart : min(cstart + CH, numel);
   const int prim = P.primary;
+  // The wave's first step (chunk step `wave`, when the chunk has it) is
+  // loaded here, so that its latency overlaps the block set-up below.
+  u32x4 pre_c = {0u, 0u, 0u, 0u}, pre_r = {0u, 0u, 0u, 0u};
+  if (vec && (uint64_t)(wave + 1) * ITER <= cend - cstart) {
+    const uint64_t i0 = cstart + (uint64_t)wave * ITER;
+    pre_c = load16(cand + i0 * ES + lane * 16u);
+    pre_r = load16(ref + i0 * ES + lane * 16u);
+  }
   // Params fields used by the step lambdas, as locals: the lambdas capture by
   // reference, and a captured by-value argument would live in private memory.
   const int32_t kk = P.k;
@@ -1681,29 +1759,27 @@ void main_kernel(const Params P) {
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, off0);
   };
 
-  // Steps of ITER elements (one KiB per wave and tensor). Either wave w
-  // streams the contiguous quarter [w q, (w + 1) q) of the chunk's steps
-  // (split), or it takes steps w, w+4, w+8, ... (round robin, the block
-  // streaming its chunk front to back); the partial tail step goes to the
-  // wave whose range it continues. (32-bit counters: a chunk holds fewer than
-  // 2^18 elements, and uniform 32-bit arithmetic stays on the scalar unit.)
+  // Steps of ITER elements (one KiB per wave and tensor), taken by the four
+  // waves in rounds of four consecutive steps, so the block streams its
+  // chunk front to back. With binary32 storage wave w takes position w of
+  // every round; with 16-bit storage the positions rotate by one per round
+  // (wave w takes position (w + round) mod 4): a faulty tile repeats at the
+  // same column of every row, and rows of 16-bit data are often exactly four
+  // steps long, so without the rotation all of its steps would fall to one
+  // wave. The partial tail step goes to the wave owning its position. (32-bit
+  // counters: a chunk holds fewer than 2^18 elements, and uniform 32-bit
+  // arithmetic stays on the scalar unit.)
   const uint32_t n_steps = (uint32_t)((cend - cstart) / ITER);  // full steps in the chunk
   // binary32 storage: round robin; 16-bit storage: rotated rounds
-  constexpr bool split = false;
   constexpr bool rot = ES == 2;
-  const uint32_t q_steps = (n_steps + 3) / 4;
-  const uint32_t w_first = split ? min(wave * q_steps, n_steps) : wave;
-  const uint32_t w_stride = split ? 1u : 4u;
   const uint32_t n_rounds = n_steps / 4, n_part = n_steps % 4;
   const uint32_t n_full = rot ? n_rounds + (((wave + n_rounds) & 3u) < n_part ? 1u : 0u)
-                          : split ? min(w_first + q_steps, n_steps) - w_first
-                                  : (n_steps > wave ? (n_steps - wave + 3) / 4 : 0u);
-  const bool tail_here = rot ? ((n_part - n_rounds) & 3u) == wave
-                         : split ? wave == 3 : n_part == wave;
+                              : (n_steps > wave ? (n_steps - wave + 3) / 4 : 0u);
+  const bool tail_here = rot ? ((n_part - n_rounds) & 3u) == wave : n_part == wave;
   const uint32_t lane_off = lane * V;
   // chunk step index of the wave's step st
   auto step_idx = [&](uint32_t st) __attribute__((always_inline)) {
-    return rot ? 4u * st + ((wave + st) & 3u) : w_first + w_stride * st;
+    return rot ? 4u * st + ((wave + st) & 3u) : wave + 4u * st;
   };
   // chunk offset of this lane's first element in the wave's step st
   auto step_off = [&](uint32_t st) __attribute__((always_inline)) {
@@ -1749,8 +1825,8 @@ void main_kernel(const Params P) {
       return load16(base + off(st));
     };
     uint32_t st = 0;
+    u32x4 ca = pre_c, ra = pre_r;  // step 0 (loaded before the set-up)
     while (st < n_full) {
-      u32x4 ca = ld(cb, st), ra = ld(rb, st);
       while (st + 1 < n_full && nd + 2 <= (uint32_t)kDeferCap) {
         const u32x4 cn = ld(cb, st + 1), rn = ld(rb, st + 1);
         __builtin_amdgcn_s_waitcnt(kWaitVm2);
@@ -1766,7 +1842,11 @@ void main_kernel(const Params P) {
         step(ca, ra, step_off(st));
         st += 1;
       }
-      if (st < n_full) flush();  // the list is full and steps remain
+      if (st < n_full) {  // the list is full and steps remain
+        flush();
+        ca = ld(cb, st);
+        ra = ld(rb, st);
+      }
     }
   } else {
     for (uint32_t st = 0; st < n_full; ++st) {
@@ -1946,19 +2026,58 @@ void main_kernel(const Params P) {
 
 // ------------------------------------------------------------ finalize
 
-// First finalize launch, one block per chunk group of the call: a case with
-// one group is written directly from its chunk records; the group of a
-// larger case is merged into a group record (the second launch, one block
-// per such case, merges those). Kernel boundaries order the records, so no
-// device-wide fences are needed.
+// Tile blocks of the finalize launch (the blocks past the group blocks):
+// copy the accumulated tile counts of the whole call to the tile-map output
+// and clear the accumulators for the next call. Each thread moves
+// kTileRun counts per round, all loaded before any is stored.
+constexpr int kTileRun = 8;
+
+__device__ __forceinline__ void publish_tiles(const Params &P) {
+  uint32_t *__restrict__ acc = P.tile_maps;
+  uint32_t *__restrict__ out = P.tile_out;
+  const uint64_t n = P.tiles_total;
+  const uint64_t nb = gridDim.x - P.n_groups, b = blockIdx.x - P.n_groups;
+  constexpr uint64_t kPer = (uint64_t)kBlockThreads * kTileRun;
+  for (uint64_t base = b * kPer + threadIdx.x; base < n; base += nb * kPer) {
+    uint32_t v[kTileRun];
+#pragma unroll
+    for (int q = 0; q < kTileRun; ++q) {
+      const uint64_t i = base + (uint64_t)q * kBlockThreads;
+      v[q] = i < n ? acc[i] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < kTileRun; ++q) {
+      const uint64_t i = base + (uint64_t)q * kBlockThreads;
+      if (i < n) {
+        out[i] = v[q];
+        acc[i] = 0;
+      }
+    }
+  }
+}
+
+// One finalize launch, one block per chunk group of the call (a group is up
+// to kGroupChunks consecutive chunks of one case). A case with one group is
+// written directly from its chunk records. For a larger case each group
+// block merges its chunks into a group record; the group block that arrives
+// last (an acquire-release count per case) then merges the case's group
+// records in group order and writes the results, so the merge order, and
+// with it every output bit, does not depend on which block arrives last.
+// The blocks past the group blocks publish the tile counts. Kernel
+// boundaries order the chunk records and tile counts before this launch.
 __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P) {
   __shared__ MergeScratch M;
+  __shared__ uint32_t s_last;
   const uint64_t g = blockIdx.x;
+  if (g >= P.n_groups) {
+    publish_tiles(P);
+    return;
+  }
   const VCK_CONST DevCase *table = (const VCK_CONST DevCase *)P.cases;
   uint64_t ci = 0;
   DevCase cs;
   if (table != nullptr) {
-    ci = find_entry(P.case_group, 0, (uint64_t)P.n_cases, g);
+    ci = P.group_case != nullptr ? (uint64_t)((const VCK_GLOBAL uint32_t *)P.group_case)[g] : g;
     cs = load_case(table + ci);
   } else {
     cs = P.single;
@@ -1980,63 +2099,46 @@ __global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P)
   const uint64_t CH = 4ull * cs.unit_elems;
   const uint32_t k = P.k > 0 ? (uint32_t)P.k : 0u;
   const uint64_t cstride = k;
+  const uint32_t g_local = (uint32_t)(g - cs.group_begin);
   if (cs.n_groups == 1) {
     finalize_case(M, F, cs, P.recs + cs.chunk_begin, cs.n_chunks, CH,
                   P.stage + cs.chunk_begin * cstride, cstride);
     return;
   }
-  const uint32_t g_local = (uint32_t)(g - cs.group_begin);
   const uint32_t gc0 = g_local * kGroupChunks;
   const uint32_t gchunks = min((uint32_t)kGroupChunks, cs.n_chunks - gc0);
   const ChunkRec *const grp = P.recs + cs.chunk_begin + gc0;
   merge_all<false>(M, grp, gchunks, CH, P.stage + (cs.chunk_begin + gc0) * cstride, cstride, k,
                    P.gstage + g * k, nullptr);
   const uint32_t gnf = M.nf_total;
-  {
-    ChunkRec *const gr = P.grecs + g;
-    const uint32_t q = threadIdx.x;
-    if (q < (uint32_t)kRecCounts) {
-      ((uint32_t *)gr)[q] = (uint32_t)M.cnt[q];
-    } else if (q == 32) {
-      gr->nfound = gnf;
-      gr->eq_bits = M.eq_all;
-      gr->amax_abs = M.amax_abs == UINT64_MAX ? kNone : (uint32_t)M.amax_abs;
-      gr->amax_rel = M.amax_rel == UINT64_MAX ? kNone : (uint32_t)M.amax_rel;
-      gr->pad = 0;
-      gr->max_abs = M.max_abs;
-      gr->max_rel = M.max_rel;
-      gr->sum_abs = M.sum_abs;
-      gr->sum_rel = M.sum_rel;
-    }
+  if (threadIdx.x == 0) {
+    ChunkRec r;
+#pragma unroll
+    for (int q = 0; q < kRecCounts; ++q) ((uint32_t *)&r)[q] = (uint32_t)M.cnt[q];
+    r.nfound = gnf;
+    r.eq_bits = M.eq_all;
+    r.amax_abs = M.amax_abs == UINT64_MAX ? kNone : (uint32_t)M.amax_abs;
+    r.amax_rel = M.amax_rel == UINT64_MAX ? kNone : (uint32_t)M.amax_rel;
+    r.pad = 0;
+    r.max_abs = M.max_abs;
+    r.max_rel = M.max_rel;
+    r.sum_abs = M.sum_abs;
+    r.sum_rel = M.sum_rel;
+    P.grecs[g] = r;
   }
-}
-
-// Second finalize launch: block i writes the results of multi-group case
-// P.multi[i] (or of the single case) from its group records.
-__global__ __launch_bounds__(kBlockThreads) void finalize_multi_kernel(const Params P) {
-  __shared__ MergeScratch M;
-  DevCase cs;
-  if (P.cases != nullptr)
-    cs = load_case((const VCK_CONST DevCase *)P.cases +
-                   ((const VCK_GLOBAL uint32_t *)P.multi)[blockIdx.x]);
-  else
-    cs = P.single;
-  FinArgs F;
-  F.stats = P.stats;
-  F.mismatches = P.mismatches;
-  F.pass_out = P.pass_out;
-  F.first_k = P.first_k;
-  F.integ = P.integ;
-  F.match_rate = P.match_rate;
-  F.numeric_rate = P.numeric_rate;
-  F.ctr = P.ctr;
-  F.n_cases = P.n_cases;
-  F.n_tols = P.n_tols;
-  F.primary = P.primary;
-  F.k = P.k;
-  F.do_integ = P.do_integ;
-  const uint64_t CH = 4ull * cs.unit_elems;
-  const uint32_t k = P.k > 0 ? (uint32_t)P.k : 0u;
+  // Publish the group record and first-k list (written by several waves):
+  // each wave releases its own stores, then one count per group.
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t prev =
+        __hip_atomic_fetch_add(&P.gdone[ci], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = prev + 1 == cs.n_groups ? 1u : 0u;
+  }
+  __syncthreads();
+  if (s_last == 0) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  if (threadIdx.x == 0) P.gdone[ci] = 0;  // (cleared for the next call)
   finalize_case(M, F, cs, P.grecs + cs.group_begin, cs.n_groups, CH * kGroupChunks,
                 P.gstage + cs.group_begin * k, k);
 }
@@ -2097,20 +2199,15 @@ hipError_t launch_prologue(const Prologue &p, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_finalize(const Params &p, uint64_t n_groups, uint64_t n_multi,
-                           hipStream_t s) {
-  if (n_groups > 0) {
-    hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)n_groups), dim3(kBlockThreads), 0, s, p);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  if (n_multi > 0) {
-    hipLaunchKernelGGL(finalize_multi_kernel, dim3((uint32_t)n_multi), dim3(kBlockThreads), 0, s,
-                       p);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+hipError_t launch_finalize(const Params &p, hipStream_t s) {
+  constexpr uint64_t kPer = (uint64_t)kBlockThreads * kTileRun;
+  uint64_t tile_blocks = 0;
+  if (p.tile_out != nullptr && p.tile_maps != nullptr && p.tiles_total > 0)
+    tile_blocks = min((p.tiles_total + kPer - 1) / kPer, (uint64_t)1024);
+  const uint64_t blocks = p.n_groups + tile_blocks;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)blocks), dim3(kBlockThreads), 0, s, p);
+  return hipGetLastError();
 }
 
 hipError_t launch_main(int dtype, int nt_class, int integ, const Params &p, uint64_t n_chunks,

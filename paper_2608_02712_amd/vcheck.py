@@ -6,9 +6,10 @@ functions carry the C names (``vcheck_compare``, ``vcheck_localize``,
 ``vcheck_integrity``, ``vcheck_sweep``, ``vcheck_workspace_bytes``,
 ``vcheck_tile_count``); each synchronous wrapper allocates outputs and a
 workspace with torch, launches on the current stream, waits, and returns the
-results as Python values. ``Sweep`` prepares a call once and relaunches it
-without allocating (for timing loops and repeated validation of one case
-matrix).
+results as Python values. ``Sweep`` prepares a sweep once
+(``vcheck_plan_sweep``: the case table stays in the workspace) and relaunches
+it without allocating or uploading anything (``vcheck_plan_launch``), for
+repeated validation of one case matrix and for timing loops.
 
 There is no fallback: if libvcheck.so is missing or fails to load, every call
 raises.
@@ -33,7 +34,7 @@ FLAG_LOWPREC_BF16, FLAG_LOWPREC_FP16 = 8, 16
 
 STATUS_NAMES = {0: "VC_OK", -1: "VC_ERR_NULL", -2: "VC_ERR_DTYPE", -3: "VC_ERR_SHAPE",
                 -4: "VC_ERR_TOL", -5: "VC_ERR_TILE", -6: "VC_ERR_K", -7: "VC_ERR_WORKSPACE",
-                -8: "VC_ERR_LIMIT", -9: "VC_ERR_HIP", -10: "VC_ERR_ALIGN"}
+                -8: "VC_ERR_LIMIT", -9: "VC_ERR_HIP", -10: "VC_ERR_ALIGN", -11: "VC_ERR_STATE"}
 
 _DTYPES = {torch.float32: VC_F32, torch.float16: VC_F16, torch.bfloat16: VC_BF16}
 
@@ -153,11 +154,19 @@ def lib() -> ctypes.CDLL:
                                   P, P, ctypes.c_size_t, P]
     L.vcheck_nearpass_workspace.argtypes = [ctypes.POINTER(VcCase), ctypes.c_int32,
                                             ctypes.POINTER(ctypes.c_size_t)]
+    L.vcheck_plan_sweep.argtypes = [ctypes.POINTER(VcCase), ctypes.c_int32, ctypes.POINTER(VcTol),
+                                    ctypes.c_int32, ctypes.POINTER(VcSweepOpts),
+                                    ctypes.POINTER(VcSweepOut), P, ctypes.c_size_t, P,
+                                    ctypes.POINTER(ctypes.c_void_p)]
+    L.vcheck_plan_launch.argtypes = [P, P]
+    L.vcheck_plan_free.argtypes = [P]
+    L.vcheck_init.argtypes = []
     for name in ("vcheck_compare", "vcheck_localize", "vcheck_integrity", "vcheck_sweep",
                  "vcheck_workspace_bytes", "vcheck_tensor_stats",
                  "vcheck_tensor_stats_workspace", "vcheck_nearpass",
                  "vcheck_nearpass_workspace", "vcheck_content_hash",
-                 "vcheck_content_hash_workspace"):
+                 "vcheck_content_hash_workspace", "vcheck_plan_sweep", "vcheck_plan_launch",
+                 "vcheck_plan_free", "vcheck_init"):
         getattr(L, name).restype = ctypes.c_int32
     if L.vcheck_abi_version() != 1:
         raise RuntimeError("libvcheck.so ABI version mismatch")
@@ -299,7 +308,7 @@ def vcheck_integrity(cand: torch.Tensor, ref: torch.Tensor, inputs, atol: float,
     inputs = list(inputs)
     case, keep = _single_case(cand, ref, inputs)
     tol = _tols([(atol, rtol, int(equal_nan))])
-    opts = VcSweepOpts(0, 1, 1, 0, 1, 0)
+    opts = VcSweepOpts(0, 0, 0, 0, 1, 0)
     nbytes = vcheck_workspace_bytes(case, 1, opts)
     ws = _ws(nbytes, ref.device)
     out = torch.zeros(88, dtype=torch.uint8, device=ref.device)
@@ -313,17 +322,24 @@ def vcheck_integrity(cand: torch.Tensor, ref: torch.Tensor, inputs, atol: float,
 
 
 class Sweep:
-    """A prepared vcheck_sweep call over a fixed case matrix.
+    """A vcheck_sweep call over a fixed case matrix.
 
     cases: list of (cand, ref) or (cand, ref, [inputs]) torch tensors.
     tols: list of (atol, rtol[, equal_nan]). tile: (tile_h, tile_w) or None;
     k: first-k length or 0; integrity: run the detectors.
-    ``launch()`` enqueues the call on a stream without allocating;
-    ``results()`` synchronises and returns the outputs.
+    mode: "prepared" (default): the sweep is prepared once
+    (vcheck_plan_sweep) and each ``launch()`` runs vcheck_plan_launch;
+    "oneshot": each ``launch()`` is a full vcheck_sweep call. ``launch()``
+    enqueues on a stream without allocating; ``results()`` synchronises and returns the outputs.
     """
 
     def __init__(self, cases, tols, primary: int = 0, tile=None, k: int = 0,
-                 integrity: bool = False, rates: bool = True, device=None):
+                 integrity: bool = False, rates: bool = True, device=None, mode="prepared",
+                 stream=None):
+        if mode not in ("prepared", "oneshot"):
+            raise ValueError("unknown mode %r" % (mode,))
+        self.mode = mode
+        self._plan = None
         self.n_cases = len(cases)
         self.n_tols = len(tols)
         self.k = int(k)
@@ -347,10 +363,10 @@ class Sweep:
         dev = torch.device(dev if dev is not None else "cuda")
         self.device = dev
         self.tols = _tols(tols)
-        th, tw = tile if tile is not None else (1, 1)
+        th, tw = tile if tile is not None else (0, 0)
         self.opts = VcSweepOpts(primary, th, tw, self.k, int(self.integrity), 0)
-        self.ws_bytes = vcheck_workspace_bytes(self.cases if self.n_cases else self.cases,
-                                               self.n_tols, self.opts) if self.n_cases else 4096
+        self.ws_bytes = vcheck_workspace_bytes(self.cases, self.n_tols, self.opts) \
+            if self.n_cases else 4096
         self.ws = _ws(self.ws_bytes, dev)
         self.stats = torch.zeros(max(self.n_cases, 1) * 128, dtype=torch.uint8, device=dev)
         self.mism = torch.zeros(max(self.n_cases * self.n_tols, 1), dtype=torch.int64, device=dev)
@@ -372,11 +388,35 @@ class Sweep:
             self.tmaps.data_ptr() if self.tmaps is not None else None,
             self.fk.data_ptr() if self.fk is not None else None,
             self.integ.data_ptr() if self.integ is not None else None)
+        if mode == "prepared":
+            plan = ctypes.c_void_p()
+            with torch.cuda.device(dev):
+                _check(lib().vcheck_plan_sweep(self.cases, self.n_cases, self.tols, self.n_tols,
+                                               ctypes.byref(self.opts), ctypes.byref(self.out),
+                                               self.ws.data_ptr(), self.ws.numel(),
+                                               _stream_ptr(stream), ctypes.byref(plan)))
+            self._plan = plan
 
     def launch(self, stream=None) -> None:
-        _check(lib().vcheck_sweep(self.cases, self.n_cases, self.tols, self.n_tols,
-                                  ctypes.byref(self.opts), ctypes.byref(self.out),
-                                  self.ws.data_ptr(), self.ws.numel(), _stream_ptr(stream)))
+        if self.mode == "prepared":
+            _check(lib().vcheck_plan_launch(self._plan, _stream_ptr(stream)))
+        else:
+            _check(lib().vcheck_sweep(self.cases, self.n_cases, self.tols, self.n_tols,
+                                      ctypes.byref(self.opts), ctypes.byref(self.out),
+                                      self.ws.data_ptr(), self.ws.numel(), _stream_ptr(stream)))
+
+    def close(self) -> None:
+        """Frees the prepared plan (after the launches in flight are done)."""
+        if self._plan is not None:
+            torch.cuda.synchronize(self.device)
+            lib().vcheck_plan_free(self._plan)
+            self._plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # interpreter shutdown
+            pass
 
     def results(self) -> dict:
         torch.cuda.synchronize(self.device)
@@ -404,9 +444,9 @@ class Sweep:
 
 def vcheck_sweep(cases, tols, primary: int = 0, tile=None, k: int = 0, integrity: bool = False,
                  stream=None) -> dict:
-    """Validate a whole case matrix in one call; returns per-case results and
-    per-pair suite match rates."""
-    sw = Sweep(cases, tols, primary=primary, tile=tile, k=k, integrity=integrity)
+    """Validate a whole case matrix in one vcheck_sweep call; returns per-case
+    results and per-pair suite match rates."""
+    sw = Sweep(cases, tols, primary=primary, tile=tile, k=k, integrity=integrity, mode="oneshot")
     sw.launch(stream)
     return sw.results()
 
