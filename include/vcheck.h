@@ -58,7 +58,8 @@
  * kernel of a one-shot call copies the call's descriptor table (a buffer is
  * reused only after the event recorded behind the call that read it has
  * completed: a thread that issues more than 8 such calls ahead of the GPU
- * waits for the oldest), guarded by a mutex. A descriptor table larger
+ * waits for the oldest); and the device address of the scratch array of
+ * vcheck_sweep_noalloc. Both are guarded by a mutex. A descriptor table larger
  * than 256 KiB (about 1,300 sweep cases) is uploaded with a pageable copy,
  * which returns only once the runtime has taken the bytes (for pageable
  * memory it first waits for the stream's earlier work). Per thread: the last
@@ -93,7 +94,8 @@ typedef int32_t vc_status;
 #define VC_ERR_LIMIT (-8)     /* n_tols, n_inputs or n_cases outside its range */
 #define VC_ERR_HIP (-9)       /* HIP runtime / launch failure */
 #define VC_ERR_ALIGN (-10)    /* data pointer not aligned to its element size */
-#define VC_ERR_STATE (-11)    /* a prepared sweep is launched on another device */
+#define VC_ERR_STATE (-11)    /* vcheck_init has not run on the current device, or a
+                                 prepared sweep is launched on another device */
 
 typedef enum vc_dtype { VC_F32 = 0, VC_F16 = 1, VC_BF16 = 2 } vc_dtype;
 
@@ -293,12 +295,34 @@ vc_status vcheck_plan_launch(vc_plan *plan, void *stream);
  * the workspace and outputs must stay alive until they are done. */
 vc_status vcheck_plan_free(vc_plan *plan);
 
-/* ---- library set-up -------------------------------------------------------- */
+/* ---- library set-up and the allocation-free sweep -------------------------- */
 
-/* Set-up for the current device: allocates the pinned staging ring (once),
- * so that later calls on the device allocate nothing. Idempotent; optional
- * (the first call that needs the ring allocates it). Errors: VC_ERR_HIP. */
+/* Set-up for the current device: allocates the pinned staging ring (once)
+ * and takes the device address of vcheck_sweep_noalloc's scratch array.
+ * Idempotent; call it once per device (with that device current) before
+ * vcheck_sweep_noalloc. Errors: VC_ERR_HIP. */
 vc_status vcheck_init(void);
+
+/* Bytes of device scratch per device that vcheck_sweep_noalloc works in. */
+#define VC_NOALLOC_SCRATCH_BYTES (64ull << 20)
+
+/*
+ * vcheck_sweep_noalloc -- vcheck_sweep for callers that cannot allocate
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. Same arguments and results as vcheck_sweep except the
+ * workspace: the library's static device scratch array of
+ * VC_NOALLOC_SCRATCH_BYTES bytes on the current device. The call allocates
+ * no device or pinned memory (vcheck_init must have run on the device:
+ * VC_ERR_STATE otherwise). It rejects, before enqueueing anything, a sweep
+ * whose workspace (vcheck_workspace_bytes) exceeds VC_NOALLOC_SCRATCH_BYTES
+ * or whose case table exceeds one 256 KiB staging buffer (VC_ERR_LIMIT).
+ * Every call on a device shares that device's scratch, whose contents the
+ * next call overwrites: calls that overlap on one device (other streams,
+ * other threads) race and must be serialized by the caller.
+ */
+vc_status vcheck_sweep_noalloc(const vc_case *cases, int32_t n_cases, const vc_tol *tols,
+                               int32_t n_tols, const vc_sweep_opts *opts,
+                               const vc_sweep_out *out, void *stream);
 
 /* ---- tensor-statistics probe ---------------------------------------------
  *

@@ -361,7 +361,8 @@ vc_status hip_check(hipError_t e, const char *what) {
 // ends: a ring of kSlots pinned host buffers of kSlotBytes each, from which
 // the prologue kernel of a one-shot call copies the call's descriptor blob
 // (a slot is reused only after the event recorded behind the kernels that
-// read it has completed). A blob larger than a slot is uploaded with a
+// read it has completed), and the device address of the allocation-free
+// entry point's scratch array. A blob larger than a slot is uploaded with a
 // pageable hipMemcpyAsync instead, which returns only once the runtime has
 // taken the bytes (waiting for the stream's earlier work).
 constexpr int kSlots = 8;
@@ -376,6 +377,7 @@ struct DeviceState {
   hipEvent_t ev[kSlots] = {};
   bool pending[kSlots] = {};
   int next = 0;
+  uint8_t *scratch = nullptr;  // device address of the scratch array (vcheck_init)
 };
 DeviceState g_dev[kMaxDevices];
 
@@ -619,7 +621,8 @@ vc_status run(const Plan &plan, const vc_tol *tols, const Outputs &out, void *ws
   return st;
 }
 
-// Argument checks and plan of a sweep (vcheck_sweep, vcheck_plan_sweep).
+// Argument checks and plan of a sweep (vcheck_sweep, vcheck_sweep_noalloc,
+// vcheck_plan_sweep).
 vc_status plan_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols, int32_t n_tols,
                      const vc_sweep_opts *opts, const vc_sweep_out *out, Plan &plan,
                      Outputs &oo) {
@@ -859,6 +862,12 @@ struct vc_plan {
   int device;
 };
 
+// Scratch of the allocation-free entry point (vcheck_sweep_noalloc): the
+// workspace of its calls, one copy per device. Host code reaches it only
+// through the device address that vcheck_init takes with
+// hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[VC_NOALLOC_SCRATCH_BYTES];
+
 extern "C" {
 
 vc_status vcheck_compare(const vc_tensor *cand, const vc_tensor *ref, const vc_tol *tol,
@@ -948,7 +957,39 @@ vc_status vcheck_init(void) {
   if (st != VC_OK) return st;
   DeviceState &ds = g_dev[dev];
   std::lock_guard<std::mutex> lock(ds.mu);
-  return ensure_ring(ds);
+  st = ensure_ring(ds);
+  if (st != VC_OK) return st;
+  if (ds.scratch == nullptr) {
+    void *p = nullptr;
+    st = hip_check(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress");
+    if (st != VC_OK) return st;
+    ds.scratch = (uint8_t *)p;
+  }
+  return VC_OK;
+}
+
+vc_status vcheck_sweep_noalloc(const vc_case *cases, int32_t n_cases, const vc_tol *tols,
+                               int32_t n_tols, const vc_sweep_opts *opts,
+                               const vc_sweep_out *out, void *stream) {
+  g_last_error.clear();
+  Plan plan;
+  Outputs oo;
+  vc_status st = plan_sweep(cases, n_cases, tols, n_tols, opts, out, plan, oo);
+  if (st != VC_OK) return st;
+  if (plan.bytes > (size_t)VC_NOALLOC_SCRATCH_BYTES)
+    return fail(VC_ERR_LIMIT, "the sweep needs %zu bytes of scratch; the maximum is %zu",
+                plan.bytes, (size_t)VC_NOALLOC_SCRATCH_BYTES);
+  int dev = 0;
+  st = current_device(dev);
+  if (st != VC_OK) return st;
+  uint8_t *ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_dev[dev].mu);
+    ws = g_dev[dev].scratch;
+  }
+  if (ws == nullptr) return fail(VC_ERR_STATE, "vcheck_init has not run on device %d", dev);
+  return run(plan, tols, oo, ws, (size_t)VC_NOALLOC_SCRATCH_BYTES, (hipStream_t)stream, false,
+             false);
 }
 
 vc_status vcheck_plan_sweep(const vc_case *cases, int32_t n_cases, const vc_tol *tols,

@@ -9,7 +9,8 @@ workspace with torch, launches on the current stream, waits, and returns the
 results as Python values. ``Sweep`` prepares a sweep once
 (``vcheck_plan_sweep``: the case table stays in the workspace) and relaunches
 it without allocating or uploading anything (``vcheck_plan_launch``), for
-repeated validation of one case matrix and for timing loops.
+repeated validation of one case matrix and for timing loops;
+``vcheck_sweep_noalloc`` runs a sweep in the library's own scratch.
 
 There is no fallback: if libvcheck.so is missing or fails to load, every call
 raises.
@@ -35,6 +36,7 @@ FLAG_LOWPREC_BF16, FLAG_LOWPREC_FP16 = 8, 16
 STATUS_NAMES = {0: "VC_OK", -1: "VC_ERR_NULL", -2: "VC_ERR_DTYPE", -3: "VC_ERR_SHAPE",
                 -4: "VC_ERR_TOL", -5: "VC_ERR_TILE", -6: "VC_ERR_K", -7: "VC_ERR_WORKSPACE",
                 -8: "VC_ERR_LIMIT", -9: "VC_ERR_HIP", -10: "VC_ERR_ALIGN", -11: "VC_ERR_STATE"}
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _DTYPES = {torch.float32: VC_F32, torch.float16: VC_F16, torch.bfloat16: VC_BF16}
 
@@ -161,12 +163,15 @@ def lib() -> ctypes.CDLL:
     L.vcheck_plan_launch.argtypes = [P, P]
     L.vcheck_plan_free.argtypes = [P]
     L.vcheck_init.argtypes = []
+    L.vcheck_sweep_noalloc.argtypes = [ctypes.POINTER(VcCase), ctypes.c_int32,
+                                       ctypes.POINTER(VcTol), ctypes.c_int32,
+                                       ctypes.POINTER(VcSweepOpts), ctypes.POINTER(VcSweepOut), P]
     for name in ("vcheck_compare", "vcheck_localize", "vcheck_integrity", "vcheck_sweep",
                  "vcheck_workspace_bytes", "vcheck_tensor_stats",
                  "vcheck_tensor_stats_workspace", "vcheck_nearpass",
                  "vcheck_nearpass_workspace", "vcheck_content_hash",
                  "vcheck_content_hash_workspace", "vcheck_plan_sweep", "vcheck_plan_launch",
-                 "vcheck_plan_free", "vcheck_init"):
+                 "vcheck_plan_free", "vcheck_init", "vcheck_sweep_noalloc"):
         getattr(L, name).restype = ctypes.c_int32
     if L.vcheck_abi_version() != 1:
         raise RuntimeError("libvcheck.so ABI version mismatch")
@@ -329,14 +334,16 @@ class Sweep:
     k: first-k length or 0; integrity: run the detectors.
     mode: "prepared" (default): the sweep is prepared once
     (vcheck_plan_sweep) and each ``launch()`` runs vcheck_plan_launch;
-    "oneshot": each ``launch()`` is a full vcheck_sweep call. ``launch()``
-    enqueues on a stream without allocating; ``results()`` synchronises and returns the outputs.
+    "oneshot": each ``launch()`` is a full vcheck_sweep call; "noalloc": each
+    ``launch()`` is a vcheck_sweep_noalloc call (no workspace is allocated;
+    vcheck_init runs first). ``launch()`` enqueues on a stream without
+    allocating; ``results()`` synchronises and returns the outputs.
     """
 
     def __init__(self, cases, tols, primary: int = 0, tile=None, k: int = 0,
                  integrity: bool = False, rates: bool = True, device=None, mode="prepared",
                  stream=None):
-        if mode not in ("prepared", "oneshot"):
+        if mode not in ("prepared", "oneshot", "noalloc"):
             raise ValueError("unknown mode %r" % (mode,))
         self.mode = mode
         self._plan = None
@@ -365,9 +372,13 @@ class Sweep:
         self.tols = _tols(tols)
         th, tw = tile if tile is not None else (0, 0)
         self.opts = VcSweepOpts(primary, th, tw, self.k, int(self.integrity), 0)
-        self.ws_bytes = vcheck_workspace_bytes(self.cases, self.n_tols, self.opts) \
-            if self.n_cases else 4096
-        self.ws = _ws(self.ws_bytes, dev)
+        if mode == "noalloc":
+            self.ws_bytes = 0
+            self.ws = None
+        else:
+            self.ws_bytes = vcheck_workspace_bytes(self.cases, self.n_tols, self.opts) \
+                if self.n_cases else 4096
+            self.ws = _ws(self.ws_bytes, dev)
         self.stats = torch.zeros(max(self.n_cases, 1) * 128, dtype=torch.uint8, device=dev)
         self.mism = torch.zeros(max(self.n_cases * self.n_tols, 1), dtype=torch.int64, device=dev)
         self.pass_ = torch.zeros(max(self.n_cases * self.n_tols, 1), dtype=torch.uint8, device=dev)
@@ -396,14 +407,21 @@ class Sweep:
                                                self.ws.data_ptr(), self.ws.numel(),
                                                _stream_ptr(stream), ctypes.byref(plan)))
             self._plan = plan
+        elif mode == "noalloc":
+            with torch.cuda.device(dev):
+                _check(lib().vcheck_init())
 
     def launch(self, stream=None) -> None:
         if self.mode == "prepared":
             _check(lib().vcheck_plan_launch(self._plan, _stream_ptr(stream)))
-        else:
+        elif self.mode == "oneshot":
             _check(lib().vcheck_sweep(self.cases, self.n_cases, self.tols, self.n_tols,
                                       ctypes.byref(self.opts), ctypes.byref(self.out),
                                       self.ws.data_ptr(), self.ws.numel(), _stream_ptr(stream)))
+        else:
+            _check(lib().vcheck_sweep_noalloc(self.cases, self.n_cases, self.tols, self.n_tols,
+                                              ctypes.byref(self.opts), ctypes.byref(self.out),
+                                              _stream_ptr(stream)))
 
     def close(self) -> None:
         """Frees the prepared plan (after the launches in flight are done)."""
@@ -447,6 +465,14 @@ def vcheck_sweep(cases, tols, primary: int = 0, tile=None, k: int = 0, integrity
     """Validate a whole case matrix in one vcheck_sweep call; returns per-case
     results and per-pair suite match rates."""
     sw = Sweep(cases, tols, primary=primary, tile=tile, k=k, integrity=integrity, mode="oneshot")
+    sw.launch(stream)
+    return sw.results()
+
+
+def vcheck_sweep_noalloc(cases, tols, primary: int = 0, tile=None, k: int = 0,
+                         integrity: bool = False, stream=None) -> dict:
+    """vcheck_sweep in the library's scratch (vcheck_sweep_noalloc)."""
+    sw = Sweep(cases, tols, primary=primary, tile=tile, k=k, integrity=integrity, mode="noalloc")
     sw.launch(stream)
     return sw.results()
 
