@@ -243,32 +243,12 @@ __device__ __forceinline__ void max_merge(double &v, I &i, double ov, I oi) {
   }
 }
 
-__device__ __forceinline__ double readfirstlane_f64(double x) {
-  const uint64_t b = (uint64_t)__double_as_longlong(x);
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
 
 __device__ __forceinline__ double readlane_f64(double x, uint32_t l) {
   const uint64_t b = (uint64_t)__double_as_longlong(x);
   const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, l);
   const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), l);
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-
-// Wave-wide (largest value, smallest index) of the lanes' (v, i), returned
-// as wave-uniform values. Lanes with nothing pass v = -1 (real values are
-// >= 0) and i = kNone.
-__device__ __forceinline__ void wave_max(double &v, uint32_t &i) {
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
-    const double ov = __shfl_xor(v, m);
-    const uint32_t oi = __shfl_xor(i, m);
-    max_merge(v, i, ov, oi);
-  }
-  v = readfirstlane_f64(v);
-  i = __builtin_amdgcn_readfirstlane(i);
 }
 
 // One step of a wave maximum: v and the value CTRL moves in (DPP; lanes with
@@ -294,6 +274,50 @@ __device__ __forceinline__ double wave_max_val(double v) {
   v = dpp_max<0x142, 0xa>(v);  // row_bcast:15
   v = dpp_max<0x143, 0xc>(v);  // row_bcast:31
   return readlane_f64(v, kWaveSize - 1);
+}
+
+// One step of a wave sum: v plus the value CTRL moves in (lanes with no
+// source, or outside the rows ROWS enables, add 0).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_add(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)b, CTRL, ROWS, 0xf, false);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(b >> 32), CTRL, ROWS, 0xf, false);
+  return v + __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Wave-wide sum of v, wave-uniform, in a fixed order: row shifts by 1, 2, 4
+// and 8 leave each row's sum in its last lane, two row broadcasts add them
+// up in lane 63.
+__device__ __forceinline__ double wave_sum(double v) {
+  v = dpp_add<0x111, 0xf>(v);  // row_shr:1
+  v = dpp_add<0x112, 0xf>(v);  // row_shr:2
+  v = dpp_add<0x114, 0xf>(v);  // row_shr:4
+  v = dpp_add<0x118, 0xf>(v);  // row_shr:8
+  v = dpp_add<0x142, 0xa>(v);  // row_bcast:15
+  v = dpp_add<0x143, 0xc>(v);  // row_bcast:31
+  return readlane_f64(v, kWaveSize - 1);
+}
+
+// Wave-wide minimum of i, wave-uniform (the pattern of wave_max_val).
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t i) {
+  i = min(i, (uint32_t)__builtin_amdgcn_update_dpp(0xffffffffu, i, 0x111, 0xf, 0xf, false));
+  i = min(i, (uint32_t)__builtin_amdgcn_update_dpp(0xffffffffu, i, 0x112, 0xf, 0xf, false));
+  i = min(i, (uint32_t)__builtin_amdgcn_update_dpp(0xffffffffu, i, 0x113, 0xf, 0xf, false));
+  i = min(i, (uint32_t)__builtin_amdgcn_update_dpp(0xffffffffu, i, 0x114, 0xf, 0xf, false));
+  i = min(i, (uint32_t)__builtin_amdgcn_update_dpp(0xffffffffu, i, 0x118, 0xf, 0xf, false));
+  i = min(i, (uint32_t)__builtin_amdgcn_update_dpp(0xffffffffu, i, 0x142, 0xa, 0xf, false));
+  i = min(i, (uint32_t)__builtin_amdgcn_update_dpp(0xffffffffu, i, 0x143, 0xc, 0xf, false));
+  return __builtin_amdgcn_readlane(i, kWaveSize - 1);
+}
+
+// Wave-wide (largest value, smallest index among the lanes holding it), as
+// wave_max, through DPP: the maximum first, then the smallest index of the
+// lanes that hold it.
+__device__ __forceinline__ void wave_max_dpp(double &v, uint32_t &i) {
+  const double m = wave_max_val(v);
+  i = wave_min_u32(v == m ? i : kNone);
+  v = m;
 }
 
 // c - r of element j of a step in binary32 (one rounding); binary16 pairs go
@@ -1747,10 +1771,16 @@ void main_kernel(const Params P) {
     acc_abs += add_a;
     acc_rel += add_q;
     if (res == kLocate) {
-      // single pair: the lane's mismatch bits wait in LDS; the entry holds
-      // the offset, bit 0, the list position and the wave
-      s_pb[wave][nd][lane] = (uint8_t)pbm;
-      defer(off0 | 1u | (nd << 1) | (wave << 6));
+      if (nd == 0) {
+        // nothing of the wave is listed: its positions are recorded now, in
+        // stream order, while the loads of the next steps are in flight
+        localize(pbm, off0);
+      } else {
+        // single pair: the lane's mismatch bits wait in LDS; the entry
+        // holds the offset, bit 0, the list position and the wave
+        s_pb[wave][nd][lane] = (uint8_t)pbm;
+        defer(off0 | 1u | (nd << 1) | (wave << 6));
+      }
     } else if (res != kDone) {
       defer(off0);
     } else if (NT > 1 && prim_count() != m0 && loc_on()) {
@@ -1908,16 +1938,13 @@ void main_kernel(const Params P) {
     if constexpr (INTEG) integ_step(ct, rt, vmask, false, o0);
   }
 
-  // wave reductions (fixed butterfly order)
+  // wave reductions (fixed order)
   double lb_abs = s_bv[0][wave][lane], lb_rel = s_bv[1][wave][lane];
   uint32_t li_abs = s_bi[0][wave][lane], li_rel = s_bi[1][wave][lane];
-  wave_max(lb_abs, li_abs);
-  wave_max(lb_rel, li_rel);
-#pragma unroll
-  for (int m = kWaveSize / 2; m >= 1; m >>= 1) {
-    acc_abs += __shfl_xor(acc_abs, m);
-    acc_rel += __shfl_xor(acc_rel, m);
-  }
+  wave_max_dpp(lb_abs, li_abs);
+  wave_max_dpp(lb_rel, li_rel);
+  acc_abs = wave_sum(acc_abs);
+  acc_rel = wave_sum(acc_rel);
   if (lane == 0) {
     ChunkRec &o = s_out[wave];
 #pragma unroll
