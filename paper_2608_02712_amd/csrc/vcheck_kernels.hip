@@ -819,6 +819,11 @@ void main_kernel(const Params P) {
   // registers): nan_c, inf_c, nan_r, inf_r, n_fin, n_rel, n_rel_undef
   __shared__ uint32_t s_rare[kWavesPerBlock][8];
 
+  // The block's set-up runs at raised wave priority: it is a short serial
+  // chain that otherwise waits behind the streaming waves of the other
+  // blocks on the SIMD, keeping the block's slot from streaming; the
+  // streaming loop runs at the base priority.
+  __builtin_amdgcn_s_setprio(3);
   const uint32_t lane = threadIdx.x & (kWaveSize - 1);
   // wave index: uniform per wave (keeps every range bound in scalar registers)
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
@@ -993,6 +998,7 @@ void main_kernel(const Params P) {
     for (uint32_t e = threadIdx.x; e < wl; e += kBlockThreads) sh_st.win[e] = 0;
   }
   __syncthreads();
+  __builtin_amdgcn_s_setprio(0);
 
   // Localization of the primary-pair mismatches given by per-lane bit mask
   // pb (bit j = the element at chunk offset off0 + j): ordered first-k
