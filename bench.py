@@ -9,17 +9,24 @@ the timed interval; each step is timed with HIP events on the launch stream.
 The streaming kernels are timed in a second pass with events the library
 records around them.
 
-Headline line: the fp16 batch of 64 cases of 2048x2048 (the configuration the
-metric is quoted on). ``probe`` reports the tensor-statistics probe over the
-128 cand and ref tensors of that batch in one call, ``nearpass`` the near-pass
+Headline line: the largest single-GPU workload, the integrity batch of 256
+fp32 cases of 4096x4096 (34.4 GB of cand and ref per call). ``probe``
+reports the tensor-statistics probe over the 128 cand and ref tensors of the
+fp16 batch (64 cases of 2048x2048) in one call, ``nearpass`` the near-pass
 statistics of its 64 cases, ``content_hash`` the content hashes of its 128
-tensors. ``workloads`` holds the same figures for all five
-workloads, measured in the same run. ``roofline`` reports the main streaming
-kernel's achieved HBM bandwidth (algorithmic bytes / its event-timed average
-duration) against the 8 TB/s peak; ``cpu_baseline`` times the CPU oracle on a
-bounded sample of the headline workload on this host.
+tensors. ``workloads`` holds the same figures for all five workloads,
+measured in the same run. ``roofline`` reports the headline's streaming
+kernel: achieved HBM bandwidth (algorithmic bytes / its event-timed average
+duration) against the 8 TB/s peak, and the HBM bytes per launch from the
+committed counter readings (profiles/traffic.json) when they were taken on
+the current sources; ``cpu_baseline`` times the CPU oracle on a bounded
+sample of the headline workload on this host.
 
 Usage: python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--headline-only]
+       python bench.py --only N [--diag]    (one workload; --diag adds the probe,
+                                             near-pass and hash over it)
+       python bench.py --pmc-summary DIR... (medians of rocprofv3 --pmc output)
+       python bench.py --record-traffic ... (profiles/traffic.json entry)
 """
 import argparse
 import hashlib
@@ -33,8 +40,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "validated GB/s (ref+cand bytes) and % of HBM peak; test cases/sec"
 HBM_PEAK_GBS = 8000.0
-HEADLINE = 2
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_02712_amd", "csrc", "vcheck_kernels.hip")
+HEADLINE = 5  # the largest workload
+DIAG_WORKLOAD = 2  # the fp16 batch: probe, near-pass and hash are timed over it
+CSRC = os.path.join(ROOT, "paper_2608_02712_amd", "csrc")
+KERNEL_SRCS = [os.path.join(CSRC, n) for n in
+               ("vcheck_kernels.hip", "vcheck_probe.hip", "vcheck_api.cpp", "vcheck_internal.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -42,17 +52,23 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def kernel_hash(text=None):
-    """Hash of the kernel source with // comments and blank lines removed, so
-    that the stored counter readings stay valid across comment-only edits."""
-    if text is None:
-        with open(KERNEL_SRC) as f:
-            text = f.read()
+def kernel_hash(texts=None):
+    """Hash of the kernel sources and the planner (which sets unit sizes and
+    launch shapes) with // comments and blank lines removed, so that stored
+    counter readings stay valid across comment-only edits and lapse on any
+    code change."""
+    if texts is None:
+        texts = []
+        for path in KERNEL_SRCS:
+            with open(path) as f:
+                texts.append(f.read())
     code = []
-    for line in text.splitlines():
-        line = line.split("//", 1)[0].rstrip()
-        if line:
-            code.append(line)
+    for text in texts:
+        for line in text.splitlines():
+            line = line.split("//", 1)[0].rstrip()
+            if line:
+                code.append(line)
+        code.append("\x00")
     return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
@@ -127,6 +143,7 @@ def measure(cfg, steps, warmup, flush):
         "tols": [[float(a), float(r)] for (a, r, *_) in w.tols],
         "tile": list(w.tile) if w.tile else None,
         "k": w.k or 0,
+        "integrity": bool(w.integrity),
         "n_cases": len(w.cases),
         "elements": w.numel,
         "ref_cand_bytes": rc,
@@ -317,13 +334,45 @@ def measure_hash(w, steps, warmup, flush):
     return out
 
 
-def cpu_baseline(w, seconds):
-    """The CPU oracle on whole cases of the workload: first one thread until
-    the time budget is used (at least one case), then the same cases spread
-    over the host's cores (one case per thread at a time; the oracle is plain
-    C without shared state, and ctypes releases the interpreter lock while it
-    runs). The multi-threaded rate is the baseline; the single-thread figure
-    is reported beside it."""
+CPU_SHARE = 16  # host threads per GPU on the measurement machines
+
+
+def host_info():
+    """Core counts and CPU model of this host (read before the GPU is
+    initialised: lscpu runs as a child process)."""
+    import subprocess
+
+    model = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        for line in out.splitlines():
+            if line.strip().startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if model is None:
+        try:
+            with open("/proc/cpuinfo") as f:
+                for line in f:
+                    if line.startswith("model name"):
+                        model = line.split(":", 1)[1].strip()
+                        break
+        except OSError:
+            pass
+    return {"os_cpu_count": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
+            "model": model}
+
+
+def cpu_baseline(w, seconds, host):
+    """The CPU oracle on whole cases of the workload (with the operator inputs
+    when the workload runs the detectors): first one thread until the time
+    budget is used (at least one case), then the same cases spread over the
+    host's cores (one case per thread at a time; the oracle is plain C
+    without shared state, and ctypes releases the interpreter lock while it
+    runs). The threads are the affinity cores, at most the host's CPU share
+    of one GPU. The multi-threaded rate is the baseline; the single-thread
+    figure is reported beside it."""
     from concurrent.futures import ThreadPoolExecutor
 
     import oracle
@@ -331,42 +380,49 @@ def cpu_baseline(w, seconds):
 
     oracle.default_lib()
     dt = wl.dtype_code(w.cases[0].ref.dtype)
-    host, spent = [], 0.0
+    host_cases, spent = [], 0.0
+
+    def one(item):
+        c, r, shape, ins = item
+        oracle.validate_case(c, r, dt, shape, w.tols, primary=w.primary, tile=w.tile, k=w.k,
+                             inputs=ins)
+
     for case in w.cases:
         cand, ref = wl.raw_numpy(case.cand).reshape(-1), wl.raw_numpy(case.ref).reshape(-1)
-        host.append((cand, ref, tuple(case.ref.shape)))
+        ins = None
+        if w.integrity:
+            ins = [(wl.raw_numpy(x).reshape(-1), wl.dtype_code(x.dtype)) for x in case.inputs]
+        item = (cand, ref, tuple(case.ref.shape), ins)
+        host_cases.append(item)
         t = time.perf_counter()
-        oracle.validate_case(cand, ref, dt, tuple(case.ref.shape), w.tols, primary=w.primary,
-                             tile=w.tile, k=w.k)
+        one(item)
         spent += time.perf_counter() - t
         if spent >= seconds:
             break
-    n_bytes = sum(c.nbytes + r.nbytes for c, r, _ in host)
-    threads = max(1, min(16, len(os.sched_getaffinity(0)), len(host)))
-
-    def one(item):
-        c, r, shape = item
-        oracle.validate_case(c, r, dt, shape, w.tols, primary=w.primary, tile=w.tile, k=w.k)
-
+    n_bytes = sum(c.nbytes + r.nbytes for c, r, _, _ in host_cases)
+    threads = max(1, min(CPU_SHARE, host["affinity"], len(host_cases)))
     with ThreadPoolExecutor(max_workers=threads) as pool:
         t = time.perf_counter()
-        list(pool.map(one, host))
+        list(pool.map(one, host_cases))
         wall = time.perf_counter() - t
     log("cpu oracle: %d cases, %.2f s on one thread, %.2f s on %d threads" % (
-        len(host), spent, wall, threads))
+        len(host_cases), spent, wall, threads))
     elems = n_bytes // (2 * w.cases[0].ref.element_size())
     return {"value": round(n_bytes / wall / 1e9, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle",
-            "cases_per_s": round(len(host) / wall, 3),
+            "cases_per_s": round(len(host_cases) / wall, 3),
             "single_thread": {"value": round(n_bytes / spent / 1e9, 4), "unit": "GB/s",
-                              "cases_per_s": round(len(host) / spent, 3)},
-            "sample": "%d of %d cases (%d elements), plain C oracle, whole cases on %d threads"
-                      % (len(host), len(w.cases), elems, threads)}
+                              "cases_per_s": round(len(host_cases) / spent, 3)},
+            "host": host,
+            "sample": "%d of %d cases (%d elements%s), plain C oracle, whole cases on %d threads "
+                      "(the affinity cores, at most %d: the host CPU share of one GPU)"
+                      % (len(host_cases), len(w.cases), elems,
+                         ", with the operator inputs" if w.integrity else "", threads, CPU_SHARE)}
 
 
-def traffic_for(name, launches_bytes):
-    """HBM bytes per launch from the committed rocprofv3 counter runs, if they
-    were taken on the current kernel source."""
+def traffic_for(name):
+    """HBM bytes per launch from the committed rocprofv3 counter readings of
+    a workload's streaming kernel, if they were taken on the current sources."""
     try:
         with open(TRAFFIC_FILE) as f:
             data = json.load(f)
@@ -378,12 +434,113 @@ def traffic_for(name, launches_bytes):
     return ent.get("hbm_bytes_per_launch")
 
 
+# ---- rocprofv3 counter output --------------------------------------------------
+
+def short_kernel(name):
+    """'main_kernel<1, 1, false>' from a demangled kernel name."""
+    n = name.replace("void ", "").replace("vck::(anonymous namespace)::", "")
+    n = n.replace("vck::", "")
+    depth, out = 0, []
+    for ch in n:  # drop the parameter list, keep template arguments
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    return "".join(out).strip()
+
+
+def read_pmc(path):
+    """{kernel: {counter: [values per dispatch]}} of every
+    *counter_collection.csv under path."""
+    import csv
+    import glob
+
+    acc = {}
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    for fn in sorted(files):
+        with open(fn) as f:
+            for row in csv.DictReader(f):
+                k = short_kernel(row["Kernel_Name"])
+                acc.setdefault(k, {}).setdefault(row["Counter_Name"], []).append(
+                    float(row["Counter_Value"]))
+    return acc
+
+
+def median(v):
+    v = sorted(v)
+    n = len(v)
+    return v[n // 2] if n % 2 else 0.5 * (v[n // 2 - 1] + v[n // 2])
+
+
+def pmc_summary(dirs, match):
+    """Median of each counter per dispatch, per kernel whose name contains one
+    of `match`, over the given rocprofv3 output directories."""
+    for d in dirs:
+        acc = read_pmc(d)
+        print("== %s" % d)
+        for k in sorted(acc):
+            if not any(m in k for m in match):
+                continue
+            cs = acc[k]
+            n = max(len(v) for v in cs.values())
+            print("  %s (%d dispatches)" % (k, n))
+            for c in sorted(cs):
+                print("    %-28s %.6g" % (c, median(cs[c])))
+
+
+def record_traffic(args):
+    """Writes the profiles/traffic.json entry of a workload from four
+    FETCH_SIZE / WRITE_SIZE runs (the workload, and a plain copy of known
+    size that scales the counters)."""
+    def one(path, counter, match):
+        acc = read_pmc(path)
+        vals = [v for k, cs in acc.items() if match in k for v in cs.get(counter, [])]
+        if not vals:
+            raise SystemExit("no %s readings of a kernel matching %r under %s" % (
+                counter, match, path))
+        return median(vals), len(vals)
+
+    fk, nf = one(args.fetch, "FETCH_SIZE", args.kernel)
+    wk, nw = one(args.write, "WRITE_SIZE", args.kernel)
+    cfk, ncf = one(args.copy_fetch, "FETCH_SIZE", args.copy_kernel)
+    cwk, ncw = one(args.copy_write, "WRITE_SIZE", args.copy_kernel)
+    copy_bytes = 1 << 30
+    fs, ws = copy_bytes / (cfk * 1024), copy_bytes / (cwk * 1024)
+    hbm = int(round(fk * 1024 * fs + wk * 1024 * ws))
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        data = {}
+    data[args.workload] = {
+        "kernel": args.kernel_label,
+        "kernel_sha": kernel_hash(),
+        "fetch_kib_per_dispatch": fk, "fetch_dispatches": nf,
+        "write_kib_per_dispatch": wk, "write_dispatches": nw,
+        "copy_probe_bytes": copy_bytes, "copy_fetch_kib": cfk, "copy_write_kib": cwk,
+        "fetch_scale": round(fs, 6), "write_scale": round(ws, 6),
+        "hbm_bytes_per_launch": hbm,
+        "algorithmic_bytes_per_launch": args.alg_bytes,
+        "traffic_over_algorithmic": round(hbm / args.alg_bytes, 4),
+    }
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print("%s: FETCH_SIZE %.4f KiB (%d dispatches) x 1024 x %.6f + WRITE_SIZE %.4f KiB (%d) x "
+          "1024 x %.6f = %d bytes per launch; algorithmic %d; ratio %.4f; copy of %d bytes read "
+          "%.4f KiB fetch, %.4f KiB write; sources key %s" % (
+              args.workload, fk, nf, fs, wk, nw, ws, hbm, args.alg_bytes, hbm / args.alg_bytes,
+              copy_bytes, cfk, cwk, kernel_hash()))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--headline-only", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="only the headline workload (and the CPU baseline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -392,12 +549,38 @@ def main():
     ap.add_argument("--only", type=int, default=0,
                     help="measure only this workload (1-5) and report it as the headline; "
                          "for profiling single workloads")
+    ap.add_argument("--diag", action="store_true",
+                    help="with --only: also time the probe, near-pass and hash over it")
+    ap.add_argument("--pmc-summary", nargs="+", metavar="DIR",
+                    help="print per-kernel counter medians of rocprofv3 --pmc output and exit")
+    ap.add_argument("--match", nargs="+", default=["main_kernel", "finalize_kernel",
+                                                   "probe_kernel", "nearpass_kernel",
+                                                   "hash_kernel", "copyBuffer"])
+    ap.add_argument("--record-traffic", action="store_true",
+                    help="write a profiles/traffic.json entry from --fetch/--write/--copy-fetch/"
+                         "--copy-write rocprofv3 output directories and exit")
+    ap.add_argument("--workload")
+    ap.add_argument("--kernel", default="main_kernel")
+    ap.add_argument("--kernel-label", default="main_kernel")
+    ap.add_argument("--copy-kernel", default="copyBuffer")
+    ap.add_argument("--alg-bytes", type=int)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--copy-fetch")
+    ap.add_argument("--copy-write")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary, args.match)
+        return
+    if args.record_traffic:
+        record_traffic(args)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the validation path runs on a single MI355X "
               "(--gpus 1); runs on several GPUs are not measured.", file=sys.stderr)
         sys.exit(2)
+    host = None if args.no_cpu else host_info()
 
     import torch
 
@@ -415,23 +598,30 @@ def main():
     first = args.only or HEADLINE
     w, head = measure(first, args.steps, args.warmup, flush)
     results[first] = head
-    cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds)
+    cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds, host)
     probe = nearpass = chash = None
-    if not args.only:
+    if args.only and args.diag:
         probe = measure_probe(w, args.steps, args.warmup, flush)
         nearpass = measure_nearpass(w, args.steps, args.warmup, flush)
         chash = measure_hash(w, args.steps, args.warmup, flush)
     del w
     torch.cuda.empty_cache()
-    if not args.headline_only and not args.only:
-        for cfg in (1, 3, 4, 5):
+    if not args.only and not args.headline_only:
+        wd, r = measure(DIAG_WORKLOAD, args.steps, args.warmup, flush)
+        results[DIAG_WORKLOAD] = r
+        probe = measure_probe(wd, args.steps, args.warmup, flush)
+        nearpass = measure_nearpass(wd, args.steps, args.warmup, flush)
+        chash = measure_hash(wd, args.steps, args.warmup, flush)
+        del wd
+        torch.cuda.empty_cache()
+        for cfg in (1, 3, 4):
             wk, r = measure(cfg, args.steps, args.warmup, flush)
             results[cfg] = r
             del wk
             torch.cuda.empty_cache()
 
     achieved = head["main_kernel_gbps"]
-    traffic = traffic_for(head["workload"], head["main_kernel_alg_bytes"])
+    traffic = traffic_for(head["workload"])
     line = {
         "metric": METRIC,
         "value": head["gbps"],
@@ -452,8 +642,9 @@ def main():
                    "ref_cand_bytes": head["ref_cand_bytes"], "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "main_kernel (%s, %d tolerance pair%s)" % (
-                         head["storage"], len(head["tols"]), "" if len(head["tols"]) == 1 else "s"),
+                     "kernel": "main_kernel (%s, %d tolerance pair%s%s)" % (
+                         head["storage"], len(head["tols"]), "" if len(head["tols"]) == 1 else "s",
+                         ", detectors" if head.get("integrity") else ""),
                      "alg_bytes_per_launch": head["main_kernel_alg_bytes"],
                      "avg_launch_ms": head["main_kernel_ms"]},
         "cpu_baseline": cpu,
