@@ -106,6 +106,51 @@ __device__ __forceinline__ uint32_t find_first(const uint64_t *first, uint32_t n
   return lo + (uint32_t)__popcll(__ballot(le)) - 1u;
 }
 
+// Wave-wide minimum (MAX = false) or maximum of v, wave-uniform: row shifts
+// by 1, 2, 3, 4 and 8 (DPP) leave each row's extreme in its last lane, two
+// row broadcasts carry the rows' extremes to lane 63. Lanes with no source
+// see the identity (+inf / -inf).
+template <int CTRL, int ROWS, bool MAX>
+__device__ __forceinline__ float dpp_ext(float v) {
+  const uint32_t o = __builtin_amdgcn_update_dpp(MAX ? 0xff800000u : 0x7f800000u,
+                                                 __float_as_uint(v), CTRL, ROWS, 0xf, false);
+  return MAX ? __builtin_fmaxf(v, __uint_as_float(o)) : __builtin_fminf(v, __uint_as_float(o));
+}
+template <bool MAX>
+__device__ __forceinline__ float wave_ext(float v) {
+  v = dpp_ext<0x111, 0xf, MAX>(v);  // row_shr:1
+  v = dpp_ext<0x112, 0xf, MAX>(v);  // row_shr:2
+  v = dpp_ext<0x113, 0xf, MAX>(v);  // row_shr:3
+  v = dpp_ext<0x114, 0xf, MAX>(v);  // row_shr:4
+  v = dpp_ext<0x118, 0xf, MAX>(v);  // row_shr:8
+  v = dpp_ext<0x142, 0xa, MAX>(v);  // row_bcast:15
+  v = dpp_ext<0x143, 0xc, MAX>(v);  // row_bcast:31
+  return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(v), 63));
+}
+
+// Wave-wide maximum of v (values -1 or >= 0), wave-uniform, the same way.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_max_d(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)b, CTRL, ROWS, 0xf, false);
+  const uint32_t hi =
+      __builtin_amdgcn_update_dpp(0xbff00000u, (uint32_t)(b >> 32), CTRL, ROWS, 0xf, false);
+  return __builtin_fmax(v, __longlong_as_double((long long)(((uint64_t)hi << 32) | lo)));
+}
+__device__ __forceinline__ double wave_max_d(double v) {
+  v = dpp_max_d<0x111, 0xf>(v);
+  v = dpp_max_d<0x112, 0xf>(v);
+  v = dpp_max_d<0x113, 0xf>(v);
+  v = dpp_max_d<0x114, 0xf>(v);
+  v = dpp_max_d<0x118, 0xf>(v);
+  v = dpp_max_d<0x142, 0xa>(v);
+  v = dpp_max_d<0x143, 0xc>(v);
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, 63);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), 63);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 // (value, index) of the smaller / larger of two candidates; equal values
 // keep the smaller index; index -1 marks no candidate.
 __device__ __forceinline__ void pick_min(double &v, int64_t &i, double v2, int64_t i2) {
@@ -210,24 +255,62 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
       for (int w = 0; w < 4; ++w) nf |= (q[w] & kMag) + kCarry;
       if (__ballot((nf & kTop) != 0) == 0) {
         float x[V];
-        float smn = __builtin_inff(), smx = -__builtin_inff();
+        float smn, smx;
 #pragma unroll
-        for (int j = 0; j < V; ++j) {
-          x[j] = pdec<DT>(q, j);
-          smn = __builtin_fminf(smn, x[j]);
-          smx = __builtin_fmaxf(smx, x[j]);
-        }
+        for (int j = 0; j < V; ++j) x[j] = pdec<DT>(q, j);
         n_fin += V;
+        if constexpr (DT == VC_F16) {
+          // Binary16: the extremes are screened on the packed halves, and
+          // the step's sums are formed in binary32 before one binary64
+          // addition per sum. A product of two binary16 values is exact in
+          // binary32 and every partial sum stays inside its range, so a
+          // step's sum of 8 terms errs by at most 7 * 2^-24 of the sum of
+          // the terms' magnitudes. Bins: binary16 exponents (subnormals
+          // included, through the exact binary32 value) lie inside the
+          // histogram's range, so no clamping.
+          typedef _Float16 ph2 __attribute__((ext_vector_type(2)));
+          // (each word is copied to a scalar before the cast: a cast of the
+          // vector element itself reads the vector's first word)
+          const uint32_t w0 = q[0];
+          ph2 lo = __builtin_bit_cast(ph2, w0), hi = lo;
 #pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const double xd = (double)x[j];
-          sm += xd;
-          sq = __builtin_fma(xd, xd, sq);
-          sa += __builtin_fabs(xd);
-          const int e = (int)((__float_as_uint(x[j]) >> 23) & 0xffu);
-          const int bin =
-              x[j] == 0.0f ? kHistBins : min(max(e - 127 - kHistEmin + 1, 0), kHistBins - 1);
-          atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+          for (int w = 1; w < 4; ++w) {
+            const uint32_t wv = q[w];
+            const ph2 h = __builtin_bit_cast(ph2, wv);
+            lo = __builtin_elementwise_min(lo, h);
+            hi = __builtin_elementwise_max(hi, h);
+          }
+          smn = __builtin_fminf((float)lo[0], (float)lo[1]);
+          smx = __builtin_fmaxf((float)hi[0], (float)hi[1]);
+          float f1 = 0.0f, f2 = 0.0f, f3 = 0.0f;
+#pragma unroll
+          for (int j = 0; j < V; ++j) {
+            f1 += x[j];
+            f2 = __builtin_fmaf(x[j], x[j], f2);
+            f3 += __builtin_fabsf(x[j]);
+            const int e = (int)((__float_as_uint(x[j]) >> 23) & 0xffu);
+            const int bin = x[j] == 0.0f ? kHistBins : e - 127 - kHistEmin + 1;
+            atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+          }
+          sm += (double)f1;
+          sq += (double)f2;
+          sa += (double)f3;
+        } else {
+          smn = __builtin_inff();
+          smx = -__builtin_inff();
+#pragma unroll
+          for (int j = 0; j < V; ++j) {
+            smn = __builtin_fminf(smn, x[j]);
+            smx = __builtin_fmaxf(smx, x[j]);
+            const double xd = (double)x[j];
+            sm += xd;
+            sq = __builtin_fma(xd, xd, sq);
+            sa += __builtin_fabs(xd);
+            const int e = (int)((__float_as_uint(x[j]) >> 23) & 0xffu);
+            const int bin =
+                x[j] == 0.0f ? kHistBins : min(max(e - 127 - kHistEmin + 1, 0), kHistBins - 1);
+            atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+          }
         }
         if (__ballot(smn < wmn || smx > wmx) != 0) {
           // every element is finite: the first one beats the lane's +inf /
@@ -240,14 +323,8 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
             mx = hi ? x[j] : mx;
             imx = hi ? o0 + (uint32_t)j : imx;
           }
-          float a = mn, z = mx;
-#pragma unroll
-          for (int m = 32; m >= 1; m >>= 1) {
-            a = __builtin_fminf(a, __shfl_xor(a, m));
-            z = __builtin_fmaxf(z, __shfl_xor(z, m));
-          }
-          wmn = a;
-          wmx = z;
+          wmn = wave_ext<false>(mn);
+          wmx = wave_ext<true>(mx);
         }
         continue;
       }
@@ -285,14 +362,8 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
     }
     // raise the wave's extremes to the lanes' (lanes with no finite element
     // hold +inf / -inf)
-    float a = mn, z = mx;
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      a = __builtin_fminf(a, __shfl_xor(a, m));
-      z = __builtin_fmaxf(z, __shfl_xor(z, m));
-    }
-    wmn = a;
-    wmx = z;
+    wmn = wave_ext<false>(mn);
+    wmx = wave_ext<true>(mx);
   }
   n_zero += row[kRowWords - 1] & 0xffu;  // zeros of the usual steps
   // histogram: thread t sums bin t % 64 over the rows of lanes
@@ -634,10 +705,7 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
       if (fail) mu = max(mu, inside ? dist : 0xffffffffu);
     }
     if (__ballot(cand_any) != 0) {  // raise the wave threshold
-      double v = li == 0xffffffffu ? -1.0 : lb;
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) v = max(v, __shfl_xor(v, m));
-      T = v;
+      T = wave_max_d(li == 0xffffffffu ? -1.0 : lb);
     }
   }
   // histograms: thread t sums bin t % 64 (52 used) over the rows of lanes

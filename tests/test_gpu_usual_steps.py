@@ -2,8 +2,9 @@
 branch-free usual-step paths: long runs of finite, tame steps, with the
 events that must leave those paths planted late in a wave's range.
 
-Probe: a strict new minimum and maximum after many usual steps, ties of
-both extremes after them (the first index must win), zeros of both signs
+Probe: a strict new minimum and maximum after many usual steps (each in a
+later element of its step), ties of both extremes after them (the first
+index must win), zeros of both signs
 throughout (counted on the usual path in a spare histogram byte), binary16
 subnormals and one late NaN.
 
@@ -48,9 +49,11 @@ def _probe_data(rng):
     zeros = rng.choice(N, N // 10, replace=False)
     x[zeros] = np.where(rng.random(zeros.size) < 0.5, -0.0, 0.0).astype(np.float32)
     x[rng.choice(N, 500, replace=False)] = 3e-7  # binary16 subnormal
-    # late strict extremes, then exact ties of both
-    x[700_001], x[700_003] = -5.0, 6.0
-    x[900_000], x[1_000_000] = -5.0, 6.0
+    # late strict extremes, then exact ties of both; each in a step of its
+    # own, at an element other than the step's first two (so a screen that
+    # looked at only part of the step would miss it)
+    x[700_005], x[700_014] = -5.0, 6.0
+    x[900_003], x[1_000_007] = -5.0, 6.0
     x[N - 3] = np.nan
     return x
 
@@ -71,7 +74,7 @@ def test_probe_usual_steps_parity():
             assert np.float64(got[k]).tobytes() == np.float64(want[k]).tobytes(), (dt, k)
         for k in ("sum", "sum_sq", "sum_abs"):
             assert abs(got[k] - want[k]) <= 1e-6 * max(want["sum_abs"], want["sum_sq"]), (dt, k)
-        assert (got["argmin"], got["argmax"]) == (700_001, 700_003)
+        assert (got["argmin"], got["argmax"]) == (700_005, 700_014)
         assert got["zero"] > N // 20  # most planted zeros survive the later plants
 
 
