@@ -588,6 +588,14 @@ __device__ void np_reduce(NpLds &s, NpRec &r) {
   }
 }
 
+// Largest binary32 value <= x, for x >= 0 (FLT_MAX beyond the range).
+__device__ __forceinline__ float np_f32_below(double x) {
+  if (x >= 3.4028234663852886e38) return 3.40282347e38f;
+  float f = (float)x;
+  if ((double)f > x) f = __uint_as_float(__float_as_uint(f) - 1u);
+  return f;
+}
+
 // Grid pattern of element j: binary16 rounding of a binary32 value, the
 // stored pattern for 16-bit storage.
 template <int DT>
@@ -616,6 +624,19 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
   const bool vec = ((uintptr_t)C.cand % 16) == 0 && ((uintptr_t)C.ref % 16) == 0;
   uint32_t n_pairs = 0, n_fail = 0, n_zt = 0, mu = 0;
   double lb = -1.0, T = -1.0;  // lane best ratio, wave threshold (-1: none)
+  // Binary32 screen of the usual step. alo, rlo: the pair lowered by 2^-20
+  // and rounded down, so fma(|r|, rlo, alo) <= atol + rtol |r| = t despite
+  // its rounding; tm = min(1, T lowered by 2^-20 and rounded down), so the
+  // rounded product tm * that <= min(1, T) * t. |c - r| in binary32 is
+  // within a relative 2^-23 of the exact difference (exact for 16-bit
+  // storage unless the exponents lie far apart; gradual underflow keeps a
+  // subnormal difference of binary32 values exact or within that bound), so
+  // |c - r|32 * (1 + 2^-21) <= tm * fma(|r|, rlo, alo) proves d <= t and
+  // d <= T t: the pair neither fails nor beats the largest ratio.
+  const float alo = np_f32_below(atol - atol * 0x1p-20);
+  const float rlo = np_f32_below(rtol - rtol * 0x1p-20);
+  constexpr float kDUp = 1.0f + 0x1p-21f;
+  float tm = 0.0f;
   uint32_t li = 0xffffffffu;
   for (uint64_t b = w0; b < w1; b += ITER) {
     const uint64_t i0 = b + (uint64_t)lane * V;
@@ -642,10 +663,11 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
         bool other = (nf & kTop) != 0;
 #pragma unroll
         for (int j = 0; j < V; ++j) {
-          const double r = (double)pdec<DT>(rq, j);
-          const double d = __builtin_fabs((double)pdec<DT>(cq, j) - r);
-          const double tt = atol + rtol * __builtin_fabs(r);
-          other |= d > tt || __builtin_fma(-T, tt, d) > 0.0;
+          const float rf = pdec<DT>(rq, j);
+          const float d = __builtin_fabsf(pdec<DT>(cq, j) - rf);
+          const float tl = __builtin_fmaf(__builtin_fabsf(rf), rlo, alo);
+          // (not <= catches NaN, from an infinite tl times tm = 0)
+          other |= !(__builtin_fmaf(d, kDUp, -(tm * tl)) <= 0.0f);
         }
         if (__ballot(other) == 0) {
           n_pairs += V;
@@ -706,6 +728,7 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
     }
     if (__ballot(cand_any) != 0) {  // raise the wave threshold
       T = wave_max_d(li == 0xffffffffu ? -1.0 : lb);
+      tm = T >= 1.0 ? 1.0f : np_f32_below(T - T * 0x1p-20);
     }
   }
   // histograms: thread t sums bin t % 64 (52 used) over the rows of lanes

@@ -117,3 +117,42 @@ def test_nearpass_usual_steps_parity(atol, rtol):
             assert got[k] == want[k], (dt, k, got[k], want[k])
         assert np.float64(got["max_ratio"]).tobytes() == np.float64(want["max_ratio"]).tobytes()
         assert got["n_fail"] > 0 and got["argmax_ratio"] >= 0
+
+
+@pytest.mark.parametrize("atol,rtol", [(1e-3, 1e-3), (1e-2, 0.0), (0.0, 1e-2)])
+def test_nearpass_usual_steps_tolerance_boundary(atol, rtol):
+    """Pairs whose difference lies within a few binary32 rounding steps of
+    the tolerance (both sides), planted late among well-inside pairs, so the
+    usual-step screen meets them once a largest ratio exists: a screen that
+    let one of them through would lose a failure, a ratio bin or the largest
+    ratio. The oracle decides each pair exactly."""
+    import torch
+
+    rng = np.random.default_rng(2608_73)
+    r = (rng.uniform(0.5, 2.0, N) * np.where(rng.random(N) < 0.5, -1, 1)).astype(np.float32)
+    c = (r * (1 + 1e-5 * rng.standard_normal(N))).astype(np.float32)
+    # a early failure sets a largest ratio above 1, then one below 1 is
+    # planted first in a second case (below)
+    pos = rng.choice(np.arange(N // 2, N), 4000, replace=False)
+    rel = np.array([-2.0 ** -18, -2.0 ** -21, -2.0 ** -23, -2.0 ** -24, 0.0, 2.0 ** -24,
+                    2.0 ** -23, 2.0 ** -21, 2.0 ** -18])
+    r64 = r[pos].astype(np.float64)
+    t64 = atol + rtol * np.abs(r64)
+    d64 = t64 * (1.0 + rel[rng.integers(0, rel.size, pos.size)])
+    c[pos] = (r64 + np.where(rng.random(pos.size) < 0.5, -1.0, 1.0) * d64).astype(np.float32)
+    c_hi = c.copy()
+    c_hi[1000] = r[1000] + np.float32(4.0) * np.float32(atol + rtol * abs(float(r[1000])) + 1e-3)
+    cases = [(_store(c_hi, dt), _store(r, dt), dt) for dt in DTYPES]
+    cases.append((_store(c, oracle.F32), _store(r, oracle.F32), oracle.F32))
+    res = vc.vcheck_nearpass([(_tensor(torch, cr, dt), _tensor(torch, rr, dt))
+                              for cr, rr, dt in cases], atol, rtol)
+    for i, ((cr, rr, dt), got) in enumerate(zip(cases, res)):
+        want = oracle.nearpass(_view(cr, dt), _view(rr, dt), dt, atol, rtol)
+        for k in ("numel", "n_pairs", "n_fail", "n_zero_tol", "argmax_ratio", "max_ulp_fail",
+                  "ratio_hist", "ulp_hist"):
+            assert got[k] == want[k], (i, dt, k, got[k], want[k])
+        assert np.float64(got["max_ratio"]).tobytes() == np.float64(want["max_ratio"]).tobytes()
+    # the binary32 case without the early failure: its largest ratio is one
+    # of the planted boundary pairs, and some of them fail
+    last = res[-1]
+    assert last["n_fail"] > 0 and last["argmax_ratio"] in set(pos.tolist())
