@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import ctypes
 import hashlib
+import hmac
 import json
 import os
 
@@ -510,10 +511,11 @@ class TensorStats:
         for i in range(len(self.tensors)):
             d = {k: arr[k][i].item() for k in TSTATS_DTYPE.names if k != "hist"}
             d["hist"] = [int(v) for v in arr["hist"][i]]
-            # derived: mean, population standard deviation, mean magnitude
+            # derived: mean and mean magnitude. (No spread statistic: the
+            # one the sums give, sum_sq / n - mean^2, cancels catastrophically
+            # when |mean| is large against the spread.)
             nf = d["n_finite"]
             d["mean"] = d["sum"] / nf if nf else 0.0
-            d["std"] = (max(d["sum_sq"] / nf - d["mean"] ** 2, 0.0) ** 0.5) if nf else 0.0
             d["abs_mean"] = d["sum_abs"] / nf if nf else 0.0
             res.append(d)
         return res
@@ -522,7 +524,7 @@ class TensorStats:
 def vcheck_tensor_stats(tensors, stream=None) -> list[dict]:
     """Tensor-statistics probe of a batch of device tensors (one pass); one
     dict per tensor: counts, min/max with first index, binary64 sums, the
-    binary-exponent histogram and the derived mean / std / abs_mean."""
+    binary-exponent histogram and the derived mean / abs_mean."""
     ts = TensorStats(tensors)
     if ts.tensors:
         ts.launch(stream)
@@ -614,13 +616,20 @@ def vcheck_content_hash(tensors, stream=None) -> list[int]:
     return h.results()
 
 
-def _evidence_digest(record: dict) -> str:
+# The engine's signing key for evidence records: drawn once per process, so
+# only this engine can produce a record that verifies (callers that keep
+# records across processes pass their own key to escalate / verify_evidence).
+_EVIDENCE_KEY = os.urandom(32)
+
+
+def _evidence_mac(record: dict, key: bytes | None = None) -> str:
     body = json.dumps(record, sort_keys=True, separators=(",", ":")).encode()
-    return hashlib.sha256(body).hexdigest()
+    return hmac.new(key if key is not None else _EVIDENCE_KEY, body, hashlib.sha256).hexdigest()
 
 
 def escalate(compact, extended, tols, primary: int = 0, gate: float = 1.0, tile=None,
-             k: int = 0, integrity: bool = False, evidence_path: str | None = None) -> dict:
+             k: int = 0, integrity: bool = True, evidence_path: str | None = None,
+             key: bytes | None = None) -> dict:
     """Two-stage validation with full-coverage evidence (Sec. 4.3, the
     validation-escalation panel of the mechanisms figure; Sec. S2.2).
 
@@ -628,11 +637,14 @@ def escalate(compact, extended, tols, primary: int = 0, gate: float = 1.0, tile=
     the primary pair reaches `gate` does the extended set (the full coverage:
     every shape and dtype) run, as one vcheck_sweep. Acceptance requires the
     extended set to certify every case (numerically passing at the primary
-    pair, no detector flag). The evidence record holds, per stage and case,
-    the pass bits, mismatch counts, detector flags and the content hashes of
-    cand and ref, the stage's match rates and a hash of its case set; the
-    record's own SHA-256 digest makes later edits detectable. Written as JSON
-    to `evidence_path` when given.
+    pair, no detector flag) with the detectors run (`integrity`, on by
+    default). The evidence record holds, per stage and case, the pass bits,
+    mismatch counts, detector flags, shape, storage type and the content
+    hashes of cand and ref, the stage's match rates, whether the detectors
+    ran, and a hash of its case set. The record is signed with an HMAC-SHA256
+    under the engine's key (`key`, else a per-process secret): an edited
+    record, or one re-signed without the key, fails verify_evidence. Written
+    as JSON to `evidence_path` when given.
 
     compact / extended: lists of (cand, ref) or (cand, ref, inputs)."""
 
@@ -643,17 +655,22 @@ def escalate(compact, extended, tols, primary: int = 0, gate: float = 1.0, tile=
         rows = []
         for i in range(len(cases)):
             flags = res["integrity"][i]["flags"] if res.get("integrity") else 0
+            ref = cases[i][1]
             rows.append({
                 "pass": [int(x) for x in res["pass"][i]],
                 "mismatches": [int(x) for x in res["mismatches"][i]],
                 "flags": int(flags),
+                "shape": [int(x) for x in ref.shape],
+                "dtype": str(ref.dtype).replace("torch.", ""),
                 "cand_hash": "%016x" % hashes[2 * i],
                 "ref_hash": "%016x" % hashes[2 * i + 1],
             })
         set_digest = hashlib.sha256("".join(
-            r["cand_hash"] + r["ref_hash"] for r in rows).encode()).hexdigest()
+            "%s%s%s%s" % (r["cand_hash"], r["ref_hash"], r["dtype"], r["shape"])
+            for r in rows).encode()).hexdigest()
         return {"n_cases": len(cases), "match_rate": [float(x) for x in res["match_rate"]],
                 "numeric_rate": [float(x) for x in res["numeric_rate"]],
+                "detectors_ran": bool(integrity),
                 "case_set_hash": set_digest, "cases": rows}
 
     record = {"tols": [list(map(float, t[:2])) for t in tols], "primary": primary,
@@ -662,18 +679,20 @@ def escalate(compact, extended, tols, primary: int = 0, gate: float = 1.0, tile=
         record["extended"] = stage(extended)
     ext = record["extended"]
     record["accepted"] = bool(ext is not None and ext["n_cases"] > 0 and
-                              ext["match_rate"][primary] == 1.0)
-    record["digest"] = _evidence_digest(record)
+                              ext["detectors_ran"] and ext["match_rate"][primary] == 1.0)
+    record["mac"] = _evidence_mac(record, key)
     if evidence_path is not None:
         with open(evidence_path, "w") as f:
             json.dump(record, f, indent=1, sort_keys=True)
     return record
 
 
-def verify_evidence(record: dict) -> bool:
-    """Whether an evidence record still matches its own digest."""
-    body = {k: v for k, v in record.items() if k != "digest"}
-    return _evidence_digest(body) == record.get("digest")
+def verify_evidence(record: dict, key: bytes | None = None) -> bool:
+    """Whether an evidence record carries a valid signature under the
+    engine's key (`key`, else this process's secret)."""
+    body = {k: v for k, v in record.items() if k != "mac"}
+    mac = record.get("mac")
+    return isinstance(mac, str) and hmac.compare_digest(_evidence_mac(body, key), mac)
 
 
 class BestCandidate:
@@ -713,11 +732,12 @@ class BestCandidate:
         self.history.append((name, score, decision))
         return decision
 
-    def record_evidence(self, name, record: dict) -> str:
+    def record_evidence(self, name, record: dict, key: bytes | None = None) -> str:
         """record() with the score of an escalate() evidence record: the
         extended set's certified match rate at the primary pair, or 0 when
-        the compact set stopped the escalation or the record was edited."""
-        if not verify_evidence(record) or record.get("extended") is None:
+        the compact set stopped the escalation or the record does not verify
+        (edited, or signed without the engine's key)."""
+        if not verify_evidence(record, key) or record.get("extended") is None:
             return self.record(name, 0.0)
         return self.record(name, record["extended"]["match_rate"][record["primary"]])
 
