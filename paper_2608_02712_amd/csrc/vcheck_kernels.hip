@@ -1499,7 +1499,7 @@ void main_kernel(const Params P) {
       // quotient 0) some d > 0: decided per element
       bool exq = true;
       if (em >= th.s_rel) {
-#pragma unroll 1
+#pragma unroll ES == 4 ? V : 1
         for (int j = 0; j < V; ++j) {
           const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
           const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
@@ -1518,7 +1518,10 @@ void main_kernel(const Params P) {
       // bounds
       uint32_t fcnt = 0, bits = 0;
       uint64_t amb = 0;
-#pragma unroll 1
+      // (binary32 storage unrolls the element loops of this path: its
+      // element index then needs no selects; 16-bit storage keeps them rolled
+      // for its register budget)
+#pragma unroll ES == 4 ? V : 1
       for (int j = 0; j < V; ++j) {
         const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
         const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
@@ -1556,7 +1559,7 @@ void main_kernel(const Params P) {
     for (int p = 0; p < NT; ++p) fcnt[p] = 0;
     uint64_t absm = 0, relm = 0;
     uint32_t bits = 0;
-#pragma unroll 1
+#pragma unroll ES == 4 ? V : 1
     for (int j = 0; j < V; ++j) {
       const double c = dec64<DT>(elem<DT>(cq, j));
       const double r = dec64<DT>(elem<DT>(rq, j));
