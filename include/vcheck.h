@@ -141,7 +141,7 @@ typedef struct vc_stats {
   int64_t argmax_abs;   /* flat index, -1 when n_finite == 0 */
   double max_rel;       /* exact (correctly rounded quotient) */
   int64_t argmax_rel;   /* -1 when n_rel == 0 */
-  double sum_abs;       /* sum of d_i, binary64 (order-dependent, ~1e-12 rel) */
+  double sum_abs;       /* sum of d_i, binary64 accumulation, within 1e-6 relative */
   double sum_rel;       /* sum of q_i, binary64, within 1e-6 relative */
   int32_t case_status;  /* 0, or a negative vc_status for a case that could not run */
   int32_t pass;         /* 1 iff case_status == 0 and mismatches == 0 */
