@@ -909,6 +909,16 @@ void main_kernel(const Params P) {
     uint32_t rel_zero;
   };
   __shared__ WaveThr s_thr[kWavesPerBlock];
+  // The quotient screen of every wave uses the largest quotient any wave of
+  // the block has found so far: it is a value reached by some element, and
+  // the screen (lowered by 2^-20) passes every quotient at or above it, ties
+  // included, so it only drops elements that cannot hold the maximum. Kept
+  // as the bits of the lowered binary32 bound b_rel (> 0; 0: none), raised by
+  // an LDS atomic maximum. The exact tests and the zero-quotient screen stay
+  // with the wave's own best: they skip ties, which only stream order within
+  // the wave justifies.
+  __shared__ uint32_t s_blk_rel;
+  if (threadIdx.x == 0) s_blk_rel = 0u;
   {
     WaveThr t;
     t.T_abs = t.T_rel = -1.0;
@@ -1078,6 +1088,9 @@ void main_kernel(const Params P) {
       s_thr[wave].rel_zero = zero ? 1u : 0u;
       s_thr[wave].b_mul = zero ? 0.0f : (DT != VC_F16 ? __builtin_fminf(b, QT) : b);
       s_thr[wave].s_rel = zero ? 0x1p-149f : 0.0f;
+      if (lane == 0 && b > 0.0f)
+        __hip_atomic_fetch_max(&s_blk_rel, __float_as_uint(b), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_WORKGROUP);
     }
   };
   // Tier-1 update of the lane bests for the lanes in absm | relm, given each
@@ -1761,7 +1774,16 @@ void main_kernel(const Params P) {
     const uint32_t m0 = prim_count();
     const bool tried = t1ok && t1_hold == 0;
     uint32_t pbm = 0;
-    const WaveThr th = s_thr[wave];
+    WaveThr th = s_thr[wave];
+    {
+      const float bb = __uint_as_float(s_blk_rel);
+      if (bb > 0.0f && bb > th.b_rel) {
+        th.b_rel = bb;
+        th.b_mul = DT != VC_F16 ? __builtin_fminf(bb, QT) : bb;
+        th.s_rel = 0.0f;
+        th.rel_zero = 0u;
+      }
+    }
     // the step's contributions to the binary64 sums (one update below)
     double add_a = 0.0, add_q = 0.0;
     int res = kNotTaken;
