@@ -775,9 +775,11 @@ __device__ __forceinline__ uint64_t find_entry(const uint64_t *first, uint64_t l
 
 // The register budget of 72 VGPRs (seven waves per SIMD) steers the
 // scheduler toward that occupancy; a variant that needs more registers still
-// gets them (none spills).
+// gets them (none spills). Binary32 storage with up to four pairs must keep
+// six waves per SIMD (80 VGPRs), which it does without spilling.
 template <int DT, int NT, bool INTEG>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_num_vgpr(72)))
+__global__ __launch_bounds__(kBlockThreads)
+__attribute__((amdgpu_num_vgpr(72), amdgpu_waves_per_eu(DT == VC_F32 && NT <= 4 ? 6 : 1)))
 void main_kernel(const Params P) {
   constexpr int V = Tr<DT>::V;
   constexpr int ES = Tr<DT>::ES;
@@ -1133,20 +1135,30 @@ void main_kernel(const Params P) {
     if (relm != 0) raise_rel(relm);
   };
 
-  // Single-pair variant of t1_update: the lanes in relm have a quotient pair
-  // sum at or above the screen threshold, so each computes its elements'
-  // quotient estimates first (largest mq), then proceeds as t1_update.
+  // Single-pair variant of t1_update (every |c - r| of the step exact in
+  // binary32, every r finite and non-zero), with its element loops unrolled
+  // and free of branches. A lane in absm whose md beats its best records the
+  // first element holding md. A lane in relm forms its elements' quotient
+  // estimates (largest mq, within 2^-21 of the quotients), then takes as
+  // candidates the elements with |d| - b |r| >= 0 for b = mq (1 - 2^-19) (an
+  // exact sign): they include every element that can hold the largest
+  // quotient, and any other element's quotient lies more than 2^-20 below it,
+  // so it cannot tie after rounding. A lane with one candidate (the rule)
+  // divides it once in binary64; a lane with several evaluates them in
+  // order, exactly.
   auto t1_update1 = [&](const u32x4 &cq, const u32x4 &rq, uint64_t absm, uint64_t relm,
                         uint32_t off0, float md) __attribute__((always_inline)) {
     if (((absm >> lane) & 1ull) && (double)md > s_bv[0][wave][lane]) {
       uint32_t jb = 0;
-#pragma unroll 1
+#pragma unroll
       for (int j = V - 1; j >= 0; --j)
-        if (__builtin_fabsf(diff32<DT>(cq, rq, j)) == md) jb = (uint32_t)j;
+        jb = __builtin_fabsf(diff32<DT>(cq, rq, j)) == md ? (uint32_t)j : jb;
       s_bv[0][wave][lane] = md;
       s_bi[0][wave][lane] = off0 + jb;
     }
-    if ((relm >> lane) & 1ull) {
+    if (DT == VC_BF16 && ((relm >> lane) & 1ull)) {
+      // (bfloat16: the unrolled form below costs registers, and with them
+      // resident waves; the rolled form tests every element in the band)
       double lb_rel = s_bv[1][wave][lane];
       uint32_t li_rel = s_bi[1][wave][lane];
       float mq = 0.0f;
@@ -1156,12 +1168,12 @@ void main_kernel(const Params P) {
         const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
         mq = __builtin_fmaxf(mq, d * __builtin_amdgcn_rcpf(a));
       }
-      const float band = mq * (1.0f - 0x1p-19f);
+      const float nb = -(mq * (1.0f - 0x1p-19f));
 #pragma unroll 1
       for (int j = 0; j < V; ++j) {
         const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
         const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
-        if (d * __builtin_amdgcn_rcpf(a) >= band) {
+        if (__builtin_fmaf(nb, a, d) >= 0.0f) {
           const double q = (double)d / (double)a;
           if (q > lb_rel) {
             lb_rel = q;
@@ -1171,6 +1183,56 @@ void main_kernel(const Params P) {
       }
       s_bv[1][wave][lane] = lb_rel;
       s_bi[1][wave][lane] = li_rel;
+    }
+    if (DT != VC_BF16 && relm != 0) {
+      const bool mine = (relm >> lane) & 1ull;
+      float mq = 0.0f;
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+        const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+        mq = __builtin_fmaxf(mq, d * __builtin_amdgcn_rcpf(a));
+      }
+      const float nb = -(mq * (1.0f - 0x1p-19f));
+      uint32_t ncand = 0, cj = 0;
+      float cd = 0.0f, ca = 1.0f;
+#pragma unroll
+      for (int j = V - 1; j >= 0; --j) {
+        const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+        const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+        const bool c = __builtin_fmaf(nb, a, d) >= 0.0f;
+        ncand += c ? 1u : 0u;
+        cj = c ? (uint32_t)j : cj;
+        cd = c ? d : cd;
+        ca = c ? a : ca;
+      }
+      double lb_rel = s_bv[1][wave][lane];
+      uint32_t li_rel = s_bi[1][wave][lane];
+      const double q1 = (double)cd / (double)ca;
+      if (mine && q1 > lb_rel) {
+        lb_rel = q1;
+        li_rel = off0 + cj;
+      }
+      // (mq = 0: every quotient is 0 and the first element holds it, as taken)
+      const bool several = mine && ncand > 1 && mq > 0.0f;
+      if (ballot(several) != 0 && several) {
+#pragma unroll 1
+        for (int j = 0; j < V; ++j) {
+          const float d = __builtin_fabsf(diff32<DT>(cq, rq, j));
+          const float a = __builtin_fabsf(dec32<DT>(elem<DT>(rq, j)));
+          if (__builtin_fmaf(nb, a, d) >= 0.0f) {
+            const double q = (double)d / (double)a;
+            if (q > lb_rel) {
+              lb_rel = q;
+              li_rel = off0 + (uint32_t)j;
+            }
+          }
+        }
+      }
+      if (mine) {
+        s_bv[1][wave][lane] = lb_rel;
+        s_bi[1][wave][lane] = li_rel;
+      }
     }
     if (absm != 0) raise_abs(absm);
     if (relm != 0) raise_rel(relm);
