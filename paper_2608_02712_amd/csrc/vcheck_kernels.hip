@@ -90,6 +90,7 @@ constexpr int kDone = 0;      // evaluated and committed
 constexpr int kDefer = 1;     // to the exact tier, after streaming
 constexpr int kNotTaken = 2;  // not this tier (nothing changed)
 constexpr int kLocate = 3;    // committed; mismatch positions are recorded after streaming
+constexpr int kUsual = 4;     // committed by the usual step: nothing else to record
 
 // 16 bytes of raw storage held by one lane.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -1563,7 +1564,7 @@ void main_kernel(const Params P) {
       ++fast_steps;
       add_a = (double)sa;
       add_q = (double)sq;
-      return kDone;
+      return kUsual;
     }
     // not exact in binary32, not finite, r = 0 or |r| out of range: tier 2
     bool ok = fin;
@@ -1853,32 +1854,37 @@ void main_kernel(const Params P) {
       if constexpr (NT == 1) res = t1_single(cq, rq, off0, pbm, th, add_a, add_q);
       else res = t1_step(cq, rq, off0, pbm, th, add_a, add_q);
     }
-    if (tried) {
-      const bool tame = res != kNotTaken;
-      t1_next = tame ? 0u : min(2u * t1_next + 1u, 7u);
-      t1_hold = tame ? 0u : t1_next;
-    } else if (t1_hold > 0) {
-      --t1_hold;
+    if (res == kUsual) {
+      // the usual step: nothing else to decide or record
+      t1_next = 0u;  // (t1_hold is 0)
+    } else {
+      if (tried) {
+        const bool tame = res != kNotTaken;
+        t1_next = tame ? 0u : min(2u * t1_next + 1u, 7u);
+        t1_hold = tame ? 0u : t1_next;
+      } else if (t1_hold > 0) {
+        --t1_hold;
+      }
+      if (res == kNotTaken) res = t2_step(cq, rq, off0, pbm, th, add_a, add_q);
+      if (res == kLocate) {
+        if (nd == 0) {
+          // nothing of the wave is listed: its positions are recorded now, in
+          // stream order, while the loads of the next steps are in flight
+          localize(pbm, off0);
+        } else {
+          // single pair: the lane's mismatch bits wait in LDS; the entry
+          // holds the offset, bit 0, the list position and the wave
+          s_pb[wave][nd][lane] = (uint8_t)pbm;
+          defer(off0 | 1u | (nd << 1) | (wave << 6));
+        }
+      } else if (res != kDone) {
+        defer(off0);
+      } else if (NT > 1 && prim_count() != m0 && loc_on()) {
+        defer(off0 | 1u);
+      }
     }
-    if (res == kNotTaken) res = t2_step(cq, rq, off0, pbm, th, add_a, add_q);
     acc_abs += add_a;
     acc_rel += add_q;
-    if (res == kLocate) {
-      if (nd == 0) {
-        // nothing of the wave is listed: its positions are recorded now, in
-        // stream order, while the loads of the next steps are in flight
-        localize(pbm, off0);
-      } else {
-        // single pair: the lane's mismatch bits wait in LDS; the entry
-        // holds the offset, bit 0, the list position and the wave
-        s_pb[wave][nd][lane] = (uint8_t)pbm;
-        defer(off0 | 1u | (nd << 1) | (wave << 6));
-      }
-    } else if (res != kDone) {
-      defer(off0);
-    } else if (NT > 1 && prim_count() != m0 && loc_on()) {
-      defer(off0 | 1u);
-    }
     if constexpr (INTEG) integ_step(cq, rq, ALL, true, off0);
   };
 
