@@ -389,27 +389,29 @@ __device__ __forceinline__ float f32_next_up(float x) {
 
 // ------------------------------------------------------------ merge helpers
 
-// Merge of up to kBlockThreads records per pass: records are staged in LDS
-// with independent 16-byte loads, then reduced column by column in 8 fixed
-// parts of 32 records (a fixed order, so the binary64 sums are reproducible).
-constexpr int kParts = 8;
-constexpr int kPartLen = kBlockThreads / kParts;
-
+// Merge of up to kBlockThreads records per pass, one record per thread, held
+// in registers (independent 16-byte loads). Each wave reduces its 64 records
+// with DPP in a fixed order (row shifts by 1, 2, 4 and 8, then two row
+// broadcasts: an inclusive scan, whose last lane holds the total), and the
+// four wave totals are combined in wave order, so the binary64 sums are
+// reproducible. The lanes of a wave hold ascending, disjoint element ranges:
+// among records with the same maximum the first lane holding it has the
+// smallest index.
 static_assert(offsetof(ChunkRec, nfound) == 92 && offsetof(ChunkRec, eq_bits) == 96 &&
                   offsetof(ChunkRec, amax_abs) == 100 && offsetof(ChunkRec, max_abs) == 112 &&
                   offsetof(ChunkRec, max_rel) == 120 && offsetof(ChunkRec, sum_abs) == 128,
-              "neutral record layout");
+              "record word layout");
+constexpr int kRecWords = (int)(sizeof(ChunkRec) / 4);
 
 struct MergeScratch {
-  ChunkRec rec[kBlockThreads];
-  uint64_t part[kParts][kRecCounts];
-  double dpart[2][kParts];
-  double mv[2][kParts];
-  uint64_t mi[2][kParts];
-  uint32_t eqp[kParts];
-  uint32_t nfp[kParts];      // first-k entries per part (saturated at k)
-  uint32_t nfpre[kParts];    // exclusive prefix of nfp (saturated at k)
-  uint32_t nfstart[kBlockThreads];  // first output position of each record
+  // per-wave totals of the current pass
+  uint32_t wcnt[kWavesPerBlock][kRecCounts];
+  uint32_t wnf[kWavesPerBlock], weq[kWavesPerBlock];
+  double wsum[2][kWavesPerBlock], wmax[2][kWavesPerBlock];
+  uint64_t widx[2][kWavesPerBlock];
+  uint32_t woff[kWavesPerBlock];             // first output position of each wave's entries
+  uint32_t nfstart[kBlockThreads];           // first output position of each record
+  uint32_t pass_lo, pass_hi;                 // output positions of the pass's entries
   // running totals over the passes
   uint64_t cnt[kRecCounts];
   double sum_abs, sum_rel, max_abs, max_rel;
@@ -417,9 +419,17 @@ struct MergeScratch {
   uint32_t eq_all, nf_total;
 };
 
-__device__ __forceinline__ uint32_t sat_add(uint32_t a, uint32_t b, uint32_t k) {
-  const uint32_t s = a + b;
-  return (s < a || s > k) ? k : s;
+// Inclusive scan of a 32-bit value over the wave with one combining
+// operation per step (lanes with no source combine with `id`).
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_scan_u32(uint32_t x, uint32_t id, Op op) {
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, x, 0x111, 0xf, 0xf, false));  // row_shr:1
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, x, 0x112, 0xf, 0xf, false));  // row_shr:2
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, x, 0x114, 0xf, 0xf, false));  // row_shr:4
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, x, 0x118, 0xf, 0xf, false));  // row_shr:8
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
+  return x;
 }
 
 // Merges records recs[0..n) into the totals in s; record i covers elements
@@ -436,7 +446,7 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
                                           uint64_t stage_stride, uint32_t k,
                                           uint32_t *__restrict__ out32,
                                           int64_t *__restrict__ out64) {
-  const uint32_t t = threadIdx.x;
+  const uint32_t t = threadIdx.x, lane = t % kWaveSize, wave = t / kWaveSize;
   if (t < (uint32_t)kRecCounts) s.cnt[t] = 0;
   if (t == 0) {
     s.sum_abs = s.sum_rel = 0.0;
@@ -447,160 +457,115 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
   }
   for (uint32_t base = 0; base < n; base += kBlockThreads) {
     const uint32_t m = min(n - base, (uint32_t)kBlockThreads);
-    __syncthreads();
+    // the record of this thread; past the pass's last record, the neutral
+    // record (no counts, no entries, all equality bits, no maximum)
+    u32x4 v[kRecWords / 4];
     if (t < m) {
       const u32x4 *src = (const u32x4 *)(recs + base + t);
-      u32x4 v[sizeof(ChunkRec) / 16];
 #pragma unroll
-      for (int q = 0; q < (int)(sizeof(ChunkRec) / 16); ++q) v[q] = src[q];
-      u32x4 *dst = (u32x4 *)&s.rec[t];
-#pragma unroll
-      for (int q = 0; q < (int)(sizeof(ChunkRec) / 16); ++q) dst[q] = v[q];
+      for (int i = 0; i < kRecWords / 4; ++i) v[i] = src[i];
     } else {
-      // the slots past the pass's last record hold the neutral record
-      // (no counts, no entries, all equality bits, no maximum), so the
-      // part loops below run over whole parts without selects
-      u32x4 *dst = (u32x4 *)&s.rec[t];
       const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int q = 0; q < 6; ++q) dst[q] = z;                   // words 0..23
-      dst[6] = (u32x4){0xffffffffu, kNone, kNone, 0u};           // eq_bits, amax, pad
-      dst[7] = (u32x4){0u, 0xbff00000u, 0u, 0xbff00000u};        // max_abs = max_rel = -1
-      dst[8] = z;                                                // sums
+      for (int i = 0; i < 6; ++i) v[i] = z;                // words 0..23
+      v[6] = (u32x4){0xffffffffu, kNone, kNone, 0u};       // eq_bits, amax, pad
+      v[7] = (u32x4){0u, 0xbff00000u, 0u, 0xbff00000u};    // max_abs = max_rel = -1
+      v[8] = z;                                            // sums
+    }
+    auto word = [&](int i) __attribute__((always_inline)) -> uint32_t { return v[i / 4][i % 4]; };
+    auto dword = [&](int i) __attribute__((always_inline)) -> double {
+      const uint64_t lo = word(i), hi = word(i + 1);
+      return __longlong_as_double((long long)(lo | hi << 32));
+    };
+    const auto add = [](uint32_t a, uint32_t b) { return a + b; };
+    // counters: a record counts at most 2^25 (one group), a wave at most 2^31
+#pragma unroll
+    for (int f = 0; f < kRecCounts; ++f) {
+      const uint32_t c = wave_scan_u32(word(f), 0u, add);
+      if (lane == kWaveSize - 1) s.wcnt[wave][f] = c;
+    }
+    const uint32_t nf = word(23);
+    const uint32_t nf_incl = wave_scan_u32(nf, 0u, add);
+    const uint32_t eq =
+        wave_scan_u32(word(24), 0xffffffffu, [](uint32_t a, uint32_t b) { return a & b; });
+#pragma unroll
+    for (int f = 0; f < 2; ++f) {
+      const double sm = wave_sum(dword(32 + 2 * f));
+      const double x = dword(28 + 2 * f);
+      const double mx = wave_max_val(x);
+      // the first lane holding the maximum (-1: no lane has one)
+      const uint64_t holders = ballot(x == mx);
+      const uint32_t hl = holders != 0 ? (uint32_t)__builtin_ctzll(holders) : 0u;
+      const uint32_t ai = __builtin_amdgcn_readlane(word(25 + f), hl);
+      if (lane == kWaveSize - 1) {
+        s.wsum[f][wave] = sm;
+        s.wmax[f][wave] = mx;
+        s.widx[f][wave] = mx > -1.0 ? (uint64_t)(base + wave * kWaveSize + hl) * span + ai
+                                    : UINT64_MAX;
+      }
+    }
+    if (lane == kWaveSize - 1) {
+      s.wnf[wave] = nf_incl;
+      s.weq[wave] = eq;
     }
     __syncthreads();
-    // part reductions: part p covers records [32p, 32p + 32) of this pass.
-    // Each loop is unrolled with its LDS reads issued first, so the roles
-    // that share a wave do not wait on per-record round trips.
-    if (t < (uint32_t)(kParts * kRecCounts)) {
-      // a record count is at most 2^25 (one group), so a part fits 32 bits
-      const uint32_t f = t % kRecCounts, p = t / kRecCounts, lo = p * kPartLen;
-      const uint32_t *col = (const uint32_t *)&s.rec[lo] + f;
-      uint32_t xs[kPartLen];
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) xs[j] = col[j * (int)(sizeof(ChunkRec) / 4)];
-      uint32_t a = 0;
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) a += xs[j];
-      s.part[p][f] = a;
-    } else if (t < (uint32_t)(kParts * kRecCounts + 2 * kParts)) {
-      const uint32_t u = t - kParts * kRecCounts, f = u & 1u, p = u >> 1, lo = p * kPartLen;
-      const double *col = f ? &s.rec[lo].sum_rel : &s.rec[lo].sum_abs;
-      double xs[kPartLen];
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) xs[j] = col[j * (int)(sizeof(ChunkRec) / 8)];
-      double a = 0.0;  // (sums are >= 0: a neutral slot adds +0 exactly)
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) a += xs[j];
-      s.dpart[f][p] = a;
-    } else if (t < (uint32_t)(kParts * kRecCounts + 4 * kParts)) {
-      // Records of a part cover ascending, disjoint element ranges, so on
-      // equal maxima the earlier record holds the smaller index: a strict
-      // comparison keeps it. A record without a maximum holds -1.
-      const uint32_t u = t - kParts * kRecCounts - 2 * kParts, f = u & 1u, p = u >> 1;
-      const uint32_t lo = p * kPartLen;
-      const double *vcol = f ? &s.rec[lo].max_rel : &s.rec[lo].max_abs;
-      const uint32_t *icol = f ? &s.rec[lo].amax_rel : &s.rec[lo].amax_abs;
-      double xs[kPartLen];
-      uint32_t as[kPartLen];
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) {
-        xs[j] = vcol[j * (int)(sizeof(ChunkRec) / 8)];
-        as[j] = icol[j * (int)(sizeof(ChunkRec) / 4)];
-      }
-      double v = -1.0;
-      uint32_t bj = 0, ba = 0;
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) {
-        const bool take = xs[j] > v;
-        v = take ? xs[j] : v;
-        bj = take ? (uint32_t)j : bj;
-        ba = take ? as[j] : ba;
-      }
-      s.mv[f][p] = v;
-      s.mi[f][p] = v > -1.0 ? (uint64_t)(base + lo + bj) * span + ba : UINT64_MAX;
-    } else if (t < (uint32_t)(kParts * kRecCounts + 5 * kParts)) {
-      const uint32_t p = t - kParts * kRecCounts - 4 * kParts, lo = p * kPartLen;
-      uint32_t eb[kPartLen], nf[kPartLen];
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) {
-        eb[j] = s.rec[lo + j].eq_bits;
-        nf[j] = s.rec[lo + j].nfound;
-      }
-      uint32_t e = 0xffffffffu, c = 0;  // (entries <= k each: no overflow)
-#pragma unroll
-      for (int j = 0; j < kPartLen; ++j) {
-        e &= eb[j];
-        c += nf[j];
-      }
-      s.eqp[p] = e;
-      s.nfp[p] = min(c, k);
-    }
-    __syncthreads();
-    // totals over the parts, one role per wave
+    // the wave totals, in wave order, one role per thread
     if (t < (uint32_t)kRecCounts) {
       uint64_t a = s.cnt[t];
 #pragma unroll
-      for (int p = 0; p < kParts; ++p) a += s.part[p][t];
+      for (int w = 0; w < kWavesPerBlock; ++w) a += s.wcnt[w][t];
       s.cnt[t] = a;
     } else if (t == 64 || t == 65) {
       const uint32_t f = t - 64;
       double a = f ? s.sum_rel : s.sum_abs;
 #pragma unroll
-      for (int p = 0; p < kParts; ++p) a += s.dpart[f][p];
+      for (int w = 0; w < kWavesPerBlock; ++w) a += s.wsum[f][w];
       if (f) s.sum_rel = a;
       else s.sum_abs = a;
     } else if (t == 128 || t == 129) {
+      // (earlier records first: a strict comparison keeps them on ties)
       const uint32_t f = t - 128;
-      double v = f ? s.max_rel : s.max_abs;
-      uint64_t ix = f ? s.amax_rel : s.amax_abs;
+      double bv = f ? s.max_rel : s.max_abs;
+      uint64_t bi = f ? s.amax_rel : s.amax_abs;
 #pragma unroll
-      for (int p = 0; p < kParts; ++p) {
-        const double x = s.mv[f][p];
-        const uint64_t xi = s.mi[f][p];
-        const bool take = (x > v) | ((x == v) & (xi < ix));
-        v = take ? x : v;
-        ix = take ? xi : ix;
+      for (int w = 0; w < kWavesPerBlock; ++w) {
+        const bool take = s.wmax[f][w] > bv;
+        bv = take ? s.wmax[f][w] : bv;
+        bi = take ? s.widx[f][w] : bi;
       }
       if (f) {
-        s.max_rel = v;
-        s.amax_rel = ix;
+        s.max_rel = bv;
+        s.amax_rel = bi;
       } else {
-        s.max_abs = v;
-        s.amax_abs = ix;
+        s.max_abs = bv;
+        s.amax_abs = bi;
       }
     } else if (t == 192) {
       uint32_t e = s.eq_all;
 #pragma unroll
-      for (int p = 0; p < kParts; ++p) e &= s.eqp[p];
+      for (int w = 0; w < kWavesPerBlock; ++w) e &= s.weq[w];
       s.eq_all = e;
     } else if (t == 193) {
+      // (a wave lists at most 64 k <= 2^16 entries: no overflow)
       uint32_t c = s.nf_total;
+      s.pass_lo = c;
 #pragma unroll
-      for (int p = 0; p < kParts; ++p) {
-        s.nfpre[p] = c;
-        c = sat_add(c, s.nfp[p], k);
+      for (int w = 0; w < kWavesPerBlock; ++w) {
+        s.woff[w] = c;
+        c = min(c + s.wnf[w], k);
       }
+      s.pass_hi = c;
+      s.nf_total = c;
     }
     __syncthreads();
     if (k > 0) {
-      // first output position of each record: its part's prefix plus the
-      // entries of the records before it in the part
-      if (t < m) {
-        const uint32_t p = t / kPartLen, lo = p * kPartLen;
-        uint32_t pos = s.nfpre[p];
-        uint32_t nf[kPartLen];
-#pragma unroll
-        for (int j = 0; j < kPartLen; ++j) nf[j] = s.rec[lo + j].nfound;
-#pragma unroll
-        for (int j = 0; j < kPartLen; ++j) pos += lo + j < t ? nf[j] : 0u;
-        pos = min(pos, k);  // (pos <= k + 32 k before the clamp)
-        s.nfstart[t] = pos;
-      }
+      // first output position of each record: its wave's offset plus the
+      // entries of the records before it in the wave
+      if (t < m) s.nfstart[t] = min(s.woff[wave] + (nf_incl - nf), k);
       __syncthreads();
       // one output entry per thread: entry e belongs to the last record whose
       // first position is <= e
-      const uint32_t lo = s.nf_total, hi = sat_add(s.nfpre[kParts - 1], s.nfp[kParts - 1], k);
+      const uint32_t lo = s.pass_lo, hi = s.pass_hi;
       for (uint32_t e = lo + t; e < hi; e += kBlockThreads) {
         uint32_t a = 0, b = m - 1;
         while (a < b) {
@@ -615,7 +580,6 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
       }
       __syncthreads();
     }
-    if (t == 193) s.nf_total = sat_add(s.nfpre[kParts - 1], s.nfp[kParts - 1], k);
   }
   __syncthreads();
 }
