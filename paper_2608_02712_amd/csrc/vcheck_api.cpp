@@ -136,6 +136,7 @@ struct Plan {
 #define VCK_WAVE_TARGET 16384
 #endif
 
+static_assert(4 * (65536 / 2) <= vck::kMaxChunkElems, "chunk size bound of the merge");
 uint32_t unit_for(uint64_t group_elems, int32_t dtype) {
   const uint64_t lo = 1024, hi = 65536 / elem_size(dtype);
   uint64_t u = lo;

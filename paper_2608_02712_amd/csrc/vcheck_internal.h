@@ -14,6 +14,7 @@ constexpr int kWavesPerBlock = 4;
 constexpr int kBlockThreads = kWaveSize * kWavesPerBlock;
 constexpr int kTileWindow = 1024;  // LDS tile counters per block
 constexpr int kGroupChunks = 256;  // chunks merged by one group record
+constexpr uint32_t kMaxChunkElems = 1u << 17;  // 4 units of at most 64 KiB of 16-bit data
 
 // Unsigned division of a 32-bit numerator by an invariant divisor d
 // (1 <= d < 2^32) as a multiply-high, an add and two shifts (Granlund and

@@ -389,12 +389,15 @@ __device__ __forceinline__ float f32_next_up(float x) {
 
 // ------------------------------------------------------------ merge helpers
 
-// Merge of up to kBlockThreads records per pass, one record per thread, held
-// in registers (independent 16-byte loads). Each wave reduces its 64 records
-// with DPP in a fixed order (row shifts by 1, 2, 4 and 8, then two row
-// broadcasts: an inclusive scan, whose last lane holds the total), and the
-// four wave totals are combined in wave order, so the binary64 sums are
-// reproducible. The lanes of a wave hold ascending, disjoint element ranges:
+// The finalize runs blocks of kFinThreads threads. Its merge takes up to
+// kFinThreads records per pass (a chunk group is one pass), one record per
+// thread, held in registers (independent 16-byte loads). Each wave reduces
+// its 64 records with DPP in a fixed order (row shifts by 1, 2, 4 and 8, then
+// two row broadcasts: an inclusive scan, whose last lane holds the total),
+// and the wave totals are combined in wave order, so the binary64 sums are
+// reproducible. (One block of 1024 threads merging up to 4096 records in
+// four passes took twice as long as 16 blocks of 256 records and a second
+// level: the records' loads through one CU bound it.) The lanes of a wave hold ascending, disjoint element ranges:
 // among records with the same maximum the first lane holding it has the
 // smallest index.
 static_assert(offsetof(ChunkRec, nfound) == 92 && offsetof(ChunkRec, eq_bits) == 96 &&
@@ -402,15 +405,18 @@ static_assert(offsetof(ChunkRec, nfound) == 92 && offsetof(ChunkRec, eq_bits) ==
                   offsetof(ChunkRec, max_rel) == 120 && offsetof(ChunkRec, sum_abs) == 128,
               "record word layout");
 constexpr int kRecWords = (int)(sizeof(ChunkRec) / 4);
+constexpr int kFinThreads = kBlockThreads;
+constexpr int kFinWaves = kFinThreads / kWaveSize;
+static_assert(kGroupChunks % kFinThreads == 0, "a chunk group is whole merge passes");
 
 struct MergeScratch {
   // per-wave totals of the current pass
-  uint32_t wcnt[kWavesPerBlock][kRecCounts];
-  uint32_t wnf[kWavesPerBlock], weq[kWavesPerBlock];
-  double wsum[2][kWavesPerBlock], wmax[2][kWavesPerBlock];
-  uint64_t widx[2][kWavesPerBlock];
-  uint32_t woff[kWavesPerBlock];             // first output position of each wave's entries
-  uint32_t nfstart[kBlockThreads];           // first output position of each record
+  uint32_t wcnt[kFinWaves][kRecCounts];
+  uint32_t wnf[kFinWaves], weq[kFinWaves];
+  double wsum[2][kFinWaves], wmax[2][kFinWaves];
+  uint64_t widx[2][kFinWaves];
+  uint32_t woff[kFinWaves];                  // first output position of each wave's entries
+  uint32_t nfstart[kFinThreads];             // first output position of each record
   uint32_t pass_lo, pass_hi;                 // output positions of the pass's entries
   // running totals over the passes
   uint64_t cnt[kRecCounts];
@@ -433,7 +439,8 @@ __device__ __forceinline__ uint32_t wave_scan_u32(uint32_t x, uint32_t id, Op op
 }
 
 // Merges records recs[0..n) into the totals in s; record i covers elements
-// [i * span, (i + 1) * span) of the parent range. With k > 0 the staged
+// [i * span, (i + 1) * span) of the parent range. With
+// k > 0 the staged
 // first-k lists are concatenated in record order (entry e of record i is
 // parent element i * span + e) into out64 (final: global indices) or out32
 // (a group: offsets within the group), at most k entries; s.nf_total is
@@ -455,8 +462,8 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
     s.eq_all = 0xffffffffu;
     s.nf_total = 0;
   }
-  for (uint32_t base = 0; base < n; base += kBlockThreads) {
-    const uint32_t m = min(n - base, (uint32_t)kBlockThreads);
+  for (uint32_t base = 0; base < n; base += kFinThreads) {
+    const uint32_t m = min(n - base, (uint32_t)kFinThreads);
     // the record of this thread; past the pass's last record, the neutral
     // record (no counts, no entries, all equality bits, no maximum)
     u32x4 v[kRecWords / 4];
@@ -478,7 +485,10 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
       return __longlong_as_double((long long)(lo | hi << 32));
     };
     const auto add = [](uint32_t a, uint32_t b) { return a + b; };
-    // counters: a record counts at most 2^25 (one group), a wave at most 2^31
+    // counters: a record counts at most kGroupChunks * kMaxChunkElems
+    // (a group record), so a wave's sum fits 32 bits
+    static_assert((uint64_t)kGroupChunks * kMaxChunkElems * kWaveSize <= (1ull << 32),
+                  "wave sums of record counts");
 #pragma unroll
     for (int f = 0; f < kRecCounts; ++f) {
       const uint32_t c = wave_scan_u32(word(f), 0u, add);
@@ -513,13 +523,13 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
     if (t < (uint32_t)kRecCounts) {
       uint64_t a = s.cnt[t];
 #pragma unroll
-      for (int w = 0; w < kWavesPerBlock; ++w) a += s.wcnt[w][t];
+      for (int w = 0; w < kFinWaves; ++w) a += s.wcnt[w][t];
       s.cnt[t] = a;
     } else if (t == 64 || t == 65) {
       const uint32_t f = t - 64;
       double a = f ? s.sum_rel : s.sum_abs;
 #pragma unroll
-      for (int w = 0; w < kWavesPerBlock; ++w) a += s.wsum[f][w];
+      for (int w = 0; w < kFinWaves; ++w) a += s.wsum[f][w];
       if (f) s.sum_rel = a;
       else s.sum_abs = a;
     } else if (t == 128 || t == 129) {
@@ -528,7 +538,7 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
       double bv = f ? s.max_rel : s.max_abs;
       uint64_t bi = f ? s.amax_rel : s.amax_abs;
 #pragma unroll
-      for (int w = 0; w < kWavesPerBlock; ++w) {
+      for (int w = 0; w < kFinWaves; ++w) {
         const bool take = s.wmax[f][w] > bv;
         bv = take ? s.wmax[f][w] : bv;
         bi = take ? s.widx[f][w] : bi;
@@ -543,14 +553,14 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
     } else if (t == 192) {
       uint32_t e = s.eq_all;
 #pragma unroll
-      for (int w = 0; w < kWavesPerBlock; ++w) e &= s.weq[w];
+      for (int w = 0; w < kFinWaves; ++w) e &= s.weq[w];
       s.eq_all = e;
     } else if (t == 193) {
       // (a wave lists at most 64 k <= 2^16 entries: no overflow)
       uint32_t c = s.nf_total;
       s.pass_lo = c;
 #pragma unroll
-      for (int w = 0; w < kWavesPerBlock; ++w) {
+      for (int w = 0; w < kFinWaves; ++w) {
         s.woff[w] = c;
         c = min(c + s.wnf[w], k);
       }
@@ -566,7 +576,7 @@ __device__ __forceinline__ void merge_all(MergeScratch &s, const ChunkRec *__res
       // one output entry per thread: entry e belongs to the last record whose
       // first position is <= e
       const uint32_t lo = s.pass_lo, hi = s.pass_hi;
-      for (uint32_t e = lo + t; e < hi; e += kBlockThreads) {
+      for (uint32_t e = lo + t; e < hi; e += kFinThreads) {
         uint32_t a = 0, b = m - 1;
         while (a < b) {
           const uint32_t mid = (a + b + 1) / 2;
@@ -613,7 +623,7 @@ __device__ __forceinline__ void finalize_case(MergeScratch &s, const FinArgs &P,
   merge_all<true>(s, recs, n, span, stage, stage_stride, ok ? k : 0u, nullptr, fk);
   if (want_fk) {
     const uint32_t nf = ok ? s.nf_total : 0u;
-    for (uint32_t pos = nf + threadIdx.x; pos < k; pos += kBlockThreads) fk[pos] = -1;
+    for (uint32_t pos = nf + threadIdx.x; pos < k; pos += kFinThreads) fk[pos] = -1;
   }
   if (threadIdx.x != 0) return;
   const int nt = P.n_tols;
@@ -2127,17 +2137,17 @@ __device__ __forceinline__ void publish_tiles(const Params &P) {
   uint32_t *__restrict__ out = P.tile_out;
   const uint64_t n = P.tiles_total;
   const uint64_t nb = gridDim.x - P.n_groups, b = blockIdx.x - P.n_groups;
-  constexpr uint64_t kPer = (uint64_t)kBlockThreads * kTileRun;
+  constexpr uint64_t kPer = (uint64_t)kFinThreads * kTileRun;
   for (uint64_t base = b * kPer + threadIdx.x; base < n; base += nb * kPer) {
     uint32_t v[kTileRun];
 #pragma unroll
     for (int q = 0; q < kTileRun; ++q) {
-      const uint64_t i = base + (uint64_t)q * kBlockThreads;
+      const uint64_t i = base + (uint64_t)q * kFinThreads;
       v[q] = i < n ? acc[i] : 0u;
     }
 #pragma unroll
     for (int q = 0; q < kTileRun; ++q) {
-      const uint64_t i = base + (uint64_t)q * kBlockThreads;
+      const uint64_t i = base + (uint64_t)q * kFinThreads;
       if (i < n) {
         out[i] = v[q];
         acc[i] = 0;
@@ -2155,7 +2165,7 @@ __device__ __forceinline__ void publish_tiles(const Params &P) {
 // with it every output bit, does not depend on which block arrives last.
 // The blocks past the group blocks publish the tile counts. Kernel
 // boundaries order the chunk records and tile counts before this launch.
-__global__ __launch_bounds__(kBlockThreads) void finalize_kernel(const Params P) {
+__global__ __launch_bounds__(kFinThreads) void finalize_kernel(const Params P) {
   __shared__ MergeScratch M;
   __shared__ uint32_t s_last;
   const uint64_t g = blockIdx.x;
@@ -2290,13 +2300,13 @@ hipError_t launch_prologue(const Prologue &p, hipStream_t s) {
 }
 
 hipError_t launch_finalize(const Params &p, hipStream_t s) {
-  constexpr uint64_t kPer = (uint64_t)kBlockThreads * kTileRun;
+  constexpr uint64_t kPer = (uint64_t)kFinThreads * kTileRun;
   uint64_t tile_blocks = 0;
   if (p.tile_out != nullptr && p.tile_maps != nullptr && p.tiles_total > 0)
     tile_blocks = min((p.tiles_total + kPer - 1) / kPer, (uint64_t)1024);
   const uint64_t blocks = p.n_groups + tile_blocks;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)blocks), dim3(kBlockThreads), 0, s, p);
+  hipLaunchKernelGGL(finalize_kernel, dim3((uint32_t)blocks), dim3(kFinThreads), 0, s, p);
   return hipGetLastError();
 }
 
