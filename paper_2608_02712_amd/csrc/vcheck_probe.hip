@@ -428,6 +428,24 @@ __global__ __launch_bounds__(kPThreads) void probe_kernel(const ProbeParams P) {
   }
 }
 
+// Sum of one 32-bit field over records part, part + 4, ... below n, with the
+// loads of eight records issued before their additions (integer sums: any
+// order gives the same total).
+template <typename Rec, typename F>
+__device__ __forceinline__ uint64_t strided_sum(const Rec *recs, uint32_t part, uint32_t n, F field) {
+  uint64_t h = 0;
+  uint32_t i = part;
+  for (; i + 28 < n; i += 32) {
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = field(recs[i + 4 * u]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) h += v[u];
+  }
+  for (; i < n; i += 4) h += field(recs[i]);
+  return h;
+}
+
 // Merges records recs[0 .. n) (n <= 256) in a fixed order; thread 0 gets the
 // totals in r, threads 0..63 the histogram bins in hist.
 __device__ void merge_recs(ProbeLds &s, const ProbeRec *recs, uint32_t n, ProbeRec &r,
@@ -449,8 +467,7 @@ __device__ void merge_recs(ProbeLds &s, const ProbeRec *recs, uint32_t n, ProbeR
   block_reduce(s, r);
   // histogram: thread t sums bin t % 64 over records t / 64, t / 64 + 4, ...
   const uint32_t bin = t & 63u, part = t >> 6;
-  uint64_t h = 0;
-  for (uint32_t i = part; i < n; i += 4) h += recs[i].hist[bin];
+  const uint64_t h = strided_sum(recs, part, n, [&](const ProbeRec &x) { return x.hist[bin]; });
   __syncthreads();
   s.c[0][t] = h;
   __syncthreads();
@@ -803,9 +820,10 @@ __device__ void np_merge(NpLds &s, const NpRec *recs, uint32_t n, NpRec &r, uint
   np_reduce(s, r);
   const uint32_t bin = t & 63u, part = t >> 6;
   uint64_t h = 0;
-  if (bin < (uint32_t)(kRatioBins + kUlpBins))
-    for (uint32_t i = part; i < n; i += 4)
-      h += bin < (uint32_t)kRatioBins ? recs[i].ratio_hist[bin] : recs[i].ulp_hist[bin - kRatioBins];
+  if (bin < (uint32_t)kRatioBins)
+    h = strided_sum(recs, part, n, [&](const NpRec &x) { return x.ratio_hist[bin]; });
+  else if (bin < (uint32_t)(kRatioBins + kUlpBins))
+    h = strided_sum(recs, part, n, [&](const NpRec &x) { return x.ulp_hist[bin - kRatioBins]; });
   __syncthreads();
   s.c[0][t] = h;
   __syncthreads();
