@@ -168,6 +168,60 @@ __device__ __forceinline__ void pick_max(double &v, int64_t &i, double v2, int64
   }
 }
 
+// One step of a 64-bit DPP pattern: the value CTRL moves in (lanes with no
+// source, or outside the rows ROWS enables, see id).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t dpp64(uint64_t x, uint64_t id) {
+  const uint32_t lo = __builtin_amdgcn_update_dpp((uint32_t)id, (uint32_t)x, CTRL, ROWS, 0xf, false);
+  const uint32_t hi =
+      __builtin_amdgcn_update_dpp((uint32_t)(id >> 32), (uint32_t)(x >> 32), CTRL, ROWS, 0xf, false);
+  return (uint64_t)hi << 32 | lo;
+}
+
+// Wave-wide reduction of a 64-bit value with op, wave-uniform, in a fixed
+// order: row shifts by 1, 2, 4 and 8 and two row broadcasts (an inclusive
+// scan whose last lane holds the result); id is op's identity.
+template <typename Op>
+__device__ __forceinline__ uint64_t wave_reduce64(uint64_t x, uint64_t id, Op op) {
+  x = op(x, dpp64<0x111, 0xf>(x, id));  // row_shr:1
+  x = op(x, dpp64<0x112, 0xf>(x, id));  // row_shr:2
+  x = op(x, dpp64<0x114, 0xf>(x, id));  // row_shr:4
+  x = op(x, dpp64<0x118, 0xf>(x, id));  // row_shr:8
+  x = op(x, dpp64<0x142, 0xa>(x, id));  // row_bcast:15
+  x = op(x, dpp64<0x143, 0xc>(x, id));  // row_bcast:31
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, 63);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(x >> 32), 63);
+  return (uint64_t)hi << 32 | lo;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
+  return wave_reduce64(x, 0ull, [](uint64_t a, uint64_t b) { return a + b; });
+}
+__device__ __forceinline__ double wave_sum_f64(double x) {
+  return __longlong_as_double((long long)wave_reduce64(
+      (uint64_t)__double_as_longlong(x), 0ull, [](uint64_t a, uint64_t b) {
+        return (uint64_t)__double_as_longlong(__longlong_as_double((long long)a) +
+                                              __longlong_as_double((long long)b));
+      }));
+}
+// The wave's (value, index) extreme among lanes with index >= 0: the
+// smallest (MAX = false) or largest value, then the smallest index holding
+// it; index -1 when no lane has one.
+template <bool MAX>
+__device__ __forceinline__ void wave_pick(double &v, int64_t &i) {
+  const double none = MAX ? -__builtin_inf() : __builtin_inf();
+  const double x = i >= 0 ? v : none;
+  const double e = __longlong_as_double((long long)wave_reduce64(
+      (uint64_t)__double_as_longlong(x), (uint64_t)__double_as_longlong(none),
+      [](uint64_t a, uint64_t b) {
+        const double da = __longlong_as_double((long long)a), db = __longlong_as_double((long long)b);
+        return (uint64_t)__double_as_longlong(MAX ? __builtin_fmax(da, db) : __builtin_fmin(da, db));
+      }));
+  const uint64_t k = wave_reduce64((i >= 0 && x == e) ? (uint64_t)i : UINT64_MAX, UINT64_MAX,
+                                   [](uint64_t a, uint64_t b) { return a < b ? a : b; });
+  v = e;
+  i = k == UINT64_MAX ? -1 : (int64_t)k;
+}
+
 struct ProbeLds {
   union {
     uint32_t hist[kPWaves * 64 * kRowWords];  // while streaming
@@ -178,12 +232,76 @@ struct ProbeLds {
       uint64_t c[4][kPThreads];
     };
   };
+  // per-wave totals of block_reduce
+  uint64_t wc[4][kPWaves];
+  double wd[3][kPWaves], wv[2][kPWaves];
+  int64_t wi[2][kPWaves];
   uint32_t tensor;
 };
 
-// Fixed-order reduction of the per-thread partials in s (256 threads) into
-// a record (valid in thread 0).
+// Fixed-order reduction of the per-thread partials in s (256 threads; each
+// thread's own slots) into a record (valid in thread 0): DPP wave
+// reductions, then the four waves in order.
 __device__ void block_reduce(ProbeLds &s, ProbeRec &r) {
+  const uint32_t t = threadIdx.x, lane = t & 63u, wave = t >> 6;
+  uint64_t c[4];
+  double d[3], v[2];
+  int64_t i[2];
+#pragma unroll
+  for (int f = 0; f < 4; ++f) c[f] = wave_sum_u64(s.c[f][t]);
+#pragma unroll
+  for (int f = 0; f < 3; ++f) d[f] = wave_sum_f64(s.d[f][t]);
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+    v[f] = s.mv[f][t];
+    i[f] = s.mi[f][t];
+  }
+  wave_pick<false>(v[0], i[0]);
+  wave_pick<true>(v[1], i[1]);
+  if (lane == 0) {
+#pragma unroll
+    for (int f = 0; f < 4; ++f) s.wc[f][wave] = c[f];
+#pragma unroll
+    for (int f = 0; f < 3; ++f) s.wd[f][wave] = d[f];
+#pragma unroll
+    for (int f = 0; f < 2; ++f) {
+      s.wv[f][wave] = v[f];
+      s.wi[f][wave] = i[f];
+    }
+  }
+  __syncthreads();
+  if (t == 0) {
+    uint64_t cc[4] = {0, 0, 0, 0};
+    double dd[3] = {0.0, 0.0, 0.0};
+    double mn = 0.0, mx = 0.0;
+    int64_t imn = -1, imx = -1;
+    for (int w = 0; w < kPWaves; ++w) {
+#pragma unroll
+      for (int f = 0; f < 4; ++f) cc[f] += s.wc[f][w];
+#pragma unroll
+      for (int f = 0; f < 3; ++f) dd[f] += s.wd[f][w];
+      pick_min(mn, imn, s.wv[0][w], s.wi[0][w]);
+      pick_max(mx, imx, s.wv[1][w], s.wi[1][w]);
+    }
+    r.nan = cc[0];
+    r.inf = cc[1];
+    r.zero = cc[2];
+    r.fin = cc[3];
+    r.sum = dd[0];
+    r.sum_sq = dd[1];
+    r.sum_abs = dd[2];
+    r.argmin = imn;
+    r.argmax = imx;
+    r.min = imn < 0 ? 0.0 : mn;
+    r.max = imx < 0 ? 0.0 : mx;
+  }
+}
+
+// Fixed-order tree reduction of the per-thread partials in s (256 threads)
+// into a record (valid in thread 0). The streaming kernel ends each chunk
+// with it: its levels below 64 threads occupy one wave, so it costs fewer
+// vector instructions than the DPP form, which the merge launches use.
+__device__ void block_reduce_tree(ProbeLds &s, ProbeRec &r) {
   const uint32_t t = threadIdx.x;
   for (uint32_t w = kPThreads / 2; w >= 1; w >>= 1) {
     __syncthreads();
@@ -391,7 +509,7 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
   s.mv[1][t] = mx;
   s.mi[1][t] = imx == 0xffffffffu ? -1 : (int64_t)(c0 + imx);
   ProbeRec r;
-  block_reduce(s, r);
+  block_reduce_tree(s, r);
   if (t == 0) {
     rec->nan = r.nan;
     rec->inf = r.inf;
@@ -571,6 +689,11 @@ struct NpLds {
       uint32_t mu[kPThreads];
     };
   };
+  // per-wave totals of np_reduce
+  uint64_t wc[3][kPWaves];
+  double wv[kPWaves];
+  int64_t wi[kPWaves];
+  uint32_t wu[kPWaves];
   uint32_t item;
 };
 
@@ -582,8 +705,49 @@ __device__ __forceinline__ void np_pick(double &v, int64_t &i, double v2, int64_
   }
 }
 
-// Fixed-order reduction of the partials in s into r (valid in thread 0).
+// Fixed-order reduction of the partials in s (each thread's own slots) into
+// r (valid in thread 0): DPP wave reductions, then the four waves in order.
 __device__ void np_reduce(NpLds &s, NpRec &r) {
+  const uint32_t t = threadIdx.x, lane = t & 63u, wave = t >> 6;
+  uint64_t c[3];
+#pragma unroll
+  for (int f = 0; f < 3; ++f) c[f] = wave_sum_u64(s.c[f][t]);
+  double v = s.mv[t];
+  int64_t i = s.mi[t];
+  wave_pick<true>(v, i);
+  const uint32_t u = (uint32_t)wave_reduce64(s.mu[t], 0ull,
+                                             [](uint64_t a, uint64_t b) { return a > b ? a : b; });
+  if (lane == 0) {
+#pragma unroll
+    for (int f = 0; f < 3; ++f) s.wc[f][wave] = c[f];
+    s.wv[wave] = v;
+    s.wi[wave] = i;
+    s.wu[wave] = u;
+  }
+  __syncthreads();
+  if (t == 0) {
+    uint64_t cc[3] = {0, 0, 0};
+    double mv = 0.0;
+    int64_t mi = -1;
+    uint32_t mu = 0;
+    for (int w = 0; w < kPWaves; ++w) {
+#pragma unroll
+      for (int f = 0; f < 3; ++f) cc[f] += s.wc[f][w];
+      np_pick(mv, mi, s.wv[w], s.wi[w]);
+      mu = max(mu, s.wu[w]);
+    }
+    r.n_pairs = cc[0];
+    r.n_fail = cc[1];
+    r.n_zero_tol = cc[2];
+    r.argmax_ratio = mi;
+    r.max_ratio = mi < 0 ? 0.0 : mv;
+    r.max_ulp_fail = mu;
+  }
+}
+
+// Fixed-order tree reduction of the partials in s into r (valid in thread
+// 0), for the end of a streaming chunk (as block_reduce_tree).
+__device__ void np_reduce_tree(NpLds &s, NpRec &r) {
   const uint32_t t = threadIdx.x;
   for (uint32_t w = kPThreads / 2; w >= 1; w >>= 1) {
     __syncthreads();
@@ -773,7 +937,7 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
   s.mi[t] = li == 0xffffffffu ? -1 : (int64_t)(c0 + li);
   s.mu[t] = mu;
   NpRec r;
-  np_reduce(s, r);
+  np_reduce_tree(s, r);
   if (t == 0) {
     rec->n_pairs = r.n_pairs;
     rec->n_fail = r.n_fail;
