@@ -1159,6 +1159,9 @@ hipError_t launch_nearpass(const NpParams &p, uint64_t n_chunks, uint64_t n_grou
   hipLaunchKernelGGL(nearpass_merge_kernel, dim3((uint32_t)n_groups), dim3(kPThreads), 0, s, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // (every case owns at least one group: as many groups as cases means no
+  // case has group records to merge)
+  if (n_groups == (uint64_t)p.n_cases) return hipSuccess;
   hipLaunchKernelGGL(nearpass_final_kernel, dim3((uint32_t)p.n_cases), dim3(kPThreads), 0, s, p);
   return hipGetLastError();
 }
@@ -1174,6 +1177,9 @@ hipError_t launch_probe(const ProbeParams &p, uint64_t n_chunks, uint64_t n_grou
   hipLaunchKernelGGL(probe_merge_kernel, dim3((uint32_t)n_groups), dim3(kPThreads), 0, s, p);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // (every tensor owns at least one group: as many groups as tensors means
+  // no tensor has group records to merge)
+  if (n_groups == (uint64_t)p.n_tensors) return hipSuccess;
   hipLaunchKernelGGL(probe_final_kernel, dim3((uint32_t)p.n_tensors), dim3(kPThreads), 0, s, p);
   return hipGetLastError();
 }
