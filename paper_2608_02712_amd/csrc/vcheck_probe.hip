@@ -18,10 +18,13 @@
 // boundaries order the launches; no floating-point atomics are used, so the
 // results are bit-reproducible.
 //
-// Histogram: each lane owns a private row of 8-bit counters in LDS (four
-// bins per word, rows padded to 17 words so that lanes incrementing the same
-// bin hit different banks); a lane counts at most U / 64 <= 128 elements
-// (U <= 8192), so no counter overflows. The rows are summed when the chunk
+// Histogram: 32-bit counters in LDS, slot-major, one column per lane
+// position that the block's four waves share (the increments are LDS
+// atomics): the counter of slot b for lane l is word 64 b + l, so the 64
+// lanes of one increment always hit 64 different banks. Slots 0..63 are the
+// bins, slot 64 counts the zeros of the usual steps (binary16 zeros go to
+// slot 16 instead, the bin of 2^-25, which no non-zero binary16 value
+// reaches). No counter can overflow. The columns are summed when the chunk
 // is done.
 #pragma clang fp contract(off)
 
@@ -32,8 +35,12 @@ namespace {
 
 constexpr int kPWaves = 4;
 constexpr int kPThreads = kPWaves * 64;
-constexpr int kRowWords = kHistBins / 4 + 1;  // 8-bit counters plus one pad word
-static_assert(kHistBins % 4 == 0, "the pad word's first byte is bin kHistBins");
+constexpr int kPSlots = kHistBins + 1;  // the bins, then the zero slot
+// Binary32 exponent field of the bin below binary16's smallest subnormal
+// (2^-24 has field 103): binary16 zeros are clamped up to it.
+constexpr uint32_t kF16ZeroField = 102;
+constexpr uint32_t kF16ZeroBin = kF16ZeroField - 127 - kHistEmin + 1;
+static_assert(kF16ZeroBin == 16, "bin of 2^-25");
 
 #define PRB_GLOBAL __attribute__((address_space(1)))
 
@@ -41,6 +48,14 @@ typedef uint32_t p32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ p32x4 pload16(const uint8_t *p) {
   return __builtin_nontemporal_load((const PRB_GLOBAL p32x4 *)(p));
+}
+
+// Raw buffer resources: the fourth descriptor word of the gfx9 family for
+// untyped dword accesses; offsets at or beyond the record count read 0.
+constexpr int kBufferWord3 = 0x00020000;
+// 16-byte nontemporal load at byte voff + soff of a raw buffer.
+__device__ __forceinline__ p32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 2 /* nt */);
 }
 
 // Exact binary32 value of element j (of V) of a 16-byte vector.
@@ -222,16 +237,31 @@ __device__ __forceinline__ void wave_pick(double &v, int64_t &i) {
   i = k == UINT64_MAX ? -1 : (int64_t)k;
 }
 
-struct ProbeLds {
+// LDS of the streaming kernel: the histogram columns while streaming, the
+// per-thread partials of the chunk afterwards (counts, binary32 extremes and
+// their offsets from the chunk's first element all fit 32 bits), so that
+// eight blocks fit one compute unit.
+constexpr uint32_t kNoOff = 0xffffffffu;  // no finite element yet
+struct alignas(16) ChunkLds {
   union {
-    uint32_t hist[kPWaves * 64 * kRowWords];  // while streaming
-    struct {                                  // per-thread partials afterwards
+    uint32_t hist[kPSlots * 64];
+    struct {
       double d[3][kPThreads];
-      double mv[2][kPThreads];
-      int64_t mi[2][kPThreads];
-      uint64_t c[4][kPThreads];
+      float v[2][kPThreads];
+      uint32_t o[2][kPThreads];
+      uint32_t n[4][kPThreads];
     };
   };
+  uint32_t tensor;
+};
+
+// LDS of the merge launches.
+struct ProbeLds {
+  // per-thread partials
+  double d[3][kPThreads];
+  double mv[2][kPThreads];
+  int64_t mi[2][kPThreads];
+  uint64_t c[4][kPThreads];
   // per-wave totals of block_reduce
   uint64_t wc[4][kPWaves];
   double wd[3][kPWaves], wv[2][kPWaves];
@@ -297,11 +327,22 @@ __device__ void block_reduce(ProbeLds &s, ProbeRec &r) {
   }
 }
 
-// Fixed-order tree reduction of the per-thread partials in s (256 threads)
-// into a record (valid in thread 0). The streaming kernel ends each chunk
-// with it: its levels below 64 threads occupy one wave, so it costs fewer
-// vector instructions than the DPP form, which the merge launches use.
-__device__ void block_reduce_tree(ProbeLds &s, ProbeRec &r) {
+// (value, offset) of the smaller (MAX = false) or larger of two binary32
+// candidates; equal values keep the smaller offset; kNoOff marks none.
+template <bool MAX>
+__device__ __forceinline__ void pick_off(float &v, uint32_t &o, float v2, uint32_t o2) {
+  if (o2 == kNoOff) return;
+  if (o == kNoOff || (MAX ? v2 > v : v2 < v) || (v2 == v && o2 < o)) {
+    v = v2;
+    o = o2;
+  }
+}
+
+// Fixed-order tree reduction of the per-thread partials of the chunk that
+// starts at element c0 into its record, written by thread 0. Its levels
+// below 64 threads occupy one wave, so it costs fewer vector instructions
+// than the DPP form that the merge launches use.
+__device__ void chunk_reduce(ChunkLds &s, uint64_t c0, ProbeRec *rec) {
   const uint32_t t = threadIdx.x;
   for (uint32_t w = kPThreads / 2; w >= 1; w >>= 1) {
     __syncthreads();
@@ -309,147 +350,156 @@ __device__ void block_reduce_tree(ProbeLds &s, ProbeRec &r) {
 #pragma unroll
       for (int f = 0; f < 3; ++f) s.d[f][t] += s.d[f][t + w];
 #pragma unroll
-      for (int f = 0; f < 4; ++f) s.c[f][t] += s.c[f][t + w];
-      pick_min(s.mv[0][t], s.mi[0][t], s.mv[0][t + w], s.mi[0][t + w]);
-      pick_max(s.mv[1][t], s.mi[1][t], s.mv[1][t + w], s.mi[1][t + w]);
+      for (int f = 0; f < 4; ++f) s.n[f][t] += s.n[f][t + w];
+      pick_off<false>(s.v[0][t], s.o[0][t], s.v[0][t + w], s.o[0][t + w]);
+      pick_off<true>(s.v[1][t], s.o[1][t], s.v[1][t + w], s.o[1][t + w]);
     }
   }
   __syncthreads();
   if (t == 0) {
-    r.nan = s.c[0][0];
-    r.inf = s.c[1][0];
-    r.zero = s.c[2][0];
-    r.fin = s.c[3][0];
-    r.sum = s.d[0][0];
-    r.sum_sq = s.d[1][0];
-    r.sum_abs = s.d[2][0];
-    r.argmin = s.mi[0][0];
-    r.argmax = s.mi[1][0];
-    r.min = s.mi[0][0] < 0 ? 0.0 : s.mv[0][0];
-    r.max = s.mi[1][0] < 0 ? 0.0 : s.mv[1][0];
+    rec->nan = s.n[0][0];
+    rec->inf = s.n[1][0];
+    rec->zero = s.n[2][0];
+    rec->fin = s.n[3][0];
+    rec->argmin = s.o[0][0] == kNoOff ? -1 : (int64_t)(c0 + s.o[0][0]);
+    rec->argmax = s.o[1][0] == kNoOff ? -1 : (int64_t)(c0 + s.o[1][0]);
+    rec->min = s.o[0][0] == kNoOff ? 0.0 : (double)s.v[0][0];
+    rec->max = s.o[1][0] == kNoOff ? 0.0 : (double)s.v[1][0];
+    rec->sum = s.d[0][0];
+    rec->sum_sq = s.d[1][0];
+    rec->sum_abs = s.d[2][0];
+    rec->pad[0] = 0;
   }
 }
 
 // Stream one chunk: per-lane partials, then the chunk record.
 template <int DT>
-__device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint64_t c1,
+__device__ void probe_chunk(ChunkLds &s, const ProbeTensor &T, uint64_t c0, uint64_t c1,
                             uint32_t U, ProbeRec *rec) {
   constexpr int V = DT == VC_F32 ? 4 : 8;
   constexpr int ES = DT == VC_F32 ? 4 : 2;
   constexpr uint32_t ITER = 64 * V;
   const uint32_t t = threadIdx.x, lane = t & 63u;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  uint32_t *const row = s.hist + t * kRowWords;
-  for (int w = 0; w < kRowWords; ++w) row[w] = 0;
+  for (uint32_t w = t; w < (uint32_t)(kPSlots * 64); w += kPThreads) s.hist[w] = 0;
+  __syncthreads();
+  // lane's column; col[64 * b] is its counter of slot b
+  uint32_t *const col = s.hist + lane;
   const uint64_t w0 = min(c0 + (uint64_t)wave * U, c1), w1 = min(w0 + U, c1);
   const bool vec = ((uintptr_t)T.data % 16) == 0;
   uint32_t n_nan = 0, n_inf = 0, n_zero = 0, n_fin = 0;
+  uint32_t n_usual = 0;  // usual steps (uniform): V finite elements per lane each
   float mn = __builtin_inff(), mx = -__builtin_inff();
-  uint32_t imn = 0xffffffffu, imx = 0xffffffffu;  // offsets from c0
+  uint32_t imn = kNoOff, imx = kNoOff;  // offsets from c0
   double sm = 0.0, sq = 0.0, sa = 0.0;
   // the wave's extremes so far (uniform; +inf / -inf before any finite
   // element)
   float wmn = __builtin_inff(), wmx = -__builtin_inff();
-  for (uint64_t b = w0; b < w1; b += ITER) {
-    const uint64_t i0 = b + (uint64_t)lane * V;
-    const bool full = vec && b + ITER <= w1;
-    const p32x4 q = full ? pload16(T.data + i0 * ES) : pload_guarded<DT>(T.data, i0, w1);
-    const uint32_t o0 = (uint32_t)(i0 - c0);
-    if (full) {
-      // Usual step: every element finite (an exponent field of all ones
-      // carries into the sign bit when its lowest bit is added). It adds to
-      // the sums, counts and histogram with no branch per element (a zero is
-      // counted in the row's spare byte, bin kHistBins). When no element lies
-      // beyond the wave's extremes no lane's first minimum or maximum can
-      // change (an element equal to an extreme comes after it); otherwise the
-      // lanes take their new extremes by selects, in index order, and the
-      // wave's extremes are raised.
+  // Usual step: every element finite (and all below w1). Binary16 screens
+  // on the packed halves with the NaN-propagating minimum and maximum
+  // (v_pk_minimum3_f16 / v_pk_maximum3_f16; -0 orders below +0, which no
+  // comparison below can tell apart): a NaN or an infinity among the
+  // elements shows in the step's smallest or largest value, which the step
+  // keeps for its extremes screen. The other types test the packed words: an
+  // exponent field of all ones carries into the sign bit when its lowest
+  // bit is added.
+  typedef _Float16 ph2 __attribute__((ext_vector_type(2)));
+  auto is_usual = [&](const p32x4 &q, float &smn, float &smx) {
+    if constexpr (DT == VC_F16) {
+      // (each word is copied to a scalar before the cast: a cast of the
+      // vector element itself reads the vector's first word)
+      const uint32_t u0 = q[0], u1 = q[1], u2 = q[2], u3 = q[3];
+      const ph2 h0 = __builtin_bit_cast(ph2, u0), h1 = __builtin_bit_cast(ph2, u1);
+      const ph2 h2 = __builtin_bit_cast(ph2, u2), h3 = __builtin_bit_cast(ph2, u3);
+      const ph2 lo = __builtin_elementwise_minimum(__builtin_elementwise_minimum(h0, h1),
+                                                   __builtin_elementwise_minimum(h2, h3));
+      const ph2 hi = __builtin_elementwise_maximum(__builtin_elementwise_maximum(h0, h1),
+                                                   __builtin_elementwise_maximum(h2, h3));
+      smn = (float)__builtin_elementwise_minimum(lo[0], lo[1]);
+      smx = (float)__builtin_elementwise_maximum(hi[0], hi[1]);
+      return __ballot(!(smn >= -65504.0f && smx <= 65504.0f)) == 0;
+    } else {
       constexpr uint32_t kMag = DT == VC_F32 ? 0x7fffffffu : 0x7fff7fffu;
       constexpr uint32_t kTop = DT == VC_F32 ? 0x80000000u : 0x80008000u;
-      constexpr uint32_t kCarry =
-          DT == VC_F32 ? 0x00800000u : (DT == VC_BF16 ? 0x00800080u : 0x04000400u);
+      constexpr uint32_t kCarry = DT == VC_F32 ? 0x00800000u : 0x00800080u;
       uint32_t nf = 0;
 #pragma unroll
       for (int w = 0; w < 4; ++w) nf |= (q[w] & kMag) + kCarry;
-      if (__ballot((nf & kTop) != 0) == 0) {
-        float x[V];
-        float smn, smx;
+      return __ballot((nf & kTop) != 0) == 0;
+    }
+  };
+  // A usual step adds to the sums, counts and histogram with no branch per
+  // element (a zero is counted in the zero slot). When no element lies
+  // beyond the wave's extremes no lane's first minimum or maximum can change
+  // (an element equal to an extreme comes after it); otherwise the lanes
+  // take their new extremes by selects, in index order, and the wave's
+  // extremes are raised.
+  auto usual_step = [&](const p32x4 &q, uint32_t o0, float smn, float smx) {
+    float x[V];
 #pragma unroll
-        for (int j = 0; j < V; ++j) x[j] = pdec<DT>(q, j);
-        n_fin += V;
-        if constexpr (DT == VC_F16) {
-          // Binary16: the extremes are screened on the packed halves, and
-          // the step's sums are formed in binary32 before one binary64
-          // addition per sum. A product of two binary16 values is exact in
-          // binary32 and every partial sum stays inside its range, so a
-          // step's sum of 8 terms errs by at most 7 * 2^-24 of the sum of
-          // the terms' magnitudes. Bins: binary16 exponents (subnormals
-          // included, through the exact binary32 value) lie inside the
-          // histogram's range, so no clamping.
-          typedef _Float16 ph2 __attribute__((ext_vector_type(2)));
-          // (each word is copied to a scalar before the cast: a cast of the
-          // vector element itself reads the vector's first word)
-          const uint32_t w0 = q[0];
-          ph2 lo = __builtin_bit_cast(ph2, w0), hi = lo;
+    for (int j = 0; j < V; ++j) x[j] = pdec<DT>(q, j);
+    ++n_usual;
+    if constexpr (DT == VC_F16) {
+      // Binary16: the step's sums are formed in binary32 before one
+      // binary64 addition per sum. A product of two binary16 values is exact in
+      // binary32 and every partial sum stays inside its range, so a
+      // step's sum of 8 terms errs by at most 7 * 2^-24 of the sum of
+      // the terms' magnitudes. Bins: binary16 exponents (subnormals
+      // included, through the exact binary32 value) lie inside the
+      // histogram's range, so no clamping; a zero (field 0) is raised
+      // to field kF16ZeroField, the zero slot.
+      // counter of exponent field e: col_f[64 e] (fields 102 .. 142)
+      uint32_t *const col_f = col - 64 * (127 + kHistEmin - 1);
+      float f1 = x[0], f2 = 0.0f, f3 = 0.0f;
 #pragma unroll
-          for (int w = 1; w < 4; ++w) {
-            const uint32_t wv = q[w];
-            const ph2 h = __builtin_bit_cast(ph2, wv);
-            lo = __builtin_elementwise_min(lo, h);
-            hi = __builtin_elementwise_max(hi, h);
-          }
-          smn = __builtin_fminf((float)lo[0], (float)lo[1]);
-          smx = __builtin_fmaxf((float)hi[0], (float)hi[1]);
-          float f1 = 0.0f, f2 = 0.0f, f3 = 0.0f;
+      for (int j = 0; j < V; ++j) {
+        if (j > 0) f1 += x[j];
+        f2 = __builtin_fmaf(x[j], x[j], f2);
+        f3 += __builtin_fabsf(x[j]);
+        const uint32_t e = max((__float_as_uint(x[j]) >> 23) & 0xffu, kF16ZeroField);
+        atomicAdd(col_f + 64 * e, 1u);
+      }
+      sm += (double)f1;
+      sq += (double)f2;
+      sa += (double)f3;
+    } else {
+      smn = __builtin_inff();
+      smx = -__builtin_inff();
 #pragma unroll
-          for (int j = 0; j < V; ++j) {
-            f1 += x[j];
-            f2 = __builtin_fmaf(x[j], x[j], f2);
-            f3 += __builtin_fabsf(x[j]);
-            const int e = (int)((__float_as_uint(x[j]) >> 23) & 0xffu);
-            const int bin = x[j] == 0.0f ? kHistBins : e - 127 - kHistEmin + 1;
-            atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
-          }
-          sm += (double)f1;
-          sq += (double)f2;
-          sa += (double)f3;
-        } else {
-          smn = __builtin_inff();
-          smx = -__builtin_inff();
-#pragma unroll
-          for (int j = 0; j < V; ++j) {
-            smn = __builtin_fminf(smn, x[j]);
-            smx = __builtin_fmaxf(smx, x[j]);
-            const double xd = (double)x[j];
-            sm += xd;
-            sq = __builtin_fma(xd, xd, sq);
-            sa += __builtin_fabs(xd);
-            const int e = (int)((__float_as_uint(x[j]) >> 23) & 0xffu);
-            const int bin =
-                x[j] == 0.0f ? kHistBins : min(max(e - 127 - kHistEmin + 1, 0), kHistBins - 1);
-            atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
-          }
-        }
-        if (__ballot(smn < wmn || smx > wmx) != 0) {
-          // every element is finite: the first one beats the lane's +inf /
-          // -inf start, so no "no extreme yet" test is needed
-#pragma unroll
-          for (int j = 0; j < V; ++j) {
-            const bool lo = x[j] < mn, hi = x[j] > mx;
-            mn = lo ? x[j] : mn;
-            imn = lo ? o0 + (uint32_t)j : imn;
-            mx = hi ? x[j] : mx;
-            imx = hi ? o0 + (uint32_t)j : imx;
-          }
-          wmn = wave_ext<false>(mn);
-          wmx = wave_ext<true>(mx);
-        }
-        continue;
+      for (int j = 0; j < V; ++j) {
+        smn = __builtin_fminf(smn, x[j]);
+        smx = __builtin_fmaxf(smx, x[j]);
+        const double xd = (double)x[j];
+        sm += xd;
+        sq = __builtin_fma(xd, xd, sq);
+        sa += __builtin_fabs(xd);
+        const int e = (int)((__float_as_uint(x[j]) >> 23) & 0xffu);
+        const int bin =
+            x[j] == 0.0f ? kHistBins : min(max(e - 127 - kHistEmin + 1, 0), kHistBins - 1);
+        atomicAdd(col + 64 * bin, 1u);
       }
     }
+    if (__ballot(smn < wmn || smx > wmx) != 0) {
+      // every element is finite: the first one beats the lane's +inf /
+      // -inf start, so no "no extreme yet" test is needed
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const bool lo = x[j] < mn, hi = x[j] > mx;
+        mn = lo ? x[j] : mn;
+        imn = lo ? o0 + (uint32_t)j : imn;
+        mx = hi ? x[j] : mx;
+        imx = hi ? o0 + (uint32_t)j : imx;
+      }
+      wmn = wave_ext<false>(mn);
+      wmx = wave_ext<true>(mx);
+    }
+  };
+  // Any other step, element by element (elements from w1 on are skipped).
+  const uint32_t ow1 = (uint32_t)(w1 - c0);
+  auto elem_step = [&](const p32x4 &q, uint32_t o0) {
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-      if (i0 + j >= w1) break;
+      if (o0 + (uint32_t)j >= ow1) break;
       const float x = pdec<DT>(q, j);
       const bool isn = x != x;
       const bool isi = __builtin_fabsf(x) == __builtin_inff();
@@ -458,11 +508,11 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
       if (isn || isi) continue;
       ++n_fin;
       const uint32_t o = o0 + (uint32_t)j;
-      if (x < mn || imn == 0xffffffffu) {
+      if (x < mn || imn == kNoOff) {
         mn = x;
         imn = o;
       }
-      if (x > mx || imx == 0xffffffffu) {
+      if (x > mx || imx == kNoOff) {
         mx = x;
         imx = o;
       }
@@ -475,66 +525,98 @@ __device__ void probe_chunk(ProbeLds &s, const ProbeTensor &T, uint64_t c0, uint
       } else {
         const uint32_t e = (__float_as_uint(x) >> 23) & 0xffu;
         const int bin = e == 0 ? 0 : min(max((int)e - 127 - kHistEmin + 1, 0), kHistBins - 1);
-        atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+        atomicAdd(col + 64 * bin, 1u);
       }
     }
     // raise the wave's extremes to the lanes' (lanes with no finite element
     // hold +inf / -inf)
     wmn = wave_ext<false>(mn);
     wmx = wave_ext<true>(mx);
+  };
+  // The full steps through a buffer resource over them (a wave's range is
+  // at most 128 KiB: 32-bit offsets, uniform ones in scalar registers),
+  // each step's loads issued one step ahead (the last step loads itself
+  // again: no branch for it). Runs of usual steps take an inner loop of
+  // their own.
+  const uint32_t nst = vec ? (uint32_t)((w1 - w0) / ITER) : 0u;
+  if (nst > 0) {
+    constexpr uint32_t SB = ITER * ES;  // bytes per step
+    const uint32_t last = (nst - 1) * SB;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(T.data + w0 * ES), (short)0, (int)(nst * SB), kBufferWord3);
+    const uint32_t loff = lane * 16u;                           // lane's bytes in a step
+    const uint32_t ol = (uint32_t)(w0 - c0) + lane * (uint32_t)V;  // lane's first offset
+    uint32_t k = 0;  // the step's first byte
+    p32x4 qn = bload16(rs, loff, 0u);
+    while (true) {
+      p32x4 q = qn;
+      qn = bload16(rs, loff, min(k + SB, last));
+      float smn = 0.0f, smx = 0.0f;  // (binary16: set by the screen)
+      bool usual = is_usual(q, smn, smx);
+      while (usual) {
+        usual_step(q, ol + k / ES, smn, smx);
+        k += SB;
+        if (k > last) break;
+        q = qn;
+        qn = bload16(rs, loff, min(k + SB, last));
+        usual = is_usual(q, smn, smx);
+      }
+      if (usual) break;  // (past the last step)
+      elem_step(q, ol + k / ES);
+      k += SB;
+      if (k > last) break;
+    }
   }
-  n_zero += row[kRowWords - 1] & 0xffu;  // zeros of the usual steps
-  // histogram: thread t sums bin t % 64 over the rows of lanes
-  // (t / 64) * 64 .. + 63, then the four partial sums are added in order
-  __syncthreads();
-  const uint32_t bin = t & 63u, part = t >> 6;
-  uint32_t h = 0;
-  for (uint32_t l = part * 64; l < part * 64 + 64; ++l)
-    h += (s.hist[l * kRowWords + (bin >> 2)] >> ((bin & 3) * 8)) & 0xffu;
-  __syncthreads();  // the rows are dead from here: the partials reuse them
-  s.c[0][t] = h;
-  __syncthreads();
-  if (t < (uint32_t)kHistBins)
-    rec->hist[t] = (uint32_t)(s.c[0][t] + s.c[0][t + 64] + s.c[0][t + 128] + s.c[0][t + 192]);
-  __syncthreads();
-  s.c[0][t] = n_nan;
-  s.c[1][t] = n_inf;
-  s.c[2][t] = n_zero;
-  s.c[3][t] = n_fin;
+  for (uint64_t b = w0 + (uint64_t)nst * ITER; b < w1; b += ITER) {
+    const uint64_t i0 = b + (uint64_t)lane * V;
+    const p32x4 q = pload_guarded<DT>(T.data, i0, w1);
+    elem_step(q, (uint32_t)(i0 - c0));
+  }
+  n_fin += V * n_usual;
+  __syncthreads();  // every wave's counts are in
+  // zeros of the usual steps: wave 0 adds the zero slot's column
+  constexpr uint32_t kZeroSlot = DT == VC_F16 ? kF16ZeroBin : (uint32_t)kHistBins;
+  if (wave == 0) n_zero += col[64 * kZeroSlot];
+  // histogram: thread t sums the columns 16 q .. 16 q + 15 of bin t / 4
+  // (q = t % 4), and a quad's four sums are added by DPP (integer sums:
+  // any order gives the same total)
+  {
+    const uint32_t bin = t >> 2;
+    const p32x4 *src = (const p32x4 *)(s.hist + 64 * bin + 16 * (t & 3u));
+    uint32_t h = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const p32x4 v = src[k];
+      h += (v[0] + v[1]) + (v[2] + v[3]);
+    }
+    h += __builtin_amdgcn_update_dpp(0u, h, 0xb1, 0xf, 0xf, false);  // quad_perm 1,0,3,2
+    h += __builtin_amdgcn_update_dpp(0u, h, 0x4e, 0xf, 0xf, false);  // quad_perm 2,3,0,1
+    if ((t & 3u) == 0) rec->hist[bin] = DT == VC_F16 && bin == kF16ZeroBin ? 0u : h;
+  }
+  __syncthreads();  // the columns are dead from here: the partials reuse them
+  s.n[0][t] = n_nan;
+  s.n[1][t] = n_inf;
+  s.n[2][t] = n_zero;
+  s.n[3][t] = n_fin;
   s.d[0][t] = sm;
   s.d[1][t] = sq;
   s.d[2][t] = sa;
-  s.mv[0][t] = mn;
-  s.mi[0][t] = imn == 0xffffffffu ? -1 : (int64_t)(c0 + imn);
-  s.mv[1][t] = mx;
-  s.mi[1][t] = imx == 0xffffffffu ? -1 : (int64_t)(c0 + imx);
-  ProbeRec r;
-  block_reduce_tree(s, r);
-  if (t == 0) {
-    rec->nan = r.nan;
-    rec->inf = r.inf;
-    rec->zero = r.zero;
-    rec->fin = r.fin;
-    rec->argmin = r.argmin;
-    rec->argmax = r.argmax;
-    rec->min = r.min;
-    rec->max = r.max;
-    rec->sum = r.sum;
-    rec->sum_sq = r.sum_sq;
-    rec->sum_abs = r.sum_abs;
-    rec->pad[0] = 0;
-  }
+  s.v[0][t] = mn;
+  s.o[0][t] = imn;
+  s.v[1][t] = mx;
+  s.o[1][t] = imx;
+  chunk_reduce(s, c0, rec);
 }
 
 __global__ __launch_bounds__(kPThreads) void probe_kernel(const ProbeParams P) {
-  __shared__ ProbeLds s;
+  __shared__ ChunkLds s;
   const uint64_t chunk = blockIdx.x;
   if (threadIdx.x < 64) {
     const uint32_t ti = find_first(P.chunk_first, (uint32_t)P.n_tensors, chunk);
     if (threadIdx.x == 0) s.tensor = ti;
   }
   __syncthreads();
-  const ProbeTensor T = P.tensors[s.tensor];
+  const ProbeTensor T = P.tensors[__builtin_amdgcn_readfirstlane(s.tensor)];
   const uint64_t CH = 4ull * P.unit;
   const uint64_t c0 = (chunk - T.chunk_begin) * CH;
   const uint64_t c1 = min(c0 + CH, T.numel);
@@ -746,7 +828,7 @@ __device__ void np_reduce(NpLds &s, NpRec &r) {
 }
 
 // Fixed-order tree reduction of the partials in s into r (valid in thread
-// 0), for the end of a streaming chunk (as block_reduce_tree).
+// 0), for the end of a streaming chunk (as chunk_reduce for the probe).
 __device__ void np_reduce_tree(NpLds &s, NpRec &r) {
   const uint32_t t = threadIdx.x;
   for (uint32_t w = kPThreads / 2; w >= 1; w >>= 1) {

@@ -112,3 +112,34 @@ def test_probe_extreme_magnitudes():
         want = oracle.tensor_stats(raw.view(np.float32) if dt == oracle.F32 else raw, dt)
         _check(got, want, "extreme %d" % i)
         assert got["sum_sq"] > 0.0
+
+
+def test_probe_largest_unit():
+    """A batch of 2^29 elements takes the largest wave range (32768 elements:
+    64 full steps per wave through the inner usual-step loop) and chunks of
+    131072 elements; each tensor of 2^27 elements spans four merge groups.
+    Late strict extremes, their ties, zeros of both signs, binary16
+    subnormals, NaN and Inf sit in every tensor."""
+    import torch
+
+    rng = np.random.default_rng(2608_63)
+    n = 1 << 27
+    batch = []
+    for dt in (oracle.F16, oracle.F16, oracle.BF16, oracle.F32):
+        x = rng.standard_normal(n, dtype=np.float32)
+        x[rng.choice(n, n // 50, replace=False)] = 0.0
+        x[rng.choice(n, 1000, replace=False)] = -0.0
+        x[rng.choice(n, 1000, replace=False)] = 3e-7  # binary16 subnormal
+        lo, hi = n - 5 * 131072 + 77, n - 3 * 131072 + 12345
+        x[[lo, hi]] = [-50.0, 60.0]          # strict extremes late in a chunk
+        x[[lo + 4096, hi + 9]] = [-50.0, 60.0]  # their ties: the first index wins
+        x[[17, n // 3, n - 1]] = [np.nan, np.inf, np.nan]
+        raw = x.view(np.uint32).copy() if dt == oracle.F32 else oracle_pins.to_raw16(x, dt)
+        batch.append((raw, dt))
+    print("probe largest unit: %d tensors of %d elements" % (len(batch), n), flush=True)
+    tensors = [_raw_to_tensor(torch, raw, dt).cuda() for raw, dt in batch]
+    res = vc.vcheck_tensor_stats(tensors)
+    for i, ((raw, dt), got) in enumerate(zip(batch, res)):
+        want = oracle.tensor_stats(raw.view(np.float32) if dt == oracle.F32 else raw, dt)
+        _check(got, want, "large tensor %d" % i)
+        assert (got["argmin"], got["argmax"]) == (n - 5 * 131072 + 77, n - 3 * 131072 + 12345)

@@ -5,7 +5,7 @@ events that must leave those paths planted late in a wave's range.
 Probe: a strict new minimum and maximum after many usual steps (each in a
 later element of its step), ties of both extremes after them (the first
 index must win), zeros of both signs
-throughout (counted on the usual path in a spare histogram byte), binary16
+throughout (counted on the usual path in the histogram's zero slot), binary16
 subnormals and one late NaN.
 
 Near-pass: pairs well inside the tolerance, with late failures, a late new
