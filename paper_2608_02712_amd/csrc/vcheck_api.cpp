@@ -682,16 +682,15 @@ struct ProbePlan {
 };
 
 // Elements per wave of the probe, the content hash and the near-pass
-// statistics: a power of two between 1 Ki and cap, about 16K waves over the
-// batch, and at least what keeps every tensor within 256 groups of 256
-// chunks. The probe's 32-bit histogram counters allow cap = 32 Ki (the
-// chunk offsets stay 32-bit); the near-pass kernel's 8-bit counters allow
-// 8 Ki (a lane counts at most cap / 64 elements).
-constexpr uint64_t kProbeUnitMax = 32768, kNearpassUnitMax = 8192;
-uint32_t probe_unit(uint64_t total, uint64_t largest, uint64_t cap) {
+// statistics: a power of two between 1 Ki and 32 Ki (a wave's range stays
+// within 128 KiB: 32-bit offsets; the histogram counters are 32-bit), about
+// 16K waves over the batch, and at least what keeps every tensor within 256
+// groups of 256 chunks.
+uint32_t probe_unit(uint64_t total, uint64_t largest) {
+  constexpr uint64_t kCap = 32768;
   uint64_t u = 1024;
-  while (u < cap && u * 2 * VCK_WAVE_TARGET <= total) u *= 2;
-  while (u < cap && 4 * u * vck::kProbeGroupChunks * vck::kProbeGroupChunks < largest) u *= 2;
+  while (u < kCap && u * 2 * VCK_WAVE_TARGET <= total) u *= 2;
+  while (u < kCap && 4 * u * vck::kProbeGroupChunks * vck::kProbeGroupChunks < largest) u *= 2;
   return (uint32_t)u;
 }
 
@@ -710,7 +709,7 @@ vc_status make_probe_plan(const vc_tensor *tensors, int32_t n, ProbePlan &plan) 
     total += m;
     largest = std::max(largest, m);
   }
-  plan.unit = probe_unit(total, largest, kProbeUnitMax);
+  plan.unit = probe_unit(total, largest);
   const uint64_t ch = 4ull * plan.unit;
   plan.tensors.resize(n);
   plan.chunk_first.resize(n);
@@ -825,7 +824,7 @@ vc_status make_np_plan(const vc_case *cases, int32_t n, NpPlan &plan) {
     total += m;
     largest = std::max(largest, m);
   }
-  plan.unit = probe_unit(total, largest, kNearpassUnitMax);
+  plan.unit = probe_unit(total, largest);
   const uint64_t ch = 4ull * plan.unit;
   plan.cases.resize(n);
   plan.chunk_first.resize(n);

@@ -45,6 +45,7 @@ static_assert(kF16ZeroBin == 16, "bin of 2^-25");
 #define PRB_GLOBAL __attribute__((address_space(1)))
 
 typedef uint32_t p32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 ph2 __attribute__((ext_vector_type(2)));  // a word's two binary16 values
 
 __device__ __forceinline__ p32x4 pload16(const uint8_t *p) {
   return __builtin_nontemporal_load((const PRB_GLOBAL p32x4 *)(p));
@@ -403,7 +404,6 @@ __device__ void probe_chunk(ChunkLds &s, const ProbeTensor &T, uint64_t c0, uint
   // keeps for its extremes screen. The other types test the packed words: an
   // exponent field of all ones carries into the sign bit when its lowest
   // bit is added.
-  typedef _Float16 ph2 __attribute__((ext_vector_type(2)));
   auto is_usual = [&](const p32x4 &q, float &smn, float &smx) {
     if constexpr (DT == VC_F16) {
       // (each word is copied to a scalar before the cast: a cast of the
@@ -759,18 +759,34 @@ __global__ __launch_bounds__(kPThreads) void probe_final_kernel(const ProbeParam
 // ratio beats the threshold (fma(-T, t, d) > 0, whose sign is exact), so the
 // binary64 division runs for candidates and failing elements only.
 
-constexpr int kNpRowWords = 15;  // 52 8-bit counters (50 used) and a pad word: an odd stride
+// Histogram slots: the ratio bins, then the grid-distance bins.
+constexpr int kNpSlots = kRatioBins + kUlpBins;
 
-struct NpLds {
+// LDS of the near-pass streaming kernel: the histogram columns while
+// streaming (as the probe's: 32-bit counters, slot-major, one column per
+// lane position that the block's waves share), the per-thread partials of
+// the chunk afterwards (32-bit counts and offsets from the chunk's first
+// element).
+struct alignas(16) NpChunkLds {
   union {
-    uint32_t hist[kPWaves * 64 * kNpRowWords];
+    uint32_t hist[kNpSlots * 64];
     struct {
-      uint64_t c[3][kPThreads];
+      uint32_t c[3][kPThreads];
       double mv[kPThreads];
-      int64_t mi[kPThreads];
+      uint32_t mo[kPThreads];
       uint32_t mu[kPThreads];
     };
   };
+  uint32_t item;
+};
+
+// LDS of the near-pass merge launches.
+struct NpLds {
+  // per-thread partials
+  uint64_t c[3][kPThreads];
+  double mv[kPThreads];
+  int64_t mi[kPThreads];
+  uint32_t mu[kPThreads];
   // per-wave totals of np_reduce
   uint64_t wc[3][kPWaves];
   double wv[kPWaves];
@@ -827,27 +843,38 @@ __device__ void np_reduce(NpLds &s, NpRec &r) {
   }
 }
 
-// Fixed-order tree reduction of the partials in s into r (valid in thread
-// 0), for the end of a streaming chunk (as chunk_reduce for the probe).
-__device__ void np_reduce_tree(NpLds &s, NpRec &r) {
+// Fixed-order tree reduction of the per-thread partials of the chunk that
+// starts at element c0 into its record, written by thread 0 (as the probe's
+// chunk_reduce): the largest ratio keeps the smaller offset among equal
+// values.
+__device__ void np_chunk_reduce(NpChunkLds &s, uint64_t c0, NpRec *rec) {
   const uint32_t t = threadIdx.x;
   for (uint32_t w = kPThreads / 2; w >= 1; w >>= 1) {
     __syncthreads();
     if (t < w) {
 #pragma unroll
       for (int f = 0; f < 3; ++f) s.c[f][t] += s.c[f][t + w];
-      np_pick(s.mv[t], s.mi[t], s.mv[t + w], s.mi[t + w]);
+      const uint32_t o2 = s.mo[t + w];
+      if (o2 != kNoOff) {
+        const double v = s.mv[t], v2 = s.mv[t + w];
+        const uint32_t o = s.mo[t];
+        if (o == kNoOff || v2 > v || (v2 == v && o2 < o)) {
+          s.mv[t] = v2;
+          s.mo[t] = o2;
+        }
+      }
       s.mu[t] = max(s.mu[t], s.mu[t + w]);
     }
   }
   __syncthreads();
   if (t == 0) {
-    r.n_pairs = s.c[0][0];
-    r.n_fail = s.c[1][0];
-    r.n_zero_tol = s.c[2][0];
-    r.argmax_ratio = s.mi[0];
-    r.max_ratio = s.mi[0] < 0 ? 0.0 : s.mv[0];
-    r.max_ulp_fail = s.mu[0];
+    rec->n_pairs = s.c[0][0];
+    rec->n_fail = s.c[1][0];
+    rec->n_zero_tol = s.c[2][0];
+    rec->argmax_ratio = s.mo[0] == kNoOff ? -1 : (int64_t)(c0 + s.mo[0]);
+    rec->max_ratio = s.mo[0] == kNoOff ? 0.0 : s.mv[0];
+    rec->max_ulp_fail = s.mu[0];
+    rec->pad0 = 0;
   }
 }
 
@@ -872,8 +899,25 @@ __device__ __forceinline__ uint32_t grid_bits(const p32x4 &q, int j) {
   }
 }
 
+// Grid distances of the two 16-bit patterns of a word pair, per 16-bit half:
+// the patterns become ordered keys (0x8000 + m for +m, 0x8000 - m for -m:
+// both zeros map to 0x8000; a finite binary16 or bfloat16 magnitude is at
+// most 0x7f7f, so a key fits 16 bits), and the distance is the larger key
+// minus the smaller (packed 16-bit operations).
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+typedef int16_t i16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t grid_key2(uint32_t w) {
+  const uint32_t sg = __builtin_bit_cast(uint32_t, __builtin_bit_cast(i16x2, w) >> (int16_t)15);
+  const u16x2 x = __builtin_bit_cast(u16x2, w ^ (sg | 0x80008000u));
+  return __builtin_bit_cast(uint32_t, x - __builtin_bit_cast(u16x2, sg));
+}
+__device__ __forceinline__ uint32_t grid_dist2(uint32_t c, uint32_t r) {
+  const u16x2 x = __builtin_bit_cast(u16x2, grid_key2(c)), y = __builtin_bit_cast(u16x2, grid_key2(r));
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(x, y) - __builtin_elementwise_min(x, y));
+}
+
 template <int DT>
-__device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, uint32_t U,
+__device__ void np_chunk(NpChunkLds &s, const NpCase &C, uint64_t c0, uint64_t c1, uint32_t U,
                          double atol, double rtol, NpRec *rec) {
   constexpr int V = DT == VC_F32 ? 4 : 8;
   constexpr int ES = DT == VC_F32 ? 4 : 2;
@@ -881,11 +925,15 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
   constexpr uint32_t kExpMask = DT == VC_BF16 ? 0x7f80u : 0x7c00u;
   const uint32_t t = threadIdx.x, lane = t & 63u;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  uint32_t *const row = s.hist + t * kNpRowWords;
-  for (int w = 0; w < kNpRowWords; ++w) row[w] = 0;
+  for (uint32_t w = t; w < (uint32_t)(kNpSlots * 64); w += kPThreads) s.hist[w] = 0;
+  __syncthreads();
+  // lane's column; col[64 * b] is its counter of slot b
+  uint32_t *const col = s.hist + lane;
   const uint64_t w0 = min(c0 + (uint64_t)wave * U, c1), w1 = min(w0 + U, c1);
+  const uint32_t ow1 = (uint32_t)(w1 - c0);
   const bool vec = ((uintptr_t)C.cand % 16) == 0 && ((uintptr_t)C.ref % 16) == 0;
   uint32_t n_pairs = 0, n_fail = 0, n_zt = 0, mu = 0;
+  uint32_t n_usual = 0;  // usual steps (uniform): V finite pairs per lane each
   double lb = -1.0, T = -1.0;  // lane best ratio, wave threshold (-1: none)
   // Binary32 screen of the usual step. alo, rlo: the pair lowered by 2^-20
   // and rounded down, so fma(|r|, rlo, alo) <= atol + rtol |r| = t despite
@@ -895,67 +943,93 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
   // storage unless the exponents lie far apart; gradual underflow keeps a
   // subnormal difference of binary32 values exact or within that bound), so
   // |c - r|32 * (1 + 2^-21) <= tm * fma(|r|, rlo, alo) proves d <= t and
-  // d <= T t: the pair neither fails nor beats the largest ratio.
+  // d <= T t: the pair neither fails nor beats the largest ratio. A NaN or
+  // an infinity in either value makes the test fail (the comparison with 0
+  // of a NaN is false; an infinite difference exceeds a finite bound, and an
+  // infinite bound comes with an infinite difference: inf - inf is NaN), so
+  // a step that passes it holds finite pairs only.
   const float alo = np_f32_below(atol - atol * 0x1p-20);
   const float rlo = np_f32_below(rtol - rtol * 0x1p-20);
   constexpr float kDUp = 1.0f + 0x1p-21f;
   float tm = 0.0f;
-  uint32_t li = 0xffffffffu;
-  for (uint64_t b = w0; b < w1; b += ITER) {
-    const uint64_t i0 = b + (uint64_t)lane * V;
-    const bool full = vec && b + ITER <= w1;
-    const p32x4 cq = full ? pload16(C.cand + i0 * ES) : pload_guarded<DT>(C.cand, i0, w1);
-    const p32x4 rq = full ? pload16(C.ref + i0 * ES) : pload_guarded<DT>(C.ref, i0, w1);
-    const uint32_t o0 = (uint32_t)(i0 - c0);
-    {
-      // Usual step: every pair finite, nothing failing and no candidate for
-      // the largest ratio (T >= 0 and d - T t <= 0, an exact sign). It only
-      // counts its pairs and their grid distances, in one pass with no exit:
-      // a key's magnitude and sign are the grid pattern's, so equal signs
-      // give |hc - hr| and opposite signs the sum of the magnitudes.
-      if (full && T >= 0.0) {
-        // a value is not finite when its exponent field is all ones: adding
-        // the field's lowest bit then carries into the sign bit
-        constexpr uint32_t kMag = DT == VC_F32 ? 0x7fffffffu : 0x7fff7fffu;
-        constexpr uint32_t kTop = DT == VC_F32 ? 0x80000000u : 0x80008000u;
-        constexpr uint32_t kCarry =
-            DT == VC_F32 ? 0x00800000u : (DT == VC_BF16 ? 0x00800080u : 0x04000400u);
-        uint32_t nf = 0;
+  // Binary16 storage screens with the difference taken in binary16 (packed:
+  // it is within a relative 2^-11 of c - r, exact when small, and a NaN or an
+  // infinity when either value is one or the difference leaves the range)
+  // and min(1, T) folded into the lowered pair: am = m atol and rm = m rtol,
+  // m = min(1, T), each lowered by 2^-20 and rounded down, so
+  // fma(|r|, rm, am) < m t; then |c - r|16 * (1 + 2^-10) <= fma(|r|, rm, am)
+  // proves |c - r| < m t. (A binary16 difference that is not zero is at
+  // least 2^-24, so a bound that rounds in the subnormal range cannot pass a
+  // non-zero difference.)
+  constexpr float kDUp16 = 1.0f + 0x1p-10f;
+  float am = 0.0f, rm = 0.0f;
+  uint32_t li = kNoOff;
+  // Usual step (T >= 0, every pair passes the screen): it only counts its
+  // pairs and their grid distances, with no exit.
+  // (the step's largest test value, by the NaN-propagating maximum, so one
+  // comparison decides; c - r as an fma with 1, which takes 16-bit operands
+  // as they are)
+  auto is_usual = [&](const p32x4 &cq, const p32x4 &rq) {
+    float m = -__builtin_inff();
+    if constexpr (DT == VC_F16) {
 #pragma unroll
-        for (int w = 0; w < 4; ++w) nf |= ((cq[w] & kMag) + kCarry) | ((rq[w] & kMag) + kCarry);
-        bool other = (nf & kTop) != 0;
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t cw = cq[w], rw = rq[w];
+        const ph2 ch = __builtin_bit_cast(ph2, cw), rh = __builtin_bit_cast(ph2, rw);
+        const ph2 dh = ch - rh;
 #pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const float rf = pdec<DT>(rq, j);
-          const float d = __builtin_fabsf(pdec<DT>(cq, j) - rf);
-          const float tl = __builtin_fmaf(__builtin_fabsf(rf), rlo, alo);
-          // (not <= catches NaN, from an infinite tl times tm = 0)
-          other |= !(__builtin_fmaf(d, kDUp, -(tm * tl)) <= 0.0f);
-        }
-        if (__ballot(other) == 0) {
-          n_pairs += V;
-#pragma unroll
-          for (int j = 0; j < V; ++j) {
-            const uint32_t hc = grid_bits<DT>(cq, j), hr = grid_bits<DT>(rq, j);
-            const uint32_t dist = ((hc ^ hr) & 0x8000u) ? (hc & 0x7fffu) + (hr & 0x7fffu)
-                                                        : (uint32_t)abs((int)hc - (int)hr);
-            int ubin = kRatioBins + 31 - __builtin_clz(2u * dist + 1u);
-            // binary32 values beyond the binary16 range sit outside the grid
-            if constexpr (DT == VC_F32)
-              ubin = ((hc & kExpMask) == kExpMask || (hr & kExpMask) == kExpMask)
-                         ? kRatioBins + kUlpBins - 1
-                         : ubin;
-            atomicAdd(row + (ubin >> 2), 1u << ((ubin & 3) * 8));
-          }
-          continue;
+        for (int h = 0; h < 2; ++h) {
+          const float tl = __builtin_fmaf(__builtin_fabsf((float)rh[h]), rm, am);
+          m = __builtin_elementwise_maximum(
+              m, __builtin_fmaf(__builtin_fabsf((float)dh[h]), kDUp16, -tl));
         }
       }
+    } else {
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float rf = pdec<DT>(rq, j);
+        const float d = __builtin_fabsf(pdec<DT>(cq, j) - rf);
+        const float tl = __builtin_fmaf(__builtin_fabsf(rf), rlo, alo);
+        m = __builtin_elementwise_maximum(m, __builtin_fmaf(d, kDUp, -(tm * tl)));
+      }
     }
+    return __ballot(!(m <= 0.0f)) == 0;
+  };
+  // Grid-distance bin of a usual pair, slot kRatioBins + bit length of the
+  // distance (0 for equal patterns): for 16-bit storage the distances of a
+  // word's two pairs come packed, and a half's bit length is 16 minus the
+  // leading zeros of the half placed above a set bit 15.
+  uint32_t *const col_u = col + 64 * (kRatioBins + 16);
+  auto usual_step = [&](const p32x4 &cq, const p32x4 &rq) {
+    ++n_usual;
+    if constexpr (DT != VC_F32) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t d = grid_dist2(cq[w], rq[w]);
+        atomicAdd(col_u - 64 * __builtin_clz((d << 16) | 0x8000u), 1u);
+        atomicAdd(col_u - 64 * __builtin_clz(d | 0x8000u), 1u);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const uint32_t hc = grid_bits<DT>(cq, j), hr = grid_bits<DT>(rq, j);
+        const uint32_t dist = ((hc ^ hr) & 0x8000u) ? (hc & 0x7fffu) + (hr & 0x7fffu)
+                                                    : (uint32_t)abs((int)hc - (int)hr);
+        // binary32 values beyond the binary16 range sit outside the grid
+        const int ubin = ((hc & kExpMask) == kExpMask || (hr & kExpMask) == kExpMask)
+                             ? kRatioBins + kUlpBins - 1
+                             : kRatioBins + 31 - __builtin_clz(2u * dist + 1u);
+        atomicAdd(col + 64 * ubin, 1u);
+      }
+    }
+  };
+  // Any other step, pair by pair in binary64 (pairs from w1 on are skipped).
+  auto elem_step = [&](const p32x4 &cq, const p32x4 &rq, uint32_t o0) {
     bool cand_any = false;
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       const float cf = pdec<DT>(cq, j), rf = pdec<DT>(rq, j);
-      const bool fin = i0 + j < w1 && __builtin_fabsf(cf) <= 3.40282347e38f &&
+      const bool fin = o0 + (uint32_t)j < ow1 && __builtin_fabsf(cf) <= 3.40282347e38f &&
                        __builtin_fabsf(rf) <= 3.40282347e38f;
       if (!fin) continue;
       ++n_pairs;
@@ -968,15 +1042,14 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
         n_zt += d > 0.0 ? 1u : 0u;
       } else if (fail || T < 0.0 || __builtin_fma(-T, tt, d) > 0.0) {
         const double qr = d / tt;
-        if (qr > lb || li == 0xffffffffu) {
+        if (qr > lb || li == kNoOff) {
           lb = qr;
           li = o0 + (uint32_t)j;
           cand_any = true;
         }
         if (fail) {
           const int e = (int)((__double_as_longlong(qr) >> 52) & 0x7ff) - 1023;  // qr >= 1
-          const int bin = min(e, kRatioBins - 1);
-          atomicAdd(row + (bin >> 2), 1u << ((bin & 3) * 8));
+          atomicAdd(col + 64 * min(e, kRatioBins - 1), 1u);
         }
       }
       const uint32_t hc = grid_bits<DT>(cq, j), hr = grid_bits<DT>(rq, j);
@@ -985,61 +1058,100 @@ __device__ void np_chunk(NpLds &s, const NpCase &C, uint64_t c0, uint64_t c1, ui
       const int kr = (hr & 0x8000u) ? -(int)(hr & 0x7fffu) : (int)(hr & 0x7fffu);
       const uint32_t dist = (uint32_t)abs(kc - kr);
       const int ub = inside ? (dist == 0 ? 0 : 32 - __builtin_clz(dist)) : kUlpBins - 1;
-      const int ubin = kRatioBins + ub;
-      atomicAdd(row + (ubin >> 2), 1u << ((ubin & 3) * 8));
+      atomicAdd(col + 64 * (kRatioBins + ub), 1u);
       if (fail) mu = max(mu, inside ? dist : 0xffffffffu);
     }
     if (__ballot(cand_any) != 0) {  // raise the wave threshold
-      T = wave_max_d(li == 0xffffffffu ? -1.0 : lb);
+      T = wave_max_d(li == kNoOff ? -1.0 : lb);
       tm = T >= 1.0 ? 1.0f : np_f32_below(T - T * 0x1p-20);
+      const double mt = T >= 1.0 ? 1.0 : T;
+      am = np_f32_below(mt * atol - mt * atol * 0x1p-20);
+      rm = np_f32_below(mt * rtol - mt * rtol * 0x1p-20);
+    }
+  };
+  // The full steps through buffer resources over the wave's range (as the
+  // probe's), each step's loads issued one step ahead; runs of usual steps
+  // take an inner loop of their own.
+  const uint32_t nst = vec ? (uint32_t)((w1 - w0) / ITER) : 0u;
+  if (nst > 0) {
+    constexpr uint32_t SB = ITER * ES;  // bytes per step and tensor
+    const uint32_t last = (nst - 1) * SB;
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(C.cand + w0 * ES), (short)0, (int)(nst * SB), kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(C.ref + w0 * ES), (short)0, (int)(nst * SB), kBufferWord3);
+    const uint32_t loff = lane * 16u;
+    const uint32_t ol = (uint32_t)(w0 - c0) + lane * (uint32_t)V;
+    uint32_t k = 0;
+    p32x4 cn = bload16(rc, loff, 0u), rn = bload16(rr, loff, 0u);
+    while (true) {
+      p32x4 cq = cn, rq = rn;
+      cn = bload16(rc, loff, min(k + SB, last));
+      rn = bload16(rr, loff, min(k + SB, last));
+      bool usual = T >= 0.0 && is_usual(cq, rq);
+      while (usual) {
+        usual_step(cq, rq);
+        k += SB;
+        if (k > last) break;
+        cq = cn;
+        rq = rn;
+        cn = bload16(rc, loff, min(k + SB, last));
+        rn = bload16(rr, loff, min(k + SB, last));
+        usual = is_usual(cq, rq);
+      }
+      if (usual) break;  // (past the last step)
+      elem_step(cq, rq, ol + k / ES);
+      k += SB;
+      if (k > last) break;
     }
   }
-  // histograms: thread t sums bin t % 64 (52 used) over the rows of lanes
-  // (t / 64) * 64 .. + 63, then the four partial sums in order
-  __syncthreads();
-  const uint32_t bin = t & 63u, part = t >> 6;
-  uint32_t h = 0;
-  if (bin < (uint32_t)(kRatioBins + kUlpBins))
-    for (uint32_t l = part * 64; l < part * 64 + 64; ++l)
-      h += (s.hist[l * kNpRowWords + (bin >> 2)] >> ((bin & 3) * 8)) & 0xffu;
-  __syncthreads();
-  s.c[0][t] = h;
-  __syncthreads();
-  if (t < (uint32_t)(kRatioBins + kUlpBins)) {
-    const uint32_t tot =
-        (uint32_t)(s.c[0][t] + s.c[0][t + 64] + s.c[0][t + 128] + s.c[0][t + 192]);
-    if (t < (uint32_t)kRatioBins) rec->ratio_hist[t] = tot;
-    else rec->ulp_hist[t - kRatioBins] = tot;
+  for (uint64_t b = w0 + (uint64_t)nst * ITER; b < w1; b += ITER) {
+    const uint64_t i0 = b + (uint64_t)lane * V;
+    const p32x4 cq = pload_guarded<DT>(C.cand, i0, w1);
+    const p32x4 rq = pload_guarded<DT>(C.ref, i0, w1);
+    elem_step(cq, rq, (uint32_t)(i0 - c0));
   }
+  n_pairs += V * n_usual;
+  // histograms: thread t < 200 sums the columns 16 q .. 16 q + 15 of slot
+  // t / 4 (q = t % 4), and a quad's four sums are added by DPP
   __syncthreads();
+  {
+    const uint32_t slot = t >> 2;
+    uint32_t h = 0;
+    if (slot < (uint32_t)kNpSlots) {
+      const p32x4 *src = (const p32x4 *)(s.hist + 64 * slot + 16 * (t & 3u));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const p32x4 v = src[k];
+        h += (v[0] + v[1]) + (v[2] + v[3]);
+      }
+    }
+    h += __builtin_amdgcn_update_dpp(0u, h, 0xb1, 0xf, 0xf, false);  // quad_perm 1,0,3,2
+    h += __builtin_amdgcn_update_dpp(0u, h, 0x4e, 0xf, 0xf, false);  // quad_perm 2,3,0,1
+    if ((t & 3u) == 0 && slot < (uint32_t)kNpSlots) {
+      if (slot < (uint32_t)kRatioBins) rec->ratio_hist[slot] = h;
+      else rec->ulp_hist[slot - kRatioBins] = h;
+    }
+  }
+  __syncthreads();  // the columns are dead from here: the partials reuse them
   s.c[0][t] = n_pairs;
   s.c[1][t] = n_fail;
   s.c[2][t] = n_zt;
   s.mv[t] = lb;
-  s.mi[t] = li == 0xffffffffu ? -1 : (int64_t)(c0 + li);
+  s.mo[t] = li;
   s.mu[t] = mu;
-  NpRec r;
-  np_reduce_tree(s, r);
-  if (t == 0) {
-    rec->n_pairs = r.n_pairs;
-    rec->n_fail = r.n_fail;
-    rec->n_zero_tol = r.n_zero_tol;
-    rec->max_ratio = r.max_ratio;
-    rec->argmax_ratio = r.argmax_ratio;
-    rec->max_ulp_fail = r.max_ulp_fail;
-    rec->pad0 = 0;
-  }
+  np_chunk_reduce(s, c0, rec);
 }
 
 __global__ __launch_bounds__(kPThreads) void nearpass_kernel(const NpParams P) {
-  __shared__ NpLds s;
+  __shared__ NpChunkLds s;
   const uint64_t chunk = blockIdx.x;
   if (threadIdx.x < 64) {
     const uint32_t ci = find_first(P.chunk_first, (uint32_t)P.n_cases, chunk);
     if (threadIdx.x == 0) s.item = ci;
   }
   __syncthreads();
-  const NpCase C = P.cases[s.item];
+  const NpCase C = P.cases[__builtin_amdgcn_readfirstlane(s.item)];
   const uint64_t CH = 4ull * P.unit;
   const uint64_t c0 = (chunk - C.chunk_begin) * CH;
   const uint64_t c1 = max(c0, min(c0 + CH, C.numel));

@@ -156,3 +156,44 @@ def test_nearpass_usual_steps_tolerance_boundary(atol, rtol):
     # of the planted boundary pairs, and some of them fail
     last = res[-1]
     assert last["n_fail"] > 0 and last["argmax_ratio"] in set(pos.tolist())
+
+
+def test_nearpass_largest_unit():
+    """Cases totalling 2^29 pairs take the largest wave range (32768 pairs:
+    64 full steps per wave through the inner usual-step loop, each step's
+    loads one step ahead) and chunks of 131072 pairs; each case of 2^27
+    pairs spans four merge groups. Most pairs are equal, a sparse few
+    perturbed; a late new largest ratio below 1 (c = 1 + 2^-9 against 1:
+    0.977 in binary16 and binary32, equal in bfloat16) and its exact tie, a
+    late failure, zeros of both signs and a late infinity sit in every
+    case."""
+    import torch
+
+    rng = np.random.default_rng(2608_74)
+    n = 1 << 27
+    atol, rtol = 1e-3, 1e-3
+    cases = []
+    for dt in (oracle.F16, oracle.F16, oracle.BF16, oracle.F32):
+        r = rng.uniform(0.5, 2.0, n).astype(np.float32)
+        r[rng.random(n) < 0.5] *= -1
+        c = r.copy()
+        pert = rng.choice(n, n // 10000, replace=False)
+        c[pert] = r[pert] * (1 + 3e-4 * rng.standard_normal(pert.size)).astype(np.float32)
+        zeros = rng.choice(n, n // 50, replace=False)
+        r[zeros], c[zeros] = -0.0, 0.0
+        late = n - 6 * 131072 + 1001
+        r[[late, late + 4096]] = 1.0
+        c[[late, late + 4096]] = np.float32(1.0 + 2.0 ** -9)
+        r[n - 3 * 131072 + 5], c[n - 3 * 131072 + 5] = 1.0, 1.5  # a late failure
+        c[n - 17] = np.inf
+        cases.append((_store(c, dt), _store(r, dt), dt))
+    print("nearpass largest unit: %d cases of %d pairs" % (len(cases), n), flush=True)
+    res = vc.vcheck_nearpass([(_tensor(torch, cr, dt), _tensor(torch, rr, dt))
+                              for cr, rr, dt in cases], atol, rtol)
+    for (cr, rr, dt), got in zip(cases, res):
+        want = oracle.nearpass(_view(cr, dt), _view(rr, dt), dt, atol, rtol)
+        for k in ("numel", "n_pairs", "n_fail", "n_zero_tol", "argmax_ratio", "max_ulp_fail",
+                  "ratio_hist", "ulp_hist"):
+            assert got[k] == want[k], (dt, k, got[k], want[k])
+        assert np.float64(got["max_ratio"]).tobytes() == np.float64(want["max_ratio"]).tobytes()
+        assert got["n_fail"] > 0
