@@ -84,7 +84,22 @@ def algorithmic_bytes(w, classes=None):
     return b
 
 
-def time_sweep(sw, steps, warmup, flush):
+def prewarm(launch, seconds):
+    """Untimed calls for about `seconds` before a measurement, so that the
+    GPU's clocks have left the idle state (the CPU baseline or a workload's
+    generation may precede it); nothing of it enters a timed region."""
+    import torch
+
+    if seconds <= 0:
+        return
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(4):
+            launch()
+        torch.cuda.synchronize()
+
+
+def time_sweep(sw, steps, warmup, flush, prewarm_s=0.0):
     """`steps` pairs of calls, the Infinity Cache flushed before every call:
     the first call of a pair is timed whole (events around the call only),
     the second has the streaming kernels timed alone (events the library
@@ -93,6 +108,7 @@ def time_sweep(sw, steps, warmup, flush):
     import torch
     from paper_2608_02712_amd import vcheck as vc
 
+    prewarm(sw.launch, prewarm_s)
     for _ in range(warmup):
         sw.launch()
     torch.cuda.synchronize()
@@ -118,7 +134,7 @@ def time_sweep(sw, steps, warmup, flush):
     return call_ms, main_ms, wall
 
 
-def measure(cfg, steps, warmup, flush):
+def measure(cfg, steps, warmup, flush, prewarm_s=0.0):
     import torch
 
     import workloads as wl
@@ -130,7 +146,7 @@ def measure(cfg, steps, warmup, flush):
     log("workload %d (%s) generated in %.1f s" % (cfg, w.name, time.perf_counter() - t))
     sw = vc.Sweep([(c.cand, c.ref, c.inputs) for c in w.cases], w.tols, primary=w.primary,
                   tile=w.tile, k=w.k or 0, integrity=w.integrity)
-    call_ms, main_ms, wall = time_sweep(sw, steps, warmup, flush)
+    call_ms, main_ms, wall = time_sweep(sw, steps, warmup, flush, prewarm_s)
     res = sw.results()
     ms = call_ms[len(call_ms) // 2]
     main_avg = sum(main_ms) / len(main_ms)
@@ -156,13 +172,14 @@ def measure(cfg, steps, warmup, flush):
         "main_kernel_gbps": round(alg / (main_avg * 1e-3) / 1e9, 2),
         "match_rate": [float(x) for x in res["match_rate"]],
         "wall_s_timed_loop": round(wall, 3),
+        "prewarm_s": prewarm_s,
     }
     log("workload %d: %.3f ms/call, %.1f GB/s (%.1f%% of peak), main kernel %.3f ms" % (
         cfg, ms, out["gbps"], out["pct_hbm_peak"], main_avg))
     return w, out
 
 
-def measure_probe(w, steps, warmup, flush):
+def measure_probe(w, steps, warmup, flush, prewarm_s=0.0):
     """The tensor-statistics probe over every cand and ref tensor of workload
     w in one call (the tensors of a batch of pipeline-boundary probes): call
     time per step (events around the call, cache flushed before it) and the
@@ -175,6 +192,7 @@ def measure_probe(w, steps, warmup, flush):
 
     tensors = [t for c in w.cases for t in (c.cand, c.ref)]
     ts = vc.TensorStats(tensors)
+    prewarm(ts.launch, prewarm_s)
     for _ in range(warmup):
         ts.launch()
     torch.cuda.synchronize()
@@ -219,13 +237,14 @@ def measure_probe(w, steps, warmup, flush):
         "stream_kernel_ms": round(kern, 5),
         "stream_kernel_gbps": round(nbytes / (kern * 1e-3) / 1e9, 2),
         "oracle_one_thread_gbps": round(done / spent / 1e9, 4),
+        "prewarm_s": prewarm_s,
     }
     log("probe: %.3f ms/call, %.1f GB/s (%.1f%% of peak), streaming kernel %.3f ms" % (
         call, out["gbps"], out["pct_hbm_peak"], kern))
     return out
 
 
-def measure_nearpass(w, steps, warmup, flush):
+def measure_nearpass(w, steps, warmup, flush, prewarm_s=0.0):
     """Near-pass statistics over every case of workload w at its primary
     tolerance pair, one call: call time (events around the call, cache
     flushed before it) and the streaming kernel's time."""
@@ -237,6 +256,7 @@ def measure_nearpass(w, steps, warmup, flush):
 
     atol, rtol = w.tols[w.primary][:2]
     npass = vc.NearPass([(c.cand, c.ref) for c in w.cases], atol, rtol)
+    prewarm(npass.launch, prewarm_s)
     for _ in range(warmup):
         npass.launch()
     torch.cuda.synchronize()
@@ -281,13 +301,14 @@ def measure_nearpass(w, steps, warmup, flush):
         "stream_kernel_gbps": round(nbytes / (kern * 1e-3) / 1e9, 2),
         "fp16_ceiling_cases": sum(1 for d in res if d["fp16_ceiling"]),
         "oracle_one_thread_gbps": round(done / spent / 1e9, 4),
+        "prewarm_s": prewarm_s,
     }
     log("near-pass: %.3f ms/call, %.1f GB/s (%.1f%% of peak), streaming kernel %.3f ms" % (
         call, out["gbps"], out["pct_hbm_peak"], kern))
     return out
 
 
-def measure_hash(w, steps, warmup, flush):
+def measure_hash(w, steps, warmup, flush, prewarm_s=0.0):
     """Content hashes of every cand and ref tensor of workload w, one call
     (the evidence of a full-coverage evaluation): call time, events around
     the call, cache flushed before it."""
@@ -299,6 +320,7 @@ def measure_hash(w, steps, warmup, flush):
 
     tensors = [t for c in w.cases for t in (c.cand, c.ref)]
     ch = vc.ContentHash(tensors)
+    prewarm(ch.launch, prewarm_s)
     for _ in range(warmup):
         ch.launch()
     torch.cuda.synchronize()
@@ -328,6 +350,7 @@ def measure_hash(w, steps, warmup, flush):
         "gbps": round(nbytes / (call * 1e-3) / 1e9, 2),
         "pct_hbm_peak": round(100.0 * nbytes / (call * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
         "oracle_one_thread_gbps": round(done / spent / 1e9, 4),
+        "prewarm_s": prewarm_s,
     }
     log("content hash: %.3f ms/call, %.1f GB/s (%.1f%% of peak)" % (
         call, out["gbps"], out["pct_hbm_peak"]))
@@ -539,6 +562,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--prewarm-s", type=float, default=0.3,
+                    help="untimed calls for this many seconds before each workload other than the "
+                         "first measured (and before the probe, near-pass and hash lines); the "
+                         "first keeps exactly --warmup untimed calls")
     ap.add_argument("--headline-only", action="store_true",
                     help="only the headline workload (and the CPU baseline)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -601,21 +628,23 @@ def main():
     cpu = None if args.no_cpu else cpu_baseline(w, args.cpu_seconds, host)
     probe = nearpass = chash = None
     if args.only and args.diag:
-        probe = measure_probe(w, args.steps, args.warmup, flush)
-        nearpass = measure_nearpass(w, args.steps, args.warmup, flush)
-        chash = measure_hash(w, args.steps, args.warmup, flush)
+        pw = args.prewarm_s
+        probe = measure_probe(w, args.steps, args.warmup, flush, pw)
+        nearpass = measure_nearpass(w, args.steps, args.warmup, flush, pw)
+        chash = measure_hash(w, args.steps, args.warmup, flush, pw)
     del w
     torch.cuda.empty_cache()
     if not args.only and not args.headline_only:
-        wd, r = measure(DIAG_WORKLOAD, args.steps, args.warmup, flush)
+        pw = args.prewarm_s
+        wd, r = measure(DIAG_WORKLOAD, args.steps, args.warmup, flush, pw)
         results[DIAG_WORKLOAD] = r
-        probe = measure_probe(wd, args.steps, args.warmup, flush)
-        nearpass = measure_nearpass(wd, args.steps, args.warmup, flush)
-        chash = measure_hash(wd, args.steps, args.warmup, flush)
+        probe = measure_probe(wd, args.steps, args.warmup, flush, pw)
+        nearpass = measure_nearpass(wd, args.steps, args.warmup, flush, pw)
+        chash = measure_hash(wd, args.steps, args.warmup, flush, pw)
         del wd
         torch.cuda.empty_cache()
         for cfg in (1, 3, 4):
-            wk, r = measure(cfg, args.steps, args.warmup, flush)
+            wk, r = measure(cfg, args.steps, args.warmup, flush, pw)
             results[cfg] = r
             del wk
             torch.cuda.empty_cache()
